@@ -1,0 +1,327 @@
+"""Seeded synthetic inputs for block-verify attention and speculative acceptance.
+
+This module only draws random numbers and lays them out; it holds none of the
+arithmetic of the method (no attention, no softmax, no acceptance test).  Both
+the HIP path and the CPU oracle read the inputs it produces.
+
+Shapes follow the workloads the speculative step runs on: a diffusion drafter
+proposes a block of B tokens per sequence in one pass and the target model
+verifies the block in parallel (Sec. 2.1); the block size is picked once per
+prompt from a small window around the training block size (Sec. 2.2, Finding II;
+Sec. 2.4, Eq. 9), so the per-step kernels see ragged B across a batch.
+
+Random streams: numpy PCG64 with ``SeedSequence(seed).spawn(9)`` sub-streams in
+the order [ctx, B, q, K, V, target logits, draft noise, draft sampling,
+uniforms].  fp32 draws are rounded to bf16 with round-to-nearest-even (torch's
+cast) when the workload is bf16; both sides read the same rounded values.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import Optional
+
+import numpy as np
+import torch
+
+MASK_CAUSAL_IN_BLOCK = 0
+MASK_BIDIR_IN_BLOCK = 1
+
+_STREAMS = ["ctx", "B", "q", "K", "V", "target", "noise", "draft", "uniforms"]
+
+
+def _streams(seed: int) -> dict:
+    kids = np.random.SeedSequence(seed).spawn(len(_STREAMS))
+    return {name: np.random.Generator(np.random.PCG64(k)) for name, k in zip(_STREAMS, kids)}
+
+
+def _to_dtype(x: np.ndarray, dtype: str) -> torch.Tensor:
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    if dtype == "bf16":
+        return t.to(torch.bfloat16)
+    if dtype == "f32":
+        return t
+    raise ValueError(f"unknown dtype {dtype!r}")
+
+
+def offsets_from_lens(block_lens: np.ndarray) -> np.ndarray:
+    """Exclusive prefix sum of the block lengths: row range of sequence s is [off[s], off[s+1])."""
+    off = np.zeros(len(block_lens) + 1, dtype=np.int32)
+    off[1:] = np.cumsum(block_lens, dtype=np.int64).astype(np.int32)
+    return off
+
+
+@dataclass
+class AttnProblem:
+    """One block-attention call.
+
+    q, out: [sum(B), Hq, D] packed ragged rows; k_cache, v_cache: [S, Hkv, Lmax, D]
+    with the block's own keys/values already written at [ctx_s, ctx_s + B_s).
+    Cache rows at or beyond ctx_s + B_s hold ``tail_fill`` (NaN by default) so a
+    read past the valid region poisons the output instead of passing silently.
+    """
+    S: int
+    Hq: int
+    Hkv: int
+    D: int
+    Lmax: int
+    ctx_lens: np.ndarray
+    block_lens: np.ndarray
+    q_offsets: np.ndarray
+    q: torch.Tensor
+    k_cache: torch.Tensor
+    v_cache: torch.Tensor
+    dtype: str
+    mask_mode: int
+    scale: float = 0.0  # 0 means 1/sqrt(D)
+    name: str = ""
+
+    @property
+    def total_q(self) -> int:
+        return int(self.q_offsets[-1])
+
+    @property
+    def max_ctx(self) -> int:
+        return int(self.ctx_lens.max()) if self.S else 0
+
+    @property
+    def max_block(self) -> int:
+        return int(self.block_lens.max()) if self.S else 0
+
+    def kv_bytes(self) -> int:
+        """Algorithmic K+V bytes: one read of every key/value row a query can see."""
+        e = 2 if self.dtype == "bf16" else 4
+        rows = int((self.ctx_lens.astype(np.int64) + self.block_lens).sum())
+        return rows * self.Hkv * self.D * 2 * e
+
+    def qo_bytes(self) -> int:
+        e = 2 if self.dtype == "bf16" else 4
+        return 2 * self.total_q * self.Hq * self.D * e
+
+    def flops(self) -> int:
+        """Upper bound 4*D flop per (query row, visible-or-masked key) pair, as priced in the roofline."""
+        return int(sum(self.Hq * int(b) * (int(c) + int(b)) * 4 * self.D
+                       for c, b in zip(self.ctx_lens, self.block_lens)))
+
+
+@dataclass
+class AcceptProblem:
+    """One acceptance call.
+
+    target: [sum(B), V] -- row off[s]+i is the target's next-token logits after block position i.
+    draft:  [sum(B)-S, V] -- row off[s]-s+j is the drafter's logits for block position j+1 (j < B_s-1).
+    draft_tokens: [sum(B)-S] int32, the drafted tokens, paired with target row j.
+    uniforms: [sum(B)] fp32 in [0,1): slot off[s]+j drives acceptance test j, slot off[s]+B_s-1 the final sample.
+    """
+    S: int
+    V: int
+    block_lens: np.ndarray
+    q_offsets: np.ndarray
+    target: torch.Tensor
+    draft: Optional[torch.Tensor]
+    draft_tokens: np.ndarray
+    uniforms: np.ndarray
+    temperature: float
+    dtype: str
+    name: str = ""
+
+    @property
+    def total_q(self) -> int:
+        return int(self.q_offsets[-1])
+
+    @property
+    def max_block(self) -> int:
+        return int(self.block_lens.max()) if self.S else 0
+
+    def logit_bytes(self) -> int:
+        """Algorithmic bytes: one read of every target row, plus every draft row when T > 0."""
+        e = 2 if self.dtype == "bf16" else 4
+        rows = self.total_q + ((self.total_q - self.S) if self.temperature > 0 else 0)
+        return rows * self.V * e
+
+
+@dataclass
+class Workload:
+    name: str
+    attn: Optional[AttnProblem]
+    accept: dict = field(default_factory=dict)  # temperature -> AcceptProblem
+
+    def verified_draft_tokens(self) -> int:
+        p = self.attn
+        return int((p.block_lens.astype(np.int64) - 1).clip(min=0).sum())
+
+
+# --------------------------------------------------------------------------- #
+# generic builders
+# --------------------------------------------------------------------------- #
+
+def make_attn(rs: dict, *, S, Hq, Hkv, D, ctx_lens, block_lens, dtype, mask_mode, Lmax=None,
+              tail_fill=float("nan"), block_key_gain=1.0, q_gain=1.0, name="") -> AttnProblem:
+    """Attention inputs: q, K, V ~ N(0,1) (times the optional gains), cast to ``dtype``.
+
+    ``block_key_gain`` scales the in-block keys [ctx, ctx+B) and ``q_gain`` the
+    queries; gains > 1 make in-block scores dominate so that an off-by-one in the
+    in-block mask moves the output by far more than the bf16 tolerance.
+    """
+    ctx_lens = np.asarray(ctx_lens, dtype=np.int32)
+    block_lens = np.asarray(block_lens, dtype=np.int32)
+    if Lmax is None:
+        Lmax = int((ctx_lens + block_lens).max()) if S else 1
+    off = offsets_from_lens(block_lens)
+    tq = int(off[-1])
+    q = rs["q"].standard_normal((tq, Hq, D), dtype=np.float32) * np.float32(q_gain)
+    k = np.full((S, Hkv, Lmax, D), tail_fill, dtype=np.float32)
+    v = np.full((S, Hkv, Lmax, D), tail_fill, dtype=np.float32)
+    for s in range(S):
+        n = int(ctx_lens[s] + block_lens[s])
+        k[s, :, :n] = rs["K"].standard_normal((Hkv, n, D), dtype=np.float32)
+        v[s, :, :n] = rs["V"].standard_normal((Hkv, n, D), dtype=np.float32)
+        if block_key_gain != 1.0:
+            c = int(ctx_lens[s])
+            k[s, :, c:n] *= np.float32(block_key_gain)
+    return AttnProblem(S=S, Hq=Hq, Hkv=Hkv, D=D, Lmax=Lmax, ctx_lens=ctx_lens, block_lens=block_lens,
+                       q_offsets=off, q=_to_dtype(q, dtype), k_cache=_to_dtype(k, dtype),
+                       v_cache=_to_dtype(v, dtype), dtype=dtype, mask_mode=mask_mode, name=name)
+
+
+def _gumbel_argmax(rs_draft, logits: np.ndarray, temperature: float) -> np.ndarray:
+    """Sample one token per row from the drafter: argmax at T=0 (lowest index on ties),
+    else the Gumbel-max draw argmax(logits/T + G), which is distributed as the drafter's
+    softmax at temperature T without forming the softmax."""
+    if temperature == 0:
+        return np.argmax(logits, axis=1).astype(np.int32)
+    out = np.empty(logits.shape[0], dtype=np.int32)
+    for r in range(logits.shape[0]):
+        g = rs_draft.gumbel(size=logits.shape[1])
+        out[r] = int(np.argmax(logits[r].astype(np.float64) / temperature + g))
+    return out
+
+
+def make_accept(rs: dict, *, block_lens, V, dtype, temperature, target_sigma, noise_sigma,
+                name="", draft_logits_needed=None) -> AcceptProblem:
+    """Acceptance inputs: target ~ N(0, target_sigma^2); draft row j = target row j + N(0, noise_sigma^2);
+    draft tokens drawn from the drafter at ``temperature``; fp32 uniforms in [0,1)."""
+    block_lens = np.asarray(block_lens, dtype=np.int32)
+    S = len(block_lens)
+    off = offsets_from_lens(block_lens)
+    tq = int(off[-1])
+    nd = tq - S
+    target = rs["target"].standard_normal((tq, V), dtype=np.float32) * np.float32(target_sigma)
+    t_dt = _to_dtype(target, dtype)
+    t_vals = t_dt.float().numpy()
+    draft = np.empty((nd, V), dtype=np.float32)
+    for s in range(S):
+        for j in range(int(block_lens[s]) - 1):
+            draft[off[s] - s + j] = t_vals[off[s] + j] + \
+                rs["noise"].standard_normal(V, dtype=np.float32) * np.float32(noise_sigma)
+    d_dt = _to_dtype(draft, dtype)
+    d_vals = d_dt.float().numpy()
+    tokens = _gumbel_argmax(rs["draft"], d_vals, temperature)
+    uniforms = rs["uniforms"].random(tq, dtype=np.float32)
+    if draft_logits_needed is None:
+        draft_logits_needed = temperature > 0
+    return AcceptProblem(S=S, V=V, block_lens=block_lens, q_offsets=off, target=t_dt,
+                         draft=d_dt if draft_logits_needed else None, draft_tokens=tokens,
+                         uniforms=uniforms, temperature=float(temperature), dtype=dtype, name=name)
+
+
+# --------------------------------------------------------------------------- #
+# the five workloads
+# --------------------------------------------------------------------------- #
+
+RAGGED_BLOCK_SET = np.array([8, 10, 12, 14, 16, 18, 20, 24], dtype=np.int32)
+
+
+def _nearest_in_set(draws: np.ndarray, allowed: np.ndarray) -> np.ndarray:
+    """Element of ``allowed`` nearest to each draw; ties go to the smaller element."""
+    d = np.abs(draws[:, None] - allowed[None, :].astype(np.float64))
+    return allowed[np.argmin(d, axis=1)]  # argmin keeps the first (smaller) on ties
+
+
+def c1_tiny(temperatures=(0.0, 1.0), seed=1001) -> Workload:
+    """Tiny CPU-checkable step: 1 sequence, 4 q heads / 1 kv head, D=64, fp32, ctx 256, B=8,
+    causal-in-block; acceptance over V=1024 with target ~ N(0,2^2), draft = target + N(0,0.5^2)."""
+    out = Workload(name="tiny_fp32_ctx256_B8_V1024", attn=None)
+    rs = _streams(seed)
+    out.attn = make_attn(rs, S=1, Hq=4, Hkv=1, D=64, ctx_lens=[256], block_lens=[8], dtype="f32",
+                         mask_mode=MASK_CAUSAL_IN_BLOCK, name=out.name)
+    for T in temperatures:
+        rs = _streams(seed)
+        out.accept[T] = make_accept(rs, block_lens=[8], V=1024, dtype="f32", temperature=T,
+                                    target_sigma=2.0, noise_sigma=0.5, name=out.name)
+    return out
+
+
+def c2_qwen3_4b_verify(temperatures=(1.0,), seed=1002, dtype="bf16") -> Workload:
+    """Qwen3-4B-shaped verify step: 1 sequence, 32/8 heads, D=128, bf16, ctx 2048, B=16, causal;
+    acceptance over V=151936 with target ~ N(0,3^2), draft = target + N(0,1)."""
+    out = Workload(name="qwen3_4b_verify_S1_ctx2048_B16", attn=None)
+    rs = _streams(seed)
+    out.attn = make_attn(rs, S=1, Hq=32, Hkv=8, D=128, ctx_lens=[2048], block_lens=[16], dtype=dtype,
+                         mask_mode=MASK_CAUSAL_IN_BLOCK, name=out.name)
+    for T in temperatures:
+        rs = _streams(seed)
+        out.accept[T] = make_accept(rs, block_lens=[16], V=151936, dtype=dtype, temperature=T,
+                                    target_sigma=3.0, noise_sigma=1.0, name=out.name)
+    return out
+
+
+def c3_block_lens(seed=1003, S=8) -> np.ndarray:
+    rs = _streams(seed)
+    draws = rs["B"].normal(16.0, 3.0, size=S)
+    return _nearest_in_set(draws, RAGGED_BLOCK_SET).astype(np.int32)
+
+
+def c3_ragged(temperatures=(0.0, 1.0), seed=1003, dtype="bf16", S=8, ctx=4096, vocab=151936,
+              with_attn=True) -> Workload:
+    """Instance-adaptive ragged blocks: 8 sequences, Qwen3-4B attention shape (32/8/128), bf16,
+    ctx 4096 each, B_s from {8,..,24} nearest to N(16,3^2); causal; acceptance over V=151936."""
+    out = Workload(name="qwen3_4b_ragged_S8_ctx4096_B8-24", attn=None)
+    B = c3_block_lens(seed, S)
+    if with_attn:
+        rs = _streams(seed)
+        out.attn = make_attn(rs, S=S, Hq=32, Hkv=8, D=128, ctx_lens=[ctx] * S, block_lens=B, dtype=dtype,
+                             mask_mode=MASK_CAUSAL_IN_BLOCK, Lmax=ctx + int(RAGGED_BLOCK_SET.max()),
+                             name=out.name)
+    for T in temperatures:
+        rs = _streams(seed)
+        out.accept[T] = make_accept(rs, block_lens=B, V=vocab, dtype=dtype, temperature=T,
+                                    target_sigma=3.0, noise_sigma=1.0, name=out.name)
+    return out
+
+
+def c4_drafter(seed=1004, dtype="bf16", S=16) -> Workload:
+    """Drafter block-diffusion pass: 16 sequences, 32/8/128, bf16, ctx ~ U{1024..8192},
+    B ~ U{8..32}, bidirectional-in-block; no acceptance."""
+    rs = _streams(seed)
+    ctx = rs["ctx"].integers(1024, 8192, endpoint=True, size=S).astype(np.int32)
+    B = rs["B"].integers(8, 32, endpoint=True, size=S).astype(np.int32)
+    out = Workload(name="drafter_bidir_S16_ctx1k-8k_B8-32", attn=None)
+    out.attn = make_attn(rs, S=S, Hq=32, Hkv=8, D=128, ctx_lens=ctx, block_lens=B, dtype=dtype,
+                         mask_mode=MASK_BIDIR_IN_BLOCK, Lmax=8192 + 32, name=out.name)
+    return out
+
+
+def c5_long_context(temperatures=(1.0,), seed=1005, dtype="bf16", S=32, with_attn=True,
+                    with_accept=True) -> Workload:
+    """Long-context serving step: 32 sequences, Qwen3-8B attention shape (32/8/128), bf16,
+    ctx ~ U{8192..32768}, B ~ U{4..32}, causal; acceptance over V=151936 at T=1."""
+    rs = _streams(seed)
+    ctx = rs["ctx"].integers(8192, 32768, endpoint=True, size=S).astype(np.int32)
+    B = rs["B"].integers(4, 32, endpoint=True, size=S).astype(np.int32)
+    out = Workload(name="qwen3_8b_long_S32_ctx8k-32k_B4-32", attn=None)
+    if with_attn:
+        out.attn = make_attn(rs, S=S, Hq=32, Hkv=8, D=128, ctx_lens=ctx, block_lens=B, dtype=dtype,
+                             mask_mode=MASK_CAUSAL_IN_BLOCK, Lmax=32768 + 32, name=out.name)
+    if with_accept:
+        for T in temperatures:
+            rs = _streams(seed)
+            out.accept[T] = make_accept(rs, block_lens=B, V=151936, dtype=dtype, temperature=T,
+                                        target_sigma=3.0, noise_sigma=1.0, name=out.name)
+    return out
+
+
+def c5_lens(seed=1005, S=32):
+    rs = _streams(seed)
+    ctx = rs["ctx"].integers(8192, 32768, endpoint=True, size=S).astype(np.int32)
+    B = rs["B"].integers(4, 32, endpoint=True, size=S).astype(np.int32)
+    return ctx, B
