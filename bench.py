@@ -1,0 +1,176 @@
+#!/usr/bin/env python3
+"""Benchmark of one speculative verify step on one MI355X: block-verify attention
+(sd_block_attn, one layer) followed by vocabulary-wide acceptance (sd_accept).
+
+Workload: the instance-adaptive ragged-block batch in the Qwen3-4B shape -- 8 sequences,
+32 query / 8 kv heads, head_dim 128, bf16 KV cache with 4096 committed tokens each,
+per-sequence block sizes from {8,10,...,20,24} around the training size 16, causal-in-block
+mask, acceptance over the 151936-token vocabulary at T = 1 (seeded synthetic inputs).
+
+One step = one attention call + one acceptance call over one batch.  Inputs are resident
+in HBM before the timed region; the step cycles through copies of every input whose total
+exceeds 1 GB so the 256 MB Infinity Cache cannot serve them.  Prints one JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--temperature T] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
+METRIC = "verified draft tokens/s + KV/logit HBM GB/s (% of peak), Qwen3-4B shape"
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=500)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--temperature", type=float, default=1.0)
+    ap.add_argument("--copies", type=int, default=0, help="input copies to rotate (0: enough for >= 1 GB)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="bound on the oracle timing")
+    return ap.parse_args()
+
+
+def cpu_baseline(work, T, seconds):
+    """The fp64 oracle on the host cores, on the same step: attention for every block row and
+    head, then acceptance.  Repeated until `seconds` have elapsed (at least once)."""
+    sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+    import oracle
+    a = work.attn
+    acc = work.accept[T]
+    q = a.q.float().numpy()
+    k = a.k_cache.float().numpy()
+    v = a.v_cache.float().numpy()
+    tl = acc.target.float().numpy()
+    dl = acc.draft.float().numpy() if acc.draft is not None else None
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.block_attn(q, k, v, a.ctx_lens, a.block_lens, a.q_offsets, a.mask_mode)
+        oracle.accept(tl, dl, acc.draft_tokens, acc.uniforms, acc.block_lens, acc.q_offsets, T)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or reps >= 20:
+            break
+    per_step = el / reps
+    return {"value": work.verified_draft_tokens() / per_step, "unit": "verified draft tokens/s",
+            "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"the full step (attention for all {a.total_q} block rows x {a.Hq} heads + acceptance of "
+                      f"{a.S} sequences at T={T:g}), {reps} repetition(s), {per_step * 1e3:.1f} ms per step",
+            "ms_per_step": per_step * 1e3}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        return 2
+    import torch
+    import paper_2606_31315_amd as sd
+    from paper_2606_31315_amd import workloads as W
+
+    T = float(args.temperature)
+    temps = tuple(sorted({T}))
+    work = W.c3_ragged(temperatures=temps)
+    a = work.attn
+    acc = work.accept[T]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    attn_bytes = a.kv_bytes() + a.qo_bytes()
+    acc_bytes = acc.logit_bytes()
+    step_bytes = attn_bytes + acc_bytes
+    copies = args.copies or max(2, int(np.ceil(1.0e9 / step_bytes)))
+
+    def upload():
+        d = dict(q=a.q.to(dev), k=a.k_cache.to(dev), v=a.v_cache.to(dev), t=acc.target.to(dev))
+        d["d"] = acc.draft.to(dev) if acc.draft is not None else None
+        return d
+
+    small = dict(ctx=torch.from_numpy(a.ctx_lens).to(dev), bl=torch.from_numpy(a.block_lens).to(dev),
+                 off=torch.from_numpy(a.q_offsets).to(dev),
+                 tok=torch.from_numpy(acc.draft_tokens).to(dev), u=torch.from_numpy(acc.uniforms).to(dev))
+    bufs = [upload() for _ in range(copies)]
+    outs = [torch.empty_like(bufs[0]["q"]) for _ in range(copies)]
+    al = torch.empty(a.S, dtype=torch.int32, device=dev)
+    nt = torch.empty(a.S, dtype=torch.int32, device=dev)
+    ws_attn = torch.zeros(sd.attn_workspace_size(sd.attn_shape(bufs[0]["q"], bufs[0]["k"], a.max_ctx, a.max_block)),
+                          dtype=torch.uint8, device=dev)
+    ws_acc = torch.zeros(sd.accept_workspace_size(sd.accept_shape(bufs[0]["t"], a.S, a.max_block), T),
+                         dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+
+    def step(i, ev=None):
+        b = bufs[i % copies]
+        if ev is not None:
+            ev[0].record()
+        sd.block_attn(b["q"], b["k"], b["v"], small["ctx"], small["bl"], small["off"], a.mask_mode,
+                      max_ctx=a.max_ctx, max_block=a.max_block, out=outs[i % copies], workspace=ws_attn)
+        if ev is not None:
+            ev[1].record()
+        sd.accept(b["t"], b["d"], small["tok"], small["u"], small["bl"], small["off"], T, max_block=a.max_block,
+                  accept_len=al, next_token=nt, workspace=ws_acc)
+        if ev is not None:
+            ev[2].record()
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # timed region: whole steps, with per-call event markers on the launch stream
+    K = args.steps
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(K):
+        step(i, evs[i])
+    stop.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(stop)
+    attn_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    acc_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
+    ms_per_step = total_ms / K
+
+    ntok = work.verified_draft_tokens()
+    value = ntok / (ms_per_step * 1e-3)
+    attn_us, acc_us = attn_ms.mean() * 1e3, acc_ms.mean() * 1e3
+    attn_gbps = attn_bytes / (attn_us * 1e-6) / 1e9
+    acc_gbps = acc_bytes / (acc_us * 1e-6) / 1e9
+    step_gbps = step_bytes / (ms_per_step * 1e-3) / 1e9
+    al_h, nt_h = al.cpu().numpy(), nt.cpu().numpy()
+
+    res = {
+        "metric": METRIC, "value": round(value, 1), "unit": "verified draft tokens/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 6), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": work.name, "num_seqs": a.S, "q_heads": a.Hq, "kv_heads": a.Hkv, "head_dim": a.D,
+                   "ctx": int(a.ctx_lens[0]), "block_lens": [int(b) for b in a.block_lens], "vocab": acc.V,
+                   "temperature": T, "mask": "causal_in_block", "layers_timed": 1, "input_copies": copies},
+        "step_gbps": round(step_gbps, 1), "step_hbm_frac": round(step_gbps / HBM_PEAK_GBPS, 4),
+        "attn_us": round(attn_us, 2), "attn_gbps": round(attn_gbps, 1),
+        "accept_us": round(acc_us, 2), "accept_gbps": round(acc_gbps, 1),
+        "bytes": {"attn": attn_bytes, "accept": acc_bytes, "step": step_bytes},
+        "verify_rows_per_s": round(a.total_q / (ms_per_step * 1e-3), 1),
+        "committed_tokens_per_s": round(float((al_h + 1).sum()) / (ms_per_step * 1e-3), 1),
+        "mean_accept_len": float(al_h.mean()),
+        "roofline": {"bound": "hbm", "kernel": "block_attn_kernel", "achieved": round(attn_gbps, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(work, T, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

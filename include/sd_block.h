@@ -1,0 +1,182 @@
+/*
+ * sd_block.h -- C ABI of libsdblock.so: the per-step hot path of diffusion-based
+ * speculative decoding with instance-adaptive block sizes (BlockPilot,
+ * arXiv 2606.31315), as hand-written HIP kernels for AMD MI355X (gfx950).
+ *
+ * One speculative step drafts a block of B tokens in one block-diffusion forward
+ * pass and the target model verifies the whole block in one parallel forward pass,
+ * accepting the longest consistent prefix (Sec. 2.1; Fig. 1 caption; App. A.1).
+ * The block size is chosen once per prompt and then fixed (Sec. 2.4, Eq. 9), so a
+ * batch carries ragged per-sequence block lengths B_s.  This library provides the
+ * two data-parallel operations of that step:
+ *
+ *   sd_block_attn  block attention of the B_s block rows of every sequence over its
+ *                  GQA key/value cache, causal inside the block (target verify) or
+ *                  bidirectional inside the block (block-diffusion drafter);
+ *   sd_accept      vocabulary-wide speculative acceptance: greedy matching at T = 0,
+ *                  lossless rejection sampling against min(1, p/q) at T > 0, giving
+ *                  the accepted prefix length and the bonus or resampled token.
+ *
+ * Conventions shared by every entry point
+ *   - All array arguments are DEVICE pointers unless stated otherwise; shape
+ *     structs are host pointers.  The caller owns every buffer; the library never
+ *     allocates, frees or retains device memory, and keeps no mutable global state
+ *     except a thread-local error message.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream of the
+ *     current device).  Calls enqueue work and return; they never synchronise.
+ *   - Every call validates its host-side arguments before touching the device and
+ *     returns a status code; it never aborts or prints.  Per-sequence values that
+ *     live in device memory (ctx_lens, block_lens, q_offsets, tokens) cannot be
+ *     checked on the host: values outside the documented ranges are undefined
+ *     behaviour.
+ *   - Workspace: each operation needs a device workspace of the size its
+ *     *_workspace_size() reports.  The workspace must be zero-filled before its
+ *     first use (sd_workspace_init, or any zero-filled allocation); every call
+ *     leaves its counters zero again, so one workspace serves any number of later
+ *     calls of any shape that fits it.  Calls that share a workspace must not
+ *     overlap in time (use one stream, or one workspace per stream).
+ *   - Row-major layouts throughout; "[a, b, c]" lists dimensions outermost first.
+ */
+#ifndef SD_BLOCK_H
+#define SD_BLOCK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes -------------------------------------------------------- */
+enum {
+  SD_OK = 0,
+  SD_ERR_INVALID_ARG = 1, /* null pointer, bad size, misalignment, bad enum */
+  SD_ERR_UNSUPPORTED = 2, /* valid request this build has no kernel for (head_dim, group size) */
+  SD_ERR_WORKSPACE = 3,   /* workspace smaller than *_workspace_size() */
+  SD_ERR_HIP = 4          /* a HIP runtime call or kernel launch failed */
+};
+
+/* ---- element types and masks --------------------------------------------- */
+enum { SD_F32 = 0, SD_BF16 = 1 };
+
+enum {
+  /* Target verification: block row i of sequence s sees keys [0, ctx_s + i]. */
+  SD_MASK_CAUSAL_IN_BLOCK = 0,
+  /* Block-diffusion drafting: every block row of s sees keys [0, ctx_s + B_s). */
+  SD_MASK_BIDIR_IN_BLOCK = 1
+};
+
+/* Thread-local message describing the last non-OK status of this thread. */
+const char *sd_last_error(void);
+
+/* Library version string, e.g. "sdblock 0.1 gfx950". */
+const char *sd_version(void);
+
+/*
+ * Zero-fill `bytes` bytes of device memory at `workspace` on `stream` (a fill
+ * kernel, so it may be recorded into a HIP graph).  `workspace` must be 16-byte
+ * aligned; `bytes` a multiple of 4.
+ */
+int sd_workspace_init(void *workspace, size_t bytes, void *stream);
+
+/* ==========================================================================
+ * Block attention (Sec. 2.1: the drafter generates the B block tokens in parallel
+ * by block-level diffusion; the target verifies the block in parallel).
+ * ========================================================================== */
+typedef struct sd_attn_shape {
+  int32_t num_seqs;     /* S >= 0 */
+  int32_t num_q_heads;  /* Hq >= 1 */
+  int32_t num_kv_heads; /* Hkv >= 1, Hq % Hkv == 0; query head h reads kv head h / (Hq/Hkv) */
+  int32_t head_dim;     /* D: 64 or 128 */
+  int32_t max_kv_len;   /* Lmax: cache rows per (sequence, kv head) */
+  int32_t total_q;      /* sum_s B_s: rows of q and out */
+  int32_t max_ctx;      /* host-known bound: ctx_lens[s] <= max_ctx for every s */
+  int32_t max_block;    /* host-known bound: block_lens[s] <= max_block, 1 <= max_block <= 64 */
+  int32_t dtype;        /* SD_BF16 or SD_F32: element type of q, caches and out */
+  float scale;          /* softmax scale; 0 means 1/sqrt(D) */
+} sd_attn_shape;
+
+/* Workspace bytes sd_block_attn needs for this shape (host-only, no device access). */
+int sd_block_attn_workspace_size(const sd_attn_shape *shape, size_t *bytes);
+
+/*
+ * out[q_offsets[s] + i, h, :] = sum_j softmax_j(scale * q_i,h . K[s, g, j, :]) V[s, g, j, :]
+ * with g = h / (Hq/Hkv) and j ranging over the keys the mask lets block row i see
+ * (causal: j <= ctx_s + i; bidirectional: j < ctx_s + B_s).  Softmax and all sums
+ * are computed in fp32; for bf16 the attention weights are rounded to bf16 before
+ * they multiply V (the output is then rounded to bf16).
+ *
+ *   q, out          [total_q, Hq, D]           dtype; row q_offsets[s] + i is block position i of s
+ *   k_cache,v_cache [S, Hkv, Lmax, D]          dtype; the block's own keys/values must already be
+ *                                              written at rows [ctx_s, ctx_s + B_s); rows at or beyond
+ *                                              ctx_s + B_s are never read
+ *   ctx_lens        [S] int32                  committed context length ctx_s, 0 <= ctx_s <= max_ctx
+ *   block_lens      [S] int32                  block length B_s, 0 <= B_s <= max_block (0: no rows)
+ *   q_offsets       [S + 1] int32              exclusive prefix sum of block_lens, q_offsets[S] = total_q
+ *   mask_mode       SD_MASK_*
+ *   workspace       >= sd_block_attn_workspace_size() bytes, 256-byte aligned, zeroed before first use
+ *
+ * Host-checked preconditions: q, caches and out 16-byte aligned; max_ctx + max_block
+ * <= Lmax; total_q <= S * max_block; (Hq/Hkv) * max_block <= 256.
+ * Errors: SD_ERR_INVALID_ARG, SD_ERR_UNSUPPORTED (head_dim), SD_ERR_WORKSPACE, SD_ERR_HIP.
+ * S == 0 or total_q == 0 returns SD_OK without touching the device.
+ */
+int sd_block_attn(const sd_attn_shape *shape, const void *q, const void *k_cache, const void *v_cache,
+                  const int32_t *ctx_lens, const int32_t *block_lens, const int32_t *q_offsets,
+                  int32_t mask_mode, void *out, void *workspace, size_t workspace_bytes, void *stream);
+
+/* ==========================================================================
+ * Speculative acceptance (Fig. 1 caption: accept the longest consistent prefix;
+ * Sec. 1 and Sec. 3.1: the target's output distribution is preserved exactly).
+ * Block layout: position 0 of a block is the last committed token (the anchor),
+ * positions 1 .. B_s-1 are drafted; so each sequence has B_s target rows,
+ * B_s - 1 draft rows, accept_len in [0, B_s - 1] and one bonus/resampled token.
+ * ========================================================================== */
+typedef struct sd_accept_shape {
+  int32_t num_seqs;  /* S >= 0 */
+  int32_t vocab;     /* V >= 1 */
+  int32_t total_q;   /* sum_s B_s */
+  int32_t max_block; /* host-known bound on B_s, 1 <= max_block <= 64 */
+  int32_t dtype;     /* SD_BF16 or SD_F32: element type of both logit arrays */
+} sd_accept_shape;
+
+/* Workspace bytes sd_accept needs for this shape at this temperature (host-only). */
+int sd_accept_workspace_size(const sd_accept_shape *shape, float temperature, size_t *bytes);
+
+/*
+ *   target_logits [total_q, V]       row q_offsets[s] + i: target logits after block position i
+ *   draft_logits  [total_q - S, V]   row q_offsets[s] - s + j: drafter logits for block position
+ *                                    j + 1, j < B_s - 1 (read only when temperature > 0; may be NULL
+ *                                    at temperature 0)
+ *   draft_tokens  [total_q - S] int32  drafted token of block position j + 1, in [0, V)
+ *   uniforms      [total_q] fp32 in [0, 1): slot q_offsets[s] + j drives acceptance test j;
+ *                                    slot q_offsets[s] + B_s - 1 drives the single final draw
+ *                                    (read only when temperature > 0; may be NULL at 0)
+ *   block_lens    [S] int32          1 <= B_s <= max_block (every block holds at least its anchor)
+ *   q_offsets     [S + 1] int32      exclusive prefix sum of block_lens
+ *   temperature   0: greedy (draft j accepted iff it equals the lowest-index argmax of target
+ *                 row j; next token = argmax of target row accept_len).
+ *                 > 0: p = softmax(target/T), q = softmax(draft/T); draft j accepted iff
+ *                 u_j < p_j(d_j) / q_j(d_j); on the first rejection at j the next token is the
+ *                 inverse-CDF draw (ascending vocabulary order, first token whose cumulative mass
+ *                 exceeds u* times the total) from max(0, p_j - q_j), or from p_j if that
+ *                 residual has no mass; with every draft accepted it is the draw from p_{B_s-1}.
+ *   accept_len    [S] int32 out      number of leading accepted drafts
+ *   next_token    [S] int32 out      bonus or resampled token
+ *
+ * Host-checked preconditions: logits 16-byte aligned; temperature finite and >= 0;
+ * S <= total_q <= S * max_block.  Statistics are fp32 (softmax sums fp32 per thread, fp64
+ * across threads); decisions within about 1e-6 of a boundary may differ from an fp64
+ * evaluation.
+ * Errors: SD_ERR_INVALID_ARG, SD_ERR_WORKSPACE, SD_ERR_HIP.  S == 0 returns SD_OK.
+ */
+int sd_accept(const sd_accept_shape *shape, const void *target_logits, const void *draft_logits,
+              const int32_t *draft_tokens, const float *uniforms, const int32_t *block_lens,
+              const int32_t *q_offsets, float temperature, int32_t *accept_len, int32_t *next_token,
+              void *workspace, size_t workspace_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SD_BLOCK_H */

@@ -1,0 +1,17 @@
+"""MI355X-native hot path of BlockPilot's speculative step (arXiv 2606.31315).
+
+Two operations, both hand-written HIP for gfx950 behind the C ABI in
+include/sd_block.h:
+
+  block_attn  block-verify / block-diffusion attention of ragged blocks over a GQA
+              KV cache (causal-in-block or bidirectional-in-block mask);
+  accept      vocabulary-wide speculative acceptance (greedy at T=0, lossless
+              rejection sampling at T>0) returning accept_len and the next token.
+"""
+from ._lib import (SD_BF16, SD_F32, SD_MASK_BIDIR_IN_BLOCK, SD_MASK_CAUSAL_IN_BLOCK, SdError, Workspace,
+                   accept, accept_shape, accept_workspace_size, attn_shape, attn_workspace_size, block_attn, lib,
+                   version)
+
+__all__ = ["block_attn", "accept", "attn_shape", "accept_shape", "attn_workspace_size", "accept_workspace_size",
+           "Workspace", "SdError", "lib", "version", "SD_BF16", "SD_F32", "SD_MASK_CAUSAL_IN_BLOCK",
+           "SD_MASK_BIDIR_IN_BLOCK"]

@@ -1,0 +1,211 @@
+"""ctypes binding of libsdblock.so: argument marshalling only.
+
+Every step of the computation runs in the HIP kernels behind the C ABI declared in
+include/sd_block.h.  torch is used for device memory and streams.  There is no
+fallback: if the library is missing or a call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsdblock.so")
+
+SD_OK, SD_ERR_INVALID_ARG, SD_ERR_UNSUPPORTED, SD_ERR_WORKSPACE, SD_ERR_HIP = range(5)
+SD_F32, SD_BF16 = 0, 1
+SD_MASK_CAUSAL_IN_BLOCK, SD_MASK_BIDIR_IN_BLOCK = 0, 1
+
+EXPORTS = ["sd_last_error", "sd_version", "sd_workspace_init", "sd_block_attn_workspace_size", "sd_block_attn",
+           "sd_accept_workspace_size", "sd_accept"]
+
+
+class SdAttnShape(ctypes.Structure):
+    _fields_ = [("num_seqs", ctypes.c_int32), ("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("max_kv_len", ctypes.c_int32), ("total_q", ctypes.c_int32),
+                ("max_ctx", ctypes.c_int32), ("max_block", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("scale", ctypes.c_float)]
+
+
+class SdAcceptShape(ctypes.Structure):
+    _fields_ = [("num_seqs", ctypes.c_int32), ("vocab", ctypes.c_int32), ("total_q", ctypes.c_int32),
+                ("max_block", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class SdError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"sdblock error {code}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libsdblock.so (built in-tree by build_lib.py); raise if it is missing."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2606_31315_amd.build_lib` "
+                               "or __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        P, I, Z = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        L.sd_last_error.restype = ctypes.c_char_p
+        L.sd_last_error.argtypes = []
+        L.sd_version.restype = ctypes.c_char_p
+        L.sd_version.argtypes = []
+        L.sd_workspace_init.restype = ctypes.c_int
+        L.sd_workspace_init.argtypes = [P, Z, P]
+        L.sd_block_attn_workspace_size.restype = ctypes.c_int
+        L.sd_block_attn_workspace_size.argtypes = [ctypes.POINTER(SdAttnShape), ctypes.POINTER(Z)]
+        L.sd_block_attn.restype = ctypes.c_int
+        L.sd_block_attn.argtypes = [ctypes.POINTER(SdAttnShape), P, P, P, P, P, P, I, P, P, Z, P]
+        L.sd_accept_workspace_size.restype = ctypes.c_int
+        L.sd_accept_workspace_size.argtypes = [ctypes.POINTER(SdAcceptShape), ctypes.c_float, ctypes.POINTER(Z)]
+        L.sd_accept.restype = ctypes.c_int
+        L.sd_accept.argtypes = [ctypes.POINTER(SdAcceptShape), P, P, P, P, P, P, ctypes.c_float, P, P, P, Z, P]
+        _lib = L
+    return _lib
+
+
+def _check(rc: int) -> None:
+    if rc != SD_OK:
+        raise SdError(rc, lib().sd_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return SD_BF16
+    if t.dtype == torch.float32:
+        return SD_F32
+    raise TypeError(f"unsupported dtype {t.dtype}; use bfloat16 or float32")
+
+
+def _need(t: torch.Tensor, name: str, dtype=None, device=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+
+
+class Workspace:
+    """A zero-initialised device buffer per device, grown on demand.
+
+    The kernels leave their counters zero after every call, so the buffer stays
+    valid across calls; calls sharing it must be ordered (one stream)."""
+
+    def __init__(self):
+        self._bufs = {}
+
+    def get(self, nbytes: int, device: torch.device) -> torch.Tensor:
+        key = device.index if device.index is not None else torch.cuda.current_device()
+        buf = self._bufs.get(key)
+        if buf is None or buf.numel() < nbytes:
+            # 256-byte alignment comes from the caching allocator; zero fill is a torch kernel
+            buf = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=device)
+            self._bufs[key] = buf
+        return buf
+
+
+_default_ws = Workspace()
+
+
+def attn_shape(q: torch.Tensor, k_cache: torch.Tensor, max_ctx: int, max_block: int, scale: float = 0.0
+               ) -> SdAttnShape:
+    S, Hkv, Lmax, D = k_cache.shape
+    return SdAttnShape(S, q.shape[1], Hkv, D, Lmax, q.shape[0], int(max_ctx), int(max_block), _dtype_code(q),
+                       float(scale))
+
+
+def attn_workspace_size(shape: SdAttnShape) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().sd_block_attn_workspace_size(ctypes.byref(shape), ctypes.byref(n)))
+    return n.value
+
+
+def block_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, ctx_lens: torch.Tensor,
+               block_lens: torch.Tensor, q_offsets: torch.Tensor, mask_mode: int, *, max_ctx: int, max_block: int,
+               scale: float = 0.0, out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+               stream=None) -> torch.Tensor:
+    """Block attention (sd_block_attn).  q [total_q, Hq, D]; caches [S, Hkv, Lmax, D];
+    ctx_lens, block_lens [S] and q_offsets [S+1] int32 on the device; max_ctx and
+    max_block are host-known bounds of the device lengths."""
+    dev = q.device
+    _need(q, "q", device=dev)
+    _need(k_cache, "k_cache", q.dtype, dev)
+    _need(v_cache, "v_cache", q.dtype, dev)
+    for name, t in (("ctx_lens", ctx_lens), ("block_lens", block_lens), ("q_offsets", q_offsets)):
+        _need(t, name, torch.int32, dev)
+    if out is None:
+        out = torch.empty_like(q)
+    _need(out, "out", q.dtype, dev)
+    shape = attn_shape(q, k_cache, max_ctx, max_block, scale)
+    nbytes = attn_workspace_size(shape)
+    if workspace is None:
+        workspace = _default_ws.get(nbytes, dev)
+    _check(lib().sd_block_attn(ctypes.byref(shape), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(ctx_lens),
+                               _ptr(block_lens), _ptr(q_offsets), int(mask_mode), _ptr(out), _ptr(workspace),
+                               workspace.numel() * workspace.element_size(), _stream(stream)))
+    return out
+
+
+def accept_shape(target_logits: torch.Tensor, num_seqs: int, max_block: int) -> SdAcceptShape:
+    return SdAcceptShape(int(num_seqs), target_logits.shape[1], target_logits.shape[0], int(max_block),
+                         _dtype_code(target_logits))
+
+
+def accept_workspace_size(shape: SdAcceptShape, temperature: float) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().sd_accept_workspace_size(ctypes.byref(shape), float(temperature), ctypes.byref(n)))
+    return n.value
+
+
+def accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor], draft_tokens: torch.Tensor,
+           uniforms: Optional[torch.Tensor], block_lens: torch.Tensor, q_offsets: torch.Tensor, temperature: float,
+           *, max_block: int, accept_len: Optional[torch.Tensor] = None, next_token: Optional[torch.Tensor] = None,
+           workspace: Optional[torch.Tensor] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Speculative acceptance (sd_accept).  Returns device int32 (accept_len[S], next_token[S])."""
+    dev = target_logits.device
+    _need(target_logits, "target_logits", device=dev)
+    S = block_lens.shape[0]
+    if temperature > 0:
+        _need(draft_logits, "draft_logits", target_logits.dtype, dev)
+        _need(uniforms, "uniforms", torch.float32, dev)
+    for name, t in (("draft_tokens", draft_tokens), ("block_lens", block_lens), ("q_offsets", q_offsets)):
+        _need(t, name, torch.int32, dev)
+    if accept_len is None:
+        accept_len = torch.empty(S, dtype=torch.int32, device=dev)
+    if next_token is None:
+        next_token = torch.empty(S, dtype=torch.int32, device=dev)
+    shape = accept_shape(target_logits, S, max_block)
+    nbytes = accept_workspace_size(shape, temperature)
+    if workspace is None:
+        workspace = _default_ws.get(nbytes, dev)
+    _check(lib().sd_accept(ctypes.byref(shape), _ptr(target_logits),
+                           _ptr(draft_logits if temperature > 0 else None), _ptr(draft_tokens),
+                           _ptr(uniforms if temperature > 0 else None), _ptr(block_lens), _ptr(q_offsets),
+                           float(temperature), _ptr(accept_len), _ptr(next_token), _ptr(workspace),
+                           workspace.numel() * workspace.element_size(), _stream(stream)))
+    return accept_len, next_token
+
+
+def version() -> str:
+    return lib().sd_version().decode()

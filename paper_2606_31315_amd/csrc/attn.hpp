@@ -1,0 +1,434 @@
+// attn.hpp -- block attention over a GQA KV cache with ragged per-sequence blocks.
+//
+// Operation (Sec. 2.1): the B_s block rows of sequence s attend to their committed
+// context and to the block itself, causally for target verification or
+// bidirectionally for the block-diffusion drafter.  Query head h reads kv head
+// h / G with G = Hq / Hkv.
+//
+// Kernel design (gfx950):
+//   * One workgroup (4 wavefronts) per (sequence, kv head, KV split).  All G*B_s
+//     query rows of the sequence's kv-head group are packed into 16-row MFMA tiles,
+//     so each K/V byte is read from HBM once for the whole group.
+//   * K tile staged in LDS row-major; V tile written to LDS transposed
+//     (d-major, 4 consecutive keys per 8-byte word) so the P.V contraction over keys
+//     reads its operand with 8-byte LDS loads.
+//   * S^T = K Q^T on v_mfma_f32_16x16x32_bf16 (16x16x4_f32 for fp32 inputs): each lane
+//     then owns four keys of one query row, which is exactly the B-operand layout the
+//     O^T += V^T P^T MFMA needs, so P never leaves registers.
+//   * Online softmax in the log2 domain (scale * log2 e folded into one FMA), with
+//     per-lane partial row sums reduced once at the end.
+//   * Splits of one (sequence, kv head) are dealt to one XCD; the last split to finish
+//     (agent-scope fence + counter) merges the fp32 partials and writes the output, so
+//     one launch does the whole operation.
+#pragma once
+
+#include "common.hpp"
+
+namespace sdb {
+
+struct AttnArgs {
+  const void *q;
+  const void *k;
+  const void *v;
+  void *out;
+  const int *ctx_lens;
+  const int *block_lens;
+  const int *q_offsets;
+  float *part_o;      // [n_work, Mpad, D] unnormalised partial outputs
+  float2 *part_ml;    // [n_work, Mpad]    (row max in log2 units, row sum)
+  unsigned *counters; // [S * Hkv] splits finished, reset to 0 by the merging workgroup
+  int S, Hq, Hkv, G, Lmax;
+  int split_len;      // keys per split, multiple of the key tile
+  int max_splits;     // splits per (sequence, kv head) at the host-known maximum length
+  int Mpad;           // rows reserved per work item in the partial buffers
+  int n_work;         // S * Hkv * max_splits
+  int per_xcd;        // ceil(n_work / 8)
+  float scale_log2;   // softmax scale * log2(e)
+  int causal;
+};
+
+template <bool BF16>
+struct AttnCfg {
+  static constexpr int EB = BF16 ? 2 : 4;    // element bytes
+  static constexpr int KT = BF16 ? 64 : 32;  // keys per tile
+  static constexpr int NSUB = KT / 16;       // 16-key sub-tiles
+  static constexpr int KPAD = 16 / EB;       // K row padding (elements)
+  static constexpr int VPAD = BF16 ? 4 : 4;  // V^T row padding (keys)
+};
+
+// ---- operand loads -------------------------------------------------------
+// K rows: chunk c (16 bytes) of the tile is row c / CPR, column chunk c % CPR.
+template <bool BF16, int D>
+__device__ __forceinline__ void load_k_tile(u32x4 (&kr)[(AttnCfg<BF16>::KT * D * AttnCfg<BF16>::EB / 16) / 256],
+                                            const char *kbase, int key0, int key_end, int tid) {
+  constexpr int CPR = D * AttnCfg<BF16>::EB / 16;
+  constexpr int N = (AttnCfg<BF16>::KT * CPR) / 256;
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    const int c = tid + 256 * j;
+    const int row = c / CPR, col = c % CPR;
+    const int key = key0 + row;
+    if (key < key_end)
+      kr[j] = *reinterpret_cast<const u32x4 *>(kbase + ((size_t)key * D) * AttnCfg<BF16>::EB + col * 16);
+    else
+      kr[j] = u32x4{0, 0, 0, 0};
+  }
+}
+
+template <bool BF16, int D>
+__device__ __forceinline__ void store_k_tile(char *ks, const u32x4 (&kr)[(AttnCfg<BF16>::KT * D * AttnCfg<BF16>::EB / 16) / 256],
+                                             int tid) {
+  using C = AttnCfg<BF16>;
+  constexpr int CPR = D * C::EB / 16;
+  constexpr int N = (C::KT * CPR) / 256;
+  constexpr int PITCH = (D + C::KPAD) * C::EB;
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    const int c = tid + 256 * j;
+    const int row = c / CPR, col = c % CPR;
+    *reinterpret_cast<u32x4 *>(ks + row * PITCH + col * 16) = kr[j];
+  }
+}
+
+// V rows: item (kg, col) = 4 consecutive keys 4*kg.. x 8 consecutive dims col*8..
+template <bool BF16, int D>
+struct VItem {
+  static constexpr int VEC_PER_KEY = 8 * AttnCfg<BF16>::EB / 16;  // 16-byte loads per key
+  u32x4 r[4 * VEC_PER_KEY];
+};
+
+template <bool BF16, int D>
+__device__ __forceinline__ void load_v_tile(VItem<BF16, D> &vi, const char *vbase, int key0, int key_end,
+                                            int tid) {
+  using C = AttnCfg<BF16>;
+  constexpr int NITEMS = (C::KT / 4) * (D / 8);
+  constexpr int VPK = VItem<BF16, D>::VEC_PER_KEY;
+  if (tid >= NITEMS) return;
+  const int kg = tid / (D / 8), col = tid % (D / 8);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int key = key0 + kg * 4 + r;
+#pragma unroll
+    for (int h = 0; h < VPK; ++h) {
+      if (key < key_end)
+        vi.r[r * VPK + h] =
+            *reinterpret_cast<const u32x4 *>(vbase + ((size_t)key * D + col * 8) * C::EB + h * 16);
+      else
+        vi.r[r * VPK + h] = u32x4{0, 0, 0, 0};
+    }
+  }
+}
+
+__device__ __forceinline__ uint32_t u32x4_get(const u32x4 &v, int i) {
+  return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
+}
+
+template <bool BF16, int D>
+__device__ __forceinline__ void store_v_tile(char *vts, const VItem<BF16, D> &vi, int tid) {
+  using C = AttnCfg<BF16>;
+  constexpr int NITEMS = (C::KT / 4) * (D / 8);
+  constexpr int PITCH = (C::KT + C::VPAD) * C::EB;  // bytes per d row of V^T
+  if (tid >= NITEMS) return;
+  const int kg = tid / (D / 8), col = tid % (D / 8);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    char *dst = vts + (col * 8 + e) * PITCH + kg * 4 * C::EB;
+    if constexpr (BF16) {
+      // element e of key r sits in 32-bit word e/2, half e%2
+      const int w = e >> 1, sh = (e & 1) * 16;
+      const uint32_t k0 = (u32x4_get(vi.r[0], w) >> sh) & 0xffffu;
+      const uint32_t k1 = (u32x4_get(vi.r[1], w) >> sh) & 0xffffu;
+      const uint32_t k2 = (u32x4_get(vi.r[2], w) >> sh) & 0xffffu;
+      const uint32_t k3 = (u32x4_get(vi.r[3], w) >> sh) & 0xffffu;
+      *reinterpret_cast<uint2 *>(dst) = uint2{k0 | (k1 << 16), k2 | (k3 << 16)};
+    } else {
+      // fp32: element e of key r is word e%4 of 16-byte load r*2 + e/4
+      const int h = e >> 2, w = e & 3;
+      *reinterpret_cast<u32x4 *>(dst) = u32x4{u32x4_get(vi.r[0 * 2 + h], w), u32x4_get(vi.r[1 * 2 + h], w),
+                                              u32x4_get(vi.r[2 * 2 + h], w), u32x4_get(vi.r[3 * 2 + h], w)};
+    }
+  }
+}
+
+// ---- the kernel -------------------------------------------------------------
+// Query operand per 16-row m-tile:
+//   bf16: D/32 bf16x8 values, element e of step t is dim t*32 + (lane/16)*8 + e
+//   fp32: D/16 float4 values, element e of vector t4 is dim t4*16 + (lane/16)*4 + e
+template <bool BF16, int D>
+struct QOperand {
+  static constexpr int N = BF16 ? D / 32 : D / 16;
+  typename std::conditional<BF16, bf16x8, f32x4>::type v[N];
+};
+
+template <bool BF16, int D, int MT>
+__global__ __launch_bounds__(256) void block_attn_kernel(AttnArgs a) {
+  using C = AttnCfg<BF16>;
+  constexpr int KT = C::KT, NSUB = C::NSUB, EB = C::EB;
+  constexpr int KPITCH = (D + C::KPAD) * EB;   // bytes per K row in LDS
+  constexpr int VPITCH = (KT + C::VPAD) * EB;  // bytes per V^T row in LDS
+  constexpr int NDT = D / 16;                  // 16-wide output column tiles
+  __shared__ __attribute__((aligned(16))) char ks[KT * KPITCH];
+  __shared__ __attribute__((aligned(16))) char vts[D * VPITCH];
+  __shared__ int s_last;
+
+  const int w = xcd_logical_id(blockIdx.x, a.per_xcd);
+  if (w >= a.n_work) return;
+  const int split = w % a.max_splits;
+  const int sg = w / a.max_splits;
+  const int g = sg % a.Hkv;
+  const int s = sg / a.Hkv;
+  const int ctx = a.ctx_lens[s];
+  const int B = a.block_lens[s];
+  if (B <= 0) return;
+  const int L = ctx + B;
+  const int nsplit = (L + a.split_len - 1) / a.split_len;
+  if (split >= nsplit) return;
+  const int k0 = split * a.split_len;
+  const int k1 = min(k0 + a.split_len, L);
+  const int M = a.G * B;
+  const int qoff = a.q_offsets[s];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int l16 = lane & 15;   // query row inside an m-tile / key row inside a sub-tile
+  const int kgrp = lane >> 4;  // 0..3
+
+  const char *kbase = reinterpret_cast<const char *>(a.k) + ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
+  const char *vbase = reinterpret_cast<const char *>(a.v) + ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
+
+  // ---- query operand and per-row state for this wave's m-tiles ----
+  const int nmt = (M + 15) >> 4;
+  QOperand<BF16, D> qop[MT];
+  f32x4 oacc[MT][NDT];
+  float m_run[MT], l_run[MT];
+  int row_i[MT];  // block position of this lane's query row (or a large value for padding rows)
+#pragma unroll
+  for (int j = 0; j < MT; ++j) {
+    const int mt = wave + 4 * j;
+    const int m = mt * 16 + l16;
+    m_run[j] = -INFINITY;
+    l_run[j] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) oacc[j][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const bool valid = (mt < nmt) && (m < M);
+    row_i[j] = valid ? m / a.G : 0x3fffffff;
+    const char *qrow = valid ? reinterpret_cast<const char *>(a.q) +
+                                   ((size_t)(qoff + m / a.G) * a.Hq + g * a.G + m % a.G) * D * EB
+                             : nullptr;
+#pragma unroll
+    for (int t = 0; t < QOperand<BF16, D>::N; ++t) {
+      if constexpr (BF16) {
+        u32x4 raw = valid ? *reinterpret_cast<const u32x4 *>(qrow + (t * 32 + kgrp * 8) * EB) : u32x4{0, 0, 0, 0};
+        qop[j].v[t] = __builtin_bit_cast(bf16x8, raw);
+      } else {
+        qop[j].v[t] = valid ? *reinterpret_cast<const f32x4 *>(qrow + (t * 16 + kgrp * 4) * EB)
+                            : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+  }
+
+  // ---- stream the split's keys in tiles of KT ----
+  constexpr int NKR = (KT * D * EB / 16) / 256;
+  u32x4 kr[NKR];
+  VItem<BF16, D> vi;
+  const int ntiles = (k1 - k0 + KT - 1) / KT;
+  load_k_tile<BF16, D>(kr, kbase, k0, k1, tid);
+  load_v_tile<BF16, D>(vi, vbase, k0, k1, tid);
+
+  for (int t = 0; t < ntiles; ++t) {
+    const int kt = k0 + t * KT;
+    if (t > 0) __syncthreads();
+    store_k_tile<BF16, D>(ks, kr, tid);
+    store_v_tile<BF16, D>(vts, vi, tid);
+    __syncthreads();
+    if (t + 1 < ntiles) {
+      load_k_tile<BF16, D>(kr, kbase, kt + KT, k1, tid);
+      load_v_tile<BF16, D>(vi, vbase, kt + KT, k1, tid);
+    }
+
+    // S^T = K Q^T for every active m-tile: sacc[j][sub] holds keys kt+sub*16+kgrp*4+r, row l16
+    f32x4 sacc[MT][NSUB];
+#pragma unroll
+    for (int j = 0; j < MT; ++j)
+#pragma unroll
+      for (int sb = 0; sb < NSUB; ++sb) sacc[j][sb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int sb = 0; sb < NSUB; ++sb) {
+      const char *krow = ks + (sb * 16 + l16) * KPITCH;
+      if constexpr (BF16) {
+#pragma unroll
+        for (int st = 0; st < D / 32; ++st) {
+          const bf16x8 av = *reinterpret_cast<const bf16x8 *>(krow + (st * 32 + kgrp * 8) * EB);
+#pragma unroll
+          for (int j = 0; j < MT; ++j)
+            if (wave + 4 * j < nmt)
+              sacc[j][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qop[j].v[st], sacc[j][sb], 0, 0, 0);
+        }
+      } else {
+#pragma unroll
+        for (int t4 = 0; t4 < D / 16; ++t4) {
+          const f32x4 av = *reinterpret_cast<const f32x4 *>(krow + (t4 * 16 + kgrp * 4) * EB);
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+#pragma unroll
+            for (int j = 0; j < MT; ++j)
+              if (wave + 4 * j < nmt)
+                sacc[j][sb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[e], qop[j].v[t4][e], sacc[j][sb], 0, 0, 0);
+        }
+      }
+    }
+
+    // mask + online softmax (log2 domain); P kept in registers
+#pragma unroll
+    for (int j = 0; j < MT; ++j) {
+      if (wave + 4 * j >= nmt) continue;
+      const int lim = a.causal ? min(k1, ctx + row_i[j] + 1) : k1;  // keys < lim are visible
+      float tmax = -INFINITY;
+#pragma unroll
+      for (int sb = 0; sb < NSUB; ++sb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = kt + sb * 16 + kgrp * 4 + r;
+          const float sv = (key < lim) ? sacc[j][sb][r] * a.scale_log2 : -INFINITY;
+          sacc[j][sb][r] = sv;
+          tmax = fmaxf(tmax, sv);
+        }
+      tmax = fmaxf(tmax, shfl_xor_f(tmax, 16));
+      tmax = fmaxf(tmax, shfl_xor_f(tmax, 32));
+      const float mnew = fmaxf(m_run[j], tmax);
+      const float muse = (mnew == -INFINITY) ? 0.f : mnew;
+      const float alpha = fast_exp2(m_run[j] - muse);
+      m_run[j] = mnew;
+      float psum = 0.f;
+#pragma unroll
+      for (int sb = 0; sb < NSUB; ++sb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float p = fast_exp2(sacc[j][sb][r] - muse);
+          sacc[j][sb][r] = p;
+          psum += p;
+        }
+      l_run[j] = l_run[j] * alpha + psum;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) oacc[j][dt] *= alpha;
+    }
+
+    // O^T += V^T P^T
+    if constexpr (BF16) {
+#pragma unroll
+      for (int kk = 0; kk < NSUB / 2; ++kk) {
+        bf16x8 pb[MT];
+#pragma unroll
+        for (int j = 0; j < MT; ++j) {
+          u32x4 raw{pack_bf16x2(sacc[j][2 * kk][0], sacc[j][2 * kk][1]),
+                    pack_bf16x2(sacc[j][2 * kk][2], sacc[j][2 * kk][3]),
+                    pack_bf16x2(sacc[j][2 * kk + 1][0], sacc[j][2 * kk + 1][1]),
+                    pack_bf16x2(sacc[j][2 * kk + 1][2], sacc[j][2 * kk + 1][3])};
+          pb[j] = __builtin_bit_cast(bf16x8, raw);
+        }
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+          const char *vrow = vts + (dt * 16 + l16) * VPITCH;
+          const uint2 lo = *reinterpret_cast<const uint2 *>(vrow + (kk * 32 + kgrp * 4) * EB);
+          const uint2 hi = *reinterpret_cast<const uint2 *>(vrow + (kk * 32 + 16 + kgrp * 4) * EB);
+          const bf16x8 av = __builtin_bit_cast(bf16x8, (u32x4{lo.x, lo.y, hi.x, hi.y}));
+#pragma unroll
+          for (int j = 0; j < MT; ++j)
+            if (wave + 4 * j < nmt)
+              oacc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, pb[j], oacc[j][dt], 0, 0, 0);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int sb = 0; sb < NSUB; ++sb)
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+          const f32x4 av = *reinterpret_cast<const f32x4 *>(vts + (dt * 16 + l16) * VPITCH + (sb * 16 + kgrp * 4) * EB);
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int j = 0; j < MT; ++j)
+              if (wave + 4 * j < nmt)
+                oacc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[r], sacc[j][sb][r], oacc[j][dt], 0, 0, 0);
+        }
+    }
+  }
+
+  // ---- row sums: reduce the per-lane partials over the four key groups ----
+#pragma unroll
+  for (int j = 0; j < MT; ++j) {
+    l_run[j] += shfl_xor_f(l_run[j], 16);
+    l_run[j] += shfl_xor_f(l_run[j], 32);
+  }
+
+  auto out_row_ptr = [&](int m) -> char * {
+    return reinterpret_cast<char *>(a.out) + ((size_t)(qoff + m / a.G) * a.Hq + g * a.G + m % a.G) * D * EB;
+  };
+
+  if (nsplit == 1) {
+#pragma unroll
+    for (int j = 0; j < MT; ++j) {
+      const int mt = wave + 4 * j;
+      const int m = mt * 16 + l16;
+      if (mt >= nmt || m >= M) continue;
+      const float inv = 1.f / l_run[j];
+      char *orow = out_row_ptr(m);
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) {
+        const int d = dt * 16 + kgrp * 4;
+        const f32x4 o = oacc[j][dt] * inv;
+        if constexpr (BF16)
+          *reinterpret_cast<uint2 *>(orow + d * EB) = uint2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
+        else
+          *reinterpret_cast<f32x4 *>(orow + d * EB) = o;
+      }
+    }
+    return;
+  }
+
+  // ---- several splits: write this split's partials, last one merges ----
+  const size_t wrow = (size_t)w * a.Mpad;
+#pragma unroll
+  for (int j = 0; j < MT; ++j) {
+    const int mt = wave + 4 * j;
+    const int m = mt * 16 + l16;
+    if (mt >= nmt || m >= M) continue;
+    float *prow = a.part_o + (wrow + m) * D;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) *reinterpret_cast<f32x4 *>(prow + dt * 16 + kgrp * 4) = oacc[j][dt];
+    if (kgrp == 0) a.part_ml[wrow + m] = float2{m_run[j], l_run[j]};
+  }
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) s_last = (atomicAdd(&a.counters[sg], 1u) == (unsigned)(nsplit - 1));
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+
+  const size_t wbase = (size_t)(sg * a.max_splits) * a.Mpad;  // work item of split 0
+  constexpr int D4 = D / 4;
+  for (int idx = tid; idx < M * D4; idx += 256) {
+    const int m = idx / D4, d = (idx % D4) * 4;
+    float mx = -INFINITY;
+    for (int sp = 0; sp < nsplit; ++sp) mx = fmaxf(mx, a.part_ml[wbase + (size_t)sp * a.Mpad + m].x);
+    float lsum = 0.f;
+    f32x4 acc{0.f, 0.f, 0.f, 0.f};
+    for (int sp = 0; sp < nsplit; ++sp) {
+      const size_t r = wbase + (size_t)sp * a.Mpad + m;
+      const float2 ml = a.part_ml[r];
+      const float wgt = (ml.x == -INFINITY) ? 0.f : fast_exp2(ml.x - mx);
+      lsum += wgt * ml.y;
+      acc += wgt * *reinterpret_cast<const f32x4 *>(a.part_o + r * D + d);
+    }
+    const f32x4 o = acc * (1.f / lsum);
+    char *orow = out_row_ptr(m);
+    if constexpr (BF16)
+      *reinterpret_cast<uint2 *>(orow + d * EB) = uint2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
+    else
+      *reinterpret_cast<f32x4 *>(orow + d * EB) = o;
+  }
+  if (tid == 0) atomicExch(&a.counters[sg], 0u);
+}
+
+}  // namespace sdb

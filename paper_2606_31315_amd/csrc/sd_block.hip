@@ -1,0 +1,334 @@
+// sd_block.hip -- C ABI of libsdblock.so (declared in include/sd_block.h).
+//
+// Host side only: argument validation, workspace layout, launch planning and kernel
+// dispatch.  The arithmetic lives in attn.hpp and accept.hpp.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+
+#include "accept.hpp"
+#include "attn.hpp"
+#include "sd_block.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return SD_OK;
+}
+
+// Every workspace starts with a fixed region of 32-bit counters, so that a workspace
+// zeroed once stays valid for calls of any shape (the counters never move).
+constexpr size_t kCounterBytes = 64 * 1024;
+constexpr int kMaxCounters = (int)(kCounterBytes / 4);
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+int check_launch(const char *what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(SD_ERR_HIP, "%s: launch failed: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+// attention planning
+// ---------------------------------------------------------------------------
+struct AttnPlan {
+  int G, KT, split_len, max_splits, Mpad, n_work, per_xcd, MT;
+  size_t off_ml, off_o, total;
+};
+
+int attn_plan(const sd_attn_shape *sh, AttnPlan *p) {
+  if (!sh) return fail(SD_ERR_INVALID_ARG, "sd_block_attn: shape is NULL");
+  const int S = sh->num_seqs, Hq = sh->num_q_heads, Hkv = sh->num_kv_heads, D = sh->head_dim;
+  if (S < 0) return fail(SD_ERR_INVALID_ARG, "num_seqs must be >= 0 (got %d)", S);
+  if (Hq < 1 || Hkv < 1) return fail(SD_ERR_INVALID_ARG, "head counts must be >= 1 (Hq=%d, Hkv=%d)", Hq, Hkv);
+  if (Hq % Hkv) return fail(SD_ERR_INVALID_ARG, "num_q_heads %d is not a multiple of num_kv_heads %d", Hq, Hkv);
+  if (sh->dtype != SD_BF16 && sh->dtype != SD_F32) return fail(SD_ERR_INVALID_ARG, "unknown dtype %d", sh->dtype);
+  if (D != 64 && D != 128) return fail(SD_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", D);
+  if (sh->max_block < 1 || sh->max_block > 64)
+    return fail(SD_ERR_INVALID_ARG, "max_block must be in [1, 64] (got %d)", sh->max_block);
+  if (sh->max_ctx < 0) return fail(SD_ERR_INVALID_ARG, "max_ctx must be >= 0 (got %d)", sh->max_ctx);
+  if (sh->max_kv_len < 1 || (long long)sh->max_ctx + sh->max_block > sh->max_kv_len)
+    return fail(SD_ERR_INVALID_ARG, "max_ctx + max_block (%d + %d) exceeds max_kv_len %d", sh->max_ctx,
+                sh->max_block, sh->max_kv_len);
+  if (sh->total_q < 0 || (long long)sh->total_q > (long long)S * sh->max_block)
+    return fail(SD_ERR_INVALID_ARG, "total_q %d outside [0, num_seqs * max_block]", sh->total_q);
+  const int G = Hq / Hkv;
+  if ((long long)G * sh->max_block > 256)
+    return fail(SD_ERR_UNSUPPORTED, "group size %d times max_block %d exceeds 256 query rows", G, sh->max_block);
+  if (!(sh->scale >= 0.f) || isinf(sh->scale)) return fail(SD_ERR_INVALID_ARG, "scale must be finite and >= 0");
+  if ((long long)S * Hkv > kMaxCounters)
+    return fail(SD_ERR_INVALID_ARG, "num_seqs * num_kv_heads exceeds %d", kMaxCounters);
+
+  p->G = G;
+  p->KT = (sh->dtype == SD_BF16) ? 64 : 32;
+  const long long max_L = (long long)sh->max_ctx + sh->max_block;
+  const long long pairs = (long long)S * Hkv;
+  // Split the keys so the grid holds about 512 workgroups (two per CU) at the maximum
+  // length, with splits of at most 1024 keys so ragged contexts still balance.
+  long long want = pairs > 0 ? (512 + pairs - 1) / pairs : 1;
+  long long sl = (max_L + want - 1) / want;
+  sl = ((sl + p->KT - 1) / p->KT) * p->KT;
+  if (sl > 1024) sl = 1024;
+  if (sl < p->KT) sl = p->KT;
+  if (const char *env = getenv("SDBLOCK_ATTN_SPLIT_LEN")) {  // tuning override, multiple of 64
+    long long v = atoll(env);
+    if (v >= 64 && v % 64 == 0) sl = v;
+  }
+  p->split_len = (int)sl;
+  p->max_splits = (int)((max_L + sl - 1) / sl);
+  p->Mpad = ((G * sh->max_block + 15) / 16) * 16;
+  const long long nw = pairs * p->max_splits;
+  if (nw > (1LL << 30)) return fail(SD_ERR_INVALID_ARG, "problem too large");
+  p->n_work = (int)nw;
+  p->per_xcd = (int)((nw + sdb::kNumXcd - 1) / sdb::kNumXcd);
+  const int nmt = p->Mpad / 16;
+  p->MT = nmt <= 4 ? 1 : nmt <= 8 ? 2 : 4;
+  size_t off = kCounterBytes;
+  p->off_ml = off;
+  if (p->max_splits > 1) off = align256(off + (size_t)nw * p->Mpad * sizeof(float2));
+  p->off_o = off;
+  if (p->max_splits > 1) off = align256(off + (size_t)nw * p->Mpad * D * sizeof(float));
+  p->total = off;
+  return ok();
+}
+
+template <bool BF16, int D, int MT>
+void launch_attn(const sdb::AttnArgs &a, int grid, hipStream_t st) {
+  hipLaunchKernelGGL((sdb::block_attn_kernel<BF16, D, MT>), dim3(grid), dim3(256), 0, st, a);
+}
+
+template <bool BF16, int D>
+void launch_attn_mt(const sdb::AttnArgs &a, int grid, int MT, hipStream_t st) {
+  if (MT == 1) launch_attn<BF16, D, 1>(a, grid, st);
+  else if (MT == 2) launch_attn<BF16, D, 2>(a, grid, st);
+  else launch_attn<BF16, D, 4>(a, grid, st);
+}
+
+// ---------------------------------------------------------------------------
+// acceptance planning
+// ---------------------------------------------------------------------------
+struct AcceptPlan {
+  int rows, nch, nch2;
+  size_t off_stats, off_info, off_samp, total;
+};
+
+int accept_plan(const sd_accept_shape *sh, float temperature, AcceptPlan *p) {
+  if (!sh) return fail(SD_ERR_INVALID_ARG, "sd_accept: shape is NULL");
+  const int S = sh->num_seqs, V = sh->vocab;
+  if (S < 0) return fail(SD_ERR_INVALID_ARG, "num_seqs must be >= 0 (got %d)", S);
+  if (V < 1) return fail(SD_ERR_INVALID_ARG, "vocab must be >= 1 (got %d)", V);
+  if (sh->dtype != SD_BF16 && sh->dtype != SD_F32) return fail(SD_ERR_INVALID_ARG, "unknown dtype %d", sh->dtype);
+  if (sh->max_block < 1 || sh->max_block > 64)
+    return fail(SD_ERR_INVALID_ARG, "max_block must be in [1, 64] (got %d)", sh->max_block);
+  if (sh->total_q < S || (long long)sh->total_q > (long long)S * sh->max_block)
+    return fail(SD_ERR_INVALID_ARG, "total_q %d outside [num_seqs, num_seqs * max_block]", sh->total_q);
+  if (!(temperature >= 0.f) || isinf(temperature))
+    return fail(SD_ERR_INVALID_ARG, "temperature must be finite and >= 0");
+  if (2LL * S > kMaxCounters) return fail(SD_ERR_INVALID_ARG, "num_seqs exceeds %d", kMaxCounters / 2);
+  const bool sample = temperature > 0.f;
+  const long long rows = (long long)sh->total_q + (sample ? (long long)sh->total_q - S : 0);
+  if (rows * (long long)V > (1LL << 46)) return fail(SD_ERR_INVALID_ARG, "problem too large");
+  const int VEC = (sh->dtype == SD_BF16) ? 8 : 4;
+  const long long vecs = V / VEC;
+  const long long max_ch = vecs / 256 > 0 ? vecs / 256 : 1;  // at least one vector per thread
+  long long nch = rows > 0 ? (2048 + rows - 1) / rows : 1;
+  if (nch > max_ch) nch = max_ch;
+  if (nch < 1) nch = 1;
+  long long nch2 = S > 0 ? (512 + S - 1) / S : 1;
+  if (nch2 > max_ch) nch2 = max_ch;
+  if (nch2 < 1) nch2 = 1;
+  if (rows * nch > (1LL << 30) || (long long)S * nch2 > (1LL << 30))
+    return fail(SD_ERR_INVALID_ARG, "problem too large");
+  p->rows = (int)rows;
+  p->nch = (int)nch;
+  p->nch2 = (int)nch2;
+  size_t off = kCounterBytes;
+  p->off_stats = off;
+  off = align256(off + (size_t)rows * nch * sizeof(float2));
+  p->off_info = off;
+  off = align256(off + (size_t)S * 2 * sizeof(float4));
+  p->off_samp = off;
+  if (sample) off = align256(off + (size_t)S * nch2 * sizeof(double2));
+  p->total = off;
+  return ok();
+}
+
+__global__ void zero_fill_kernel(uint32_t *p, size_t n) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *sd_last_error(void) { return g_err.c_str(); }
+
+const char *sd_version(void) { return "sdblock 0.1 gfx950"; }
+
+int sd_workspace_init(void *workspace, size_t bytes, void *stream) {
+  if (!workspace && bytes) return fail(SD_ERR_INVALID_ARG, "workspace is NULL");
+  if (!aligned16(workspace)) return fail(SD_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+  if (bytes % 4) return fail(SD_ERR_INVALID_ARG, "bytes must be a multiple of 4");
+  if (!bytes) return ok();
+  const size_t n = bytes / 4;
+  size_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(zero_fill_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream,
+                     (uint32_t *)workspace, n);
+  return check_launch("sd_workspace_init");
+}
+
+int sd_block_attn_workspace_size(const sd_attn_shape *shape, size_t *bytes) {
+  if (!bytes) return fail(SD_ERR_INVALID_ARG, "bytes is NULL");
+  AttnPlan p;
+  int rc = attn_plan(shape, &p);
+  if (rc) return rc;
+  *bytes = p.total;
+  return ok();
+}
+
+int sd_block_attn(const sd_attn_shape *sh, const void *q, const void *k_cache, const void *v_cache,
+                  const int32_t *ctx_lens, const int32_t *block_lens, const int32_t *q_offsets,
+                  int32_t mask_mode, void *out, void *workspace, size_t workspace_bytes, void *stream) {
+  AttnPlan p;
+  int rc = attn_plan(sh, &p);
+  if (rc) return rc;
+  if (mask_mode != SD_MASK_CAUSAL_IN_BLOCK && mask_mode != SD_MASK_BIDIR_IN_BLOCK)
+    return fail(SD_ERR_INVALID_ARG, "unknown mask_mode %d", mask_mode);
+  if (sh->num_seqs == 0 || sh->total_q == 0) return ok();
+  if (!q || !k_cache || !v_cache || !out || !ctx_lens || !block_lens || !q_offsets || !workspace)
+    return fail(SD_ERR_INVALID_ARG, "sd_block_attn: NULL pointer argument");
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out))
+    return fail(SD_ERR_INVALID_ARG, "q, caches and out must be 16-byte aligned");
+  if (((uintptr_t)workspace & 255u) != 0) return fail(SD_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  if (workspace_bytes < p.total)
+    return fail(SD_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, p.total);
+
+  sdb::AttnArgs a;
+  a.q = q;
+  a.k = k_cache;
+  a.v = v_cache;
+  a.out = out;
+  a.ctx_lens = ctx_lens;
+  a.block_lens = block_lens;
+  a.q_offsets = q_offsets;
+  char *ws = (char *)workspace;
+  a.counters = (unsigned *)ws;
+  a.part_ml = (float2 *)(ws + p.off_ml);
+  a.part_o = (float *)(ws + p.off_o);
+  a.S = sh->num_seqs;
+  a.Hq = sh->num_q_heads;
+  a.Hkv = sh->num_kv_heads;
+  a.G = p.G;
+  a.Lmax = sh->max_kv_len;
+  a.split_len = p.split_len;
+  a.max_splits = p.max_splits;
+  a.Mpad = p.Mpad;
+  a.n_work = p.n_work;
+  a.per_xcd = p.per_xcd;
+  const float scale = sh->scale > 0.f ? sh->scale : 1.0f / sqrtf((float)sh->head_dim);
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.causal = mask_mode == SD_MASK_CAUSAL_IN_BLOCK;
+  const int grid = p.per_xcd * sdb::kNumXcd;
+  hipStream_t st = (hipStream_t)stream;
+  const bool bf = sh->dtype == SD_BF16;
+  if (sh->head_dim == 128) {
+    if (bf) launch_attn_mt<true, 128>(a, grid, p.MT, st);
+    else launch_attn_mt<false, 128>(a, grid, p.MT, st);
+  } else {
+    if (bf) launch_attn_mt<true, 64>(a, grid, p.MT, st);
+    else launch_attn_mt<false, 64>(a, grid, p.MT, st);
+  }
+  return check_launch("sd_block_attn");
+}
+
+int sd_accept_workspace_size(const sd_accept_shape *shape, float temperature, size_t *bytes) {
+  if (!bytes) return fail(SD_ERR_INVALID_ARG, "bytes is NULL");
+  AcceptPlan p;
+  int rc = accept_plan(shape, temperature, &p);
+  if (rc) return rc;
+  *bytes = p.total;
+  return ok();
+}
+
+int sd_accept(const sd_accept_shape *sh, const void *target_logits, const void *draft_logits,
+              const int32_t *draft_tokens, const float *uniforms, const int32_t *block_lens,
+              const int32_t *q_offsets, float temperature, int32_t *accept_len, int32_t *next_token,
+              void *workspace, size_t workspace_bytes, void *stream) {
+  AcceptPlan p;
+  int rc = accept_plan(sh, temperature, &p);
+  if (rc) return rc;
+  if (sh->num_seqs == 0) return ok();
+  const bool sample = temperature > 0.f;
+  if (!target_logits || !block_lens || !q_offsets || !accept_len || !next_token || !workspace)
+    return fail(SD_ERR_INVALID_ARG, "sd_accept: NULL pointer argument");
+  if (sh->total_q > sh->num_seqs && !draft_tokens) return fail(SD_ERR_INVALID_ARG, "draft_tokens is NULL");
+  if (sample && (!draft_logits || !uniforms))
+    return fail(SD_ERR_INVALID_ARG, "draft_logits and uniforms are required when temperature > 0");
+  if (!aligned16(target_logits) || (sample && !aligned16(draft_logits)))
+    return fail(SD_ERR_INVALID_ARG, "logits must be 16-byte aligned");
+  if (((uintptr_t)workspace & 255u) != 0) return fail(SD_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  if (workspace_bytes < p.total)
+    return fail(SD_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, p.total);
+
+  sdb::AcceptArgs a;
+  a.target = target_logits;
+  a.draft = draft_logits;
+  a.draft_tokens = draft_tokens;
+  a.uniforms = uniforms;
+  a.block_lens = block_lens;
+  a.q_offsets = q_offsets;
+  a.accept_len = accept_len;
+  a.next_token = next_token;
+  char *ws = (char *)workspace;
+  a.cnt1 = (unsigned *)ws;
+  a.cnt2 = (unsigned *)ws + sh->num_seqs;
+  a.stats = (float2 *)(ws + p.off_stats);
+  a.seqinfo = (float4 *)(ws + p.off_info);
+  a.samp = (double2 *)(ws + p.off_samp);
+  a.S = sh->num_seqs;
+  a.V = sh->vocab;
+  a.total_q = sh->total_q;
+  a.nch = p.nch;
+  a.nch2 = p.nch2;
+  a.c = sample ? (float)(1.4426950408889634 / (double)temperature) : 0.f;
+  hipStream_t st = (hipStream_t)stream;
+  const bool bf = sh->dtype == SD_BF16;
+  const unsigned g1 = (unsigned)(p.rows * p.nch);
+  if (sample) {
+    if (bf) hipLaunchKernelGGL((sdb::accept_stats_kernel<true, true>), dim3(g1), dim3(256), 0, st, a);
+    else hipLaunchKernelGGL((sdb::accept_stats_kernel<false, true>), dim3(g1), dim3(256), 0, st, a);
+    rc = check_launch("sd_accept stats");
+    if (rc) return rc;
+    const unsigned g2 = (unsigned)(sh->num_seqs * p.nch2);
+    if (bf) hipLaunchKernelGGL((sdb::accept_sample_kernel<true>), dim3(g2), dim3(256), 0, st, a);
+    else hipLaunchKernelGGL((sdb::accept_sample_kernel<false>), dim3(g2), dim3(256), 0, st, a);
+    return check_launch("sd_accept sample");
+  }
+  if (bf) hipLaunchKernelGGL((sdb::accept_stats_kernel<true, false>), dim3(g1), dim3(256), 0, st, a);
+  else hipLaunchKernelGGL((sdb::accept_stats_kernel<false, false>), dim3(g1), dim3(256), 0, st, a);
+  return check_launch("sd_accept stats");
+}
+
+}  // extern "C"

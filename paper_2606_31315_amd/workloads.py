@@ -155,8 +155,8 @@ class Workload:
 # --------------------------------------------------------------------------- #
 
 def make_attn(rs: dict, *, S, Hq, Hkv, D, ctx_lens, block_lens, dtype, mask_mode, Lmax=None,
-              tail_fill=float("nan"), block_key_gain=1.0, q_gain=1.0, name="") -> AttnProblem:
-    """Attention inputs: q, K, V ~ N(0,1) (times the optional gains), cast to ``dtype``.
+              tail_fill=float("nan"), block_key_gain=1.0, q_gain=1.0, value_gain=1.0, name="") -> AttnProblem:
+    """Attention inputs: q, K, V ~ N(0,1) (times the optional gains), rounded to ``dtype``.
 
     ``block_key_gain`` scales the in-block keys [ctx, ctx+B) and ``q_gain`` the
     queries; gains > 1 make in-block scores dominate so that an off-by-one in the
@@ -164,23 +164,30 @@ def make_attn(rs: dict, *, S, Hq, Hkv, D, ctx_lens, block_lens, dtype, mask_mode
     """
     ctx_lens = np.asarray(ctx_lens, dtype=np.int32)
     block_lens = np.asarray(block_lens, dtype=np.int32)
-    if Lmax is None:
-        Lmax = int((ctx_lens + block_lens).max()) if S else 1
+    if Lmax is None:  # capacity for the longest context plus the largest block
+        Lmax = int(ctx_lens.max() + block_lens.max()) if S else 1
     off = offsets_from_lens(block_lens)
     tq = int(off[-1])
     q = rs["q"].standard_normal((tq, Hq, D), dtype=np.float32) * np.float32(q_gain)
-    k = np.full((S, Hkv, Lmax, D), tail_fill, dtype=np.float32)
-    v = np.full((S, Hkv, Lmax, D), tail_fill, dtype=np.float32)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    if dtype not in ("bf16", "f32"):
+        raise ValueError(f"unknown dtype {dtype!r}")
+    k = torch.full((S, Hkv, Lmax, D), tail_fill, dtype=tdt)
+    v = torch.full((S, Hkv, Lmax, D), tail_fill, dtype=tdt)
     for s in range(S):
         n = int(ctx_lens[s] + block_lens[s])
-        k[s, :, :n] = rs["K"].standard_normal((Hkv, n, D), dtype=np.float32)
-        v[s, :, :n] = rs["V"].standard_normal((Hkv, n, D), dtype=np.float32)
+        ks = rs["K"].standard_normal((Hkv, n, D), dtype=np.float32)
+        vs = rs["V"].standard_normal((Hkv, n, D), dtype=np.float32)
         if block_key_gain != 1.0:
             c = int(ctx_lens[s])
-            k[s, :, c:n] *= np.float32(block_key_gain)
+            ks[:, c:n] *= np.float32(block_key_gain)
+        if value_gain != 1.0:
+            vs *= np.float32(value_gain)
+        k[s, :, :n] = torch.from_numpy(ks).to(tdt)
+        v[s, :, :n] = torch.from_numpy(vs).to(tdt)
     return AttnProblem(S=S, Hq=Hq, Hkv=Hkv, D=D, Lmax=Lmax, ctx_lens=ctx_lens, block_lens=block_lens,
-                       q_offsets=off, q=_to_dtype(q, dtype), k_cache=_to_dtype(k, dtype),
-                       v_cache=_to_dtype(v, dtype), dtype=dtype, mask_mode=mask_mode, name=name)
+                       q_offsets=off, q=_to_dtype(q, dtype), k_cache=k,
+                       v_cache=v, dtype=dtype, mask_mode=mask_mode, name=name)
 
 
 def _gumbel_argmax(rs_draft, logits: np.ndarray, temperature: float) -> np.ndarray:

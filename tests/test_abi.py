@@ -1,0 +1,169 @@
+"""The C ABI on the host: the library loads, exports what include/sd_block.h declares,
+and rejects bad arguments with the documented status codes before touching a device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_31315_amd import _lib as L
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sd_block.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sd_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    lib = L.lib()
+    names = declared_functions()
+    assert set(names) == set(L.EXPORTS), names
+    for n in names:
+        assert hasattr(lib, n), f"missing export {n}"
+    assert L.version().startswith("sdblock")
+
+
+def good_attn_shape(**kw):
+    sh = L.SdAttnShape(num_seqs=2, num_q_heads=32, num_kv_heads=8, head_dim=128, max_kv_len=4200, total_q=20,
+                       max_ctx=4096, max_block=16, dtype=L.SD_BF16, scale=0.0)
+    for k, v in kw.items():
+        setattr(sh, k, v)
+    return sh
+
+
+def attn_ws(sh):
+    n = ctypes.c_size_t(0)
+    rc = L.lib().sd_block_attn_workspace_size(ctypes.byref(sh), ctypes.byref(n))
+    return rc, n.value
+
+
+def test_attn_workspace_size_valid():
+    rc, n = attn_ws(good_attn_shape())
+    assert rc == L.SD_OK and n >= 64 * 1024
+    rc2, n2 = attn_ws(good_attn_shape(num_seqs=4, total_q=40))
+    assert rc2 == L.SD_OK and n2 >= n
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("num_seqs", -1, L.SD_ERR_INVALID_ARG),
+    ("num_q_heads", 0, L.SD_ERR_INVALID_ARG),
+    ("num_kv_heads", 5, L.SD_ERR_INVALID_ARG),       # 32 % 5 != 0
+    ("head_dim", 96, L.SD_ERR_UNSUPPORTED),
+    ("max_block", 0, L.SD_ERR_INVALID_ARG),
+    ("max_block", 65, L.SD_ERR_INVALID_ARG),
+    ("max_kv_len", 4000, L.SD_ERR_INVALID_ARG),      # max_ctx + max_block > Lmax
+    ("total_q", 33, L.SD_ERR_INVALID_ARG),           # > S * max_block
+    ("dtype", 7, L.SD_ERR_INVALID_ARG),
+    ("scale", float("nan"), L.SD_ERR_INVALID_ARG),
+    ("scale", -1.0, L.SD_ERR_INVALID_ARG),
+])
+def test_attn_shape_errors(field, value, code):
+    rc, _ = attn_ws(good_attn_shape(**{field: value}))
+    assert rc == code
+    assert L.lib().sd_last_error().decode()
+
+
+def test_attn_group_too_large():
+    rc, _ = attn_ws(good_attn_shape(num_q_heads=64, num_kv_heads=1, max_block=8, total_q=16))  # 64*8 > 256 rows
+    assert rc == L.SD_ERR_UNSUPPORTED
+
+
+def call_attn(sh, ptrs=None, mask=0, ws_bytes=None, ws_ptr=256):
+    P = ctypes.c_void_p
+    p = dict(q=4096, k=8192, v=12288, ctx=16, bl=32, off=48, out=16384)
+    if ptrs:
+        p.update(ptrs)
+    if ws_bytes is None:
+        ws_bytes = attn_ws(sh)[1]
+    return L.lib().sd_block_attn(ctypes.byref(sh) if sh is not None else None, P(p["q"]), P(p["k"]), P(p["v"]),
+                                 P(p["ctx"]), P(p["bl"]), P(p["off"]), mask, P(p["out"]), P(ws_ptr), ws_bytes, None)
+
+
+def test_attn_call_errors_without_device():
+    # every one of these is rejected on the host: the fake addresses are never dereferenced
+    assert L.lib().sd_block_attn(None, *([None] * 6), 0, None, None, 0, None) == L.SD_ERR_INVALID_ARG
+    sh = good_attn_shape()
+    assert call_attn(sh, mask=2) == L.SD_ERR_INVALID_ARG
+    assert call_attn(sh, ptrs=dict(q=0)) == L.SD_ERR_INVALID_ARG
+    assert call_attn(sh, ptrs=dict(k=8200)) == L.SD_ERR_INVALID_ARG        # misaligned cache
+    assert call_attn(sh, ws_ptr=300) == L.SD_ERR_INVALID_ARG               # misaligned workspace
+    assert call_attn(sh, ws_bytes=1024) == L.SD_ERR_WORKSPACE
+    # empty batches succeed without any device work
+    assert call_attn(good_attn_shape(num_seqs=0, total_q=0)) == L.SD_OK
+    assert call_attn(good_attn_shape(total_q=0)) == L.SD_OK
+
+
+def good_accept_shape(**kw):
+    sh = L.SdAcceptShape(num_seqs=8, vocab=151936, total_q=124, max_block=24, dtype=L.SD_BF16)
+    for k, v in kw.items():
+        setattr(sh, k, v)
+    return sh
+
+
+def accept_ws(sh, T):
+    n = ctypes.c_size_t(0)
+    rc = L.lib().sd_accept_workspace_size(ctypes.byref(sh), ctypes.c_float(T), ctypes.byref(n))
+    return rc, n.value
+
+
+def test_accept_workspace_size_valid():
+    rc0, n0 = accept_ws(good_accept_shape(), 0.0)
+    rc1, n1 = accept_ws(good_accept_shape(), 1.0)
+    assert rc0 == rc1 == L.SD_OK and n1 >= n0 >= 64 * 1024
+
+
+@pytest.mark.parametrize("field,value,T,code", [
+    ("num_seqs", -1, 1.0, L.SD_ERR_INVALID_ARG),
+    ("vocab", 0, 1.0, L.SD_ERR_INVALID_ARG),
+    ("max_block", 0, 1.0, L.SD_ERR_INVALID_ARG),
+    ("max_block", 65, 0.0, L.SD_ERR_INVALID_ARG),
+    ("total_q", 7, 0.0, L.SD_ERR_INVALID_ARG),        # fewer rows than sequences
+    ("total_q", 8 * 24 + 1, 0.0, L.SD_ERR_INVALID_ARG),
+    ("dtype", 3, 0.0, L.SD_ERR_INVALID_ARG),
+    ("vocab", 1000, -1.0, L.SD_ERR_INVALID_ARG),
+    ("vocab", 1000, float("inf"), L.SD_ERR_INVALID_ARG),
+    ("vocab", 1000, float("nan"), L.SD_ERR_INVALID_ARG),
+])
+def test_accept_shape_errors(field, value, T, code):
+    rc, _ = accept_ws(good_accept_shape(**{field: value}), T)
+    assert rc == code
+
+
+def call_accept(sh, T, ptrs=None, ws_bytes=None, ws_ptr=256):
+    P = ctypes.c_void_p
+    p = dict(t=4096, d=8192, tok=16, u=32, bl=48, off=64, al=80, nt=96)
+    if ptrs:
+        p.update(ptrs)
+    if ws_bytes is None:
+        ws_bytes = accept_ws(sh, T)[1]
+    return L.lib().sd_accept(ctypes.byref(sh), P(p["t"]), P(p["d"]), P(p["tok"]), P(p["u"]), P(p["bl"]),
+                             P(p["off"]), ctypes.c_float(T), P(p["al"]), P(p["nt"]), P(ws_ptr), ws_bytes, None)
+
+
+def test_accept_call_errors_without_device():
+    sh = good_accept_shape()
+    assert call_accept(sh, 1.0, ptrs=dict(d=0)) == L.SD_ERR_INVALID_ARG    # T>0 needs draft logits
+    assert call_accept(sh, 1.0, ptrs=dict(u=0)) == L.SD_ERR_INVALID_ARG    # and uniforms
+    assert call_accept(sh, 0.0, ptrs=dict(tok=0)) == L.SD_ERR_INVALID_ARG
+    assert call_accept(sh, 0.0, ptrs=dict(t=4100)) == L.SD_ERR_INVALID_ARG
+    assert call_accept(sh, 1.0, ws_bytes=100) == L.SD_ERR_WORKSPACE
+    assert call_accept(good_accept_shape(num_seqs=0, total_q=0), 1.0) == L.SD_OK
+
+
+def test_workspace_init_errors():
+    P = ctypes.c_void_p
+    assert L.lib().sd_workspace_init(P(0), 64, None) == L.SD_ERR_INVALID_ARG
+    assert L.lib().sd_workspace_init(P(4100), 64, None) == L.SD_ERR_INVALID_ARG
+    assert L.lib().sd_workspace_init(P(4096), 63, None) == L.SD_ERR_INVALID_ARG
+    assert L.lib().sd_workspace_init(P(4096), 0, None) == L.SD_OK
+
+
+def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
+    monkeypatch.setattr(L, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(L, "_lib", None)
+    with pytest.raises(RuntimeError, match="missing"):
+        L.lib()

@@ -1,0 +1,137 @@
+"""GPU parity of sd_accept against the fp64 oracle on the same seeded inputs."""
+import numpy as np
+import pytest
+import scipy.stats
+import torch
+
+import gpu_util as G
+from paper_2606_31315_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("T", [0.0, 1.0])
+def test_tiny(T):
+    """Tiny step: V=1024 fp32, B=8; target ~ N(0,2^2), draft = target + N(0,0.5^2)."""
+    G.check_accept(W.c1_tiny(temperatures=(T,)).accept[T])
+
+
+@pytest.mark.parametrize("T", [0.0, 1.0])
+def test_qwen3_4b_verify(T):
+    """Qwen3-4B verify: V=151936 bf16, B=16, target ~ N(0,3^2), draft = target + N(0,1)."""
+    G.check_accept(W.c2_qwen3_4b_verify(temperatures=(T,)).accept[T])
+
+
+@pytest.mark.parametrize("T", [0.0, 1.0])
+def test_ragged_blocks(T):
+    """8 ragged blocks B in {8..24} over V=151936."""
+    G.check_accept(W.c3_ragged(temperatures=(T,), with_attn=False).accept[T])
+
+
+@pytest.mark.parametrize("T", [0.0, 1.0])
+def test_long_context_batch(T):
+    """32 sequences, B U{4..32}, V=151936."""
+    G.check_accept(W.c5_long_context(temperatures=(T,), with_attn=False).accept[T])
+
+
+def _many_seq_problem(seed, S, V, bl_range, dtype, T, target_sigma=2.0, noise_sigma=0.7, name=""):
+    rs = W._streams(seed)
+    bl = rs["B"].integers(bl_range[0], bl_range[1], endpoint=True, size=S).astype(np.int32)
+    return W.make_accept(rs, block_lens=bl, V=V, dtype=dtype, temperature=T, target_sigma=target_sigma,
+                         noise_sigma=noise_sigma, name=name)
+
+
+@pytest.mark.parametrize("T", [0.0, 1.0])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("V", [1, 7, 8, 1003, 4096, 50001])
+def test_vocab_edges(V, dtype, T):
+    """Vocabulary sizes below one vector, unaligned rows, exact multiples, many sequences and B=1 rows."""
+    p = _many_seq_problem(V + (7 if dtype == "bf16" else 0), 40, V, (1, 20), dtype, T, name=f"V{V}")
+    G.check_accept(p)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_greedy_ties_lowest_index(dtype):
+    """Integer-valued logits at V=151936: the maximum is tied in many rows, and across vocabulary
+    chunks; the lowest tied index must win, exactly as in the oracle."""
+    rs = W._streams(4242)
+    bl = np.array([16, 1, 9, 24, 5], dtype=np.int32)
+    p = W.make_accept(rs, block_lens=bl, V=151936, dtype=dtype, temperature=0.0, target_sigma=1.0,
+                      noise_sigma=0.0, name="ties")
+    t = torch.round(p.target.float() * 2).clamp(-6, 6).to(p.target.dtype)
+    p.target = t
+    # drafts: the highest tied index (rejected) for half the positions, the lowest (accepted) otherwise
+    tv = t.float().numpy()
+    toks = []
+    for s in range(len(bl)):
+        for j in range(int(bl[s]) - 1):
+            row = tv[p.q_offsets[s] + j]
+            idx = np.nonzero(row == row.max())[0]
+            toks.append(idx[-1] if (j % 3 == 2) else idx[0])
+    p.draft_tokens = np.array(toks, dtype=np.int32)
+    al, nt, ref = G.check_accept(p)
+    assert (ref.accept_len > 0).any()
+
+
+def test_identical_draft_accepts_everything():
+    rs = W._streams(31)
+    bl = np.array([12, 3, 7], dtype=np.int32)
+    p = W.make_accept(rs, block_lens=bl, V=32000, dtype="bf16", temperature=1.0, target_sigma=3.0,
+                      noise_sigma=0.0, name="identical")
+    al, nt, ref = G.check_accept(p)
+    assert (al == bl - 1).all()
+
+
+def test_temperature_two():
+    rs = W._streams(32)
+    bl = np.array([10, 14, 4, 20], dtype=np.int32)
+    p = W.make_accept(rs, block_lens=bl, V=151936, dtype="bf16", temperature=2.0, target_sigma=3.0,
+                      noise_sigma=1.0, name="T2")
+    G.check_accept(p)
+
+
+def test_lossless_chi2_on_gpu():
+    """Lossless property on the GPU's own draws (small V): committed tokens ~ target rows."""
+    V, B, N = 16, 4, 8000
+    rng = np.random.default_rng(99)
+    t = rng.normal(0, 1.5, (B, V)).astype(np.float32)
+    dl = (t[:B - 1] + rng.normal(0, 1.0, (B - 1, V))).astype(np.float32)
+
+    def sm(x):
+        e = np.exp(x - x.max())
+        return e / e.sum()
+
+    p = np.stack([sm(t[i].astype(np.float64)) for i in range(B)])
+    q = np.stack([sm(dl[i].astype(np.float64)) for i in range(B - 1)])
+    tok = np.stack([rng.choice(V, size=N, p=q[j]) for j in range(B - 1)], axis=1).astype(np.int32)
+    u = rng.random((N, B), dtype=np.float32)
+    bl = np.full(N, B, np.int32)
+    prob = W.AcceptProblem(S=N, V=V, block_lens=bl, q_offsets=W.offsets_from_lens(bl),
+                           target=torch.from_numpy(np.tile(t, (N, 1))), draft=torch.from_numpy(np.tile(dl, (N, 1))),
+                           draft_tokens=tok.reshape(-1), uniforms=u.reshape(-1), temperature=1.0, dtype="f32",
+                           name="chi2")
+    al, nt = G.run_accept(prob)
+    first = np.where(al >= 1, tok[:, 0], nt)
+    cnt = np.bincount(first, minlength=V)
+    assert scipy.stats.chisquare(cnt, p[0] * N).pvalue > 1e-3
+    m = al == B - 1
+    cnt = np.bincount(nt[m], minlength=V)
+    assert scipy.stats.chisquare(cnt, p[B - 1] * m.sum()).pvalue > 1e-3
+    alpha = np.minimum(p[:B - 1], q).sum(axis=1)
+    expect = sum(np.prod(alpha[:i + 1]) for i in range(B - 1))
+    assert abs(al.mean() - expect) < 4 * al.std() / np.sqrt(N)
+
+
+def test_repeated_calls_reuse_workspace():
+    import paper_2606_31315_amd as sd
+    big = W.c3_ragged(temperatures=(1.0,), with_attn=False).accept[1.0]
+    small = _many_seq_problem(8, 3, 151936, (2, 9), "bf16", 1.0, target_sigma=3.0, noise_sigma=1.0, name="small")
+    d = G.accept_to_device(big)
+    ws = torch.zeros(sd.accept_workspace_size(sd.accept_shape(d["t"], big.S, big.max_block), 1.0),
+                     dtype=torch.uint8, device=G.dev())
+    a1 = G.run_accept(big, d, workspace=ws)
+    ref = G.oracle_accept(small)
+    als, nts = G.run_accept(small, workspace=ws)
+    G.compare_accept(small, als, nts, ref)
+    a2 = G.run_accept(big, d, workspace=ws)
+    assert (a1[0] == a2[0]).all() and (a1[1] == a2[1]).all()

@@ -1,0 +1,107 @@
+"""GPU parity of sd_block_attn against the fp64 oracle on the same seeded inputs."""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import gpu_util as G
+from paper_2606_31315_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+CAUSAL, BIDIR = W.MASK_CAUSAL_IN_BLOCK, W.MASK_BIDIR_IN_BLOCK
+
+
+def test_tiny_fp32():
+    """Tiny CPU-checkable step: 4 q heads / 1 kv head, D=64, fp32, ctx 256, B=8, causal."""
+    G.check_attn(W.c1_tiny().attn)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_qwen3_4b_verify(dtype):
+    """Qwen3-4B verify step (32/8/128, ctx 2048, B=16, causal); fp32 inputs pin the mask at 1e-5."""
+    G.check_attn(W.c2_qwen3_4b_verify(temperatures=(), dtype=dtype).attn)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_ragged_blocks(dtype):
+    """8 sequences, ctx 4096, ragged B in {8..24}, causal; every output row compared."""
+    G.check_attn(W.c3_ragged(temperatures=(), dtype=dtype).attn)
+
+
+def test_drafter_bidirectional():
+    """16 sequences, ctx U{1024..8192}, B U{8..32}, bidirectional-in-block; every row compared."""
+    G.check_attn(W.c4_drafter().attn)
+
+
+def test_long_context_sampled_rows():
+    """32 sequences, ctx U{8192..32768}, B U{4..32}: sampled rows against the oracle."""
+    p = W.c5_long_context(with_accept=False).attn
+    G.check_attn(p, full=False, per_seq=8)
+
+
+@pytest.mark.parametrize("mode", [CAUSAL, BIDIR])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_block_dominant_mask_sensitivity(mode, dtype):
+    """In-block keys scaled so in-block scores dominate: an off-by-one in the in-block mask
+    moves the output by far more than the tolerance."""
+    rs = W._streams(77)
+    p = W.make_attn(rs, S=4, Hq=32, Hkv=8, D=128, ctx_lens=[2048, 700, 0, 1500], block_lens=[16, 9, 24, 1],
+                    dtype=dtype, mask_mode=mode, block_key_gain=6.0, value_gain=0.25, name="block_dominant")
+    G.check_attn(p)
+
+
+EDGE = [
+    # name, S, Hq, Hkv, D, ctx, B, dtype, mode
+    ("ctx0", 2, 8, 2, 128, [0, 0], [5, 16], "bf16", CAUSAL),
+    ("ctx0_bidir", 2, 8, 2, 128, [0, 3], [5, 16], "bf16", BIDIR),
+    ("B1_decode", 3, 32, 8, 128, [100, 4095, 1], [1, 1, 1], "bf16", CAUSAL),
+    ("B64_maxrows", 2, 32, 8, 128, [300, 2000], [64, 33], "bf16", CAUSAL),
+    ("B64_fp32", 1, 16, 4, 128, [129], [64], "f32", CAUSAL),
+    ("mha_G1", 2, 8, 8, 128, [77, 1030], [7, 12], "bf16", CAUSAL),
+    ("G8", 2, 32, 4, 128, [500, 1900], [16, 32], "bf16", BIDIR),
+    ("D64_bf16", 3, 16, 4, 64, [64, 65, 2000], [3, 16, 30], "bf16", CAUSAL),
+    ("D64_fp32", 3, 16, 4, 64, [64, 65, 2000], [3, 16, 30], "f32", BIDIR),
+    ("empty_block", 3, 8, 2, 128, [40, 50, 60], [4, 0, 6], "bf16", CAUSAL),
+    ("ragged_tail_fp32", 2, 8, 2, 128, [63, 1000], [1, 17], "f32", CAUSAL),
+    ("long_fp32", 1, 8, 2, 128, [9000], [12], "f32", CAUSAL),
+]
+
+
+@pytest.mark.parametrize("case", EDGE, ids=[c[0] for c in EDGE])
+def test_edge_cases(case):
+    name, S, Hq, Hkv, D, ctx, B, dtype, mode = case
+    rs = W._streams(zlib.crc32(name.encode()) % 10000)
+    p = W.make_attn(rs, S=S, Hq=Hq, Hkv=Hkv, D=D, ctx_lens=ctx, block_lens=B, dtype=dtype, mask_mode=mode,
+                    name=name)
+    G.check_attn(p)
+
+
+def test_explicit_scale():
+    rs = W._streams(91)
+    p = W.make_attn(rs, S=2, Hq=8, Hkv=2, D=128, ctx_lens=[300, 20], block_lens=[8, 3], dtype="f32",
+                    mask_mode=CAUSAL, name="scale")
+    p.scale = 0.05
+    G.check_attn(p)
+
+
+def test_repeated_calls_reuse_workspace():
+    """The merge counters return to zero after every call: a second call with the same workspace
+    and a smaller batch gives the oracle's answer again, and the first call's outputs reproduce bit-exactly."""
+    big = W.c3_ragged(temperatures=(), dtype="bf16").attn
+    d = G.attn_to_device(big)
+    import paper_2606_31315_amd as sd
+    ws = torch.zeros(sd.attn_workspace_size(sd.attn_shape(d["q"], d["k"], big.max_ctx, big.max_block)),
+                     dtype=torch.uint8, device=G.dev())
+    o1 = G.run_attn(big, d, workspace=ws).clone()
+    rs = W._streams(5)
+    small = W.make_attn(rs, S=3, Hq=32, Hkv=8, D=128, ctx_lens=[3000, 10, 2500], block_lens=[5, 9, 20],
+                        dtype="bf16", mask_mode=CAUSAL, name="small_after_big")
+    o_small = G.run_attn(small, workspace=ws).float().cpu().numpy()
+    import oracle
+    ref = oracle.block_attn(small.q, small.k_cache, small.v_cache, small.ctx_lens, small.block_lens,
+                            small.q_offsets, small.mask_mode)
+    assert np.abs(o_small - ref).max() < 2e-2
+    o2 = G.run_attn(big, d, workspace=ws)
+    assert torch.equal(o1, o2)
