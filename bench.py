@@ -162,7 +162,7 @@ def main():
         "verify_rows_per_s": round(a.total_q / (ms_per_step * 1e-3), 1),
         "committed_tokens_per_s": round(float((al_h + 1).sum()) / (ms_per_step * 1e-3), 1),
         "mean_accept_len": float(al_h.mean()),
-        "roofline": {"bound": "hbm", "kernel": "block_attn_kernel", "achieved": round(attn_gbps, 1),
+        "roofline": {"bound": "hbm", "kernel": "sd_block_attn (split + merge kernels)", "achieved": round(attn_gbps, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
                      "traffic": None},
     }

@@ -29,12 +29,10 @@
  *     live in device memory (ctx_lens, block_lens, q_offsets, tokens) cannot be
  *     checked on the host: values outside the documented ranges are undefined
  *     behaviour.
- *   - Workspace: each operation needs a device workspace of the size its
- *     *_workspace_size() reports.  The workspace must be zero-filled before its
- *     first use (sd_workspace_init, or any zero-filled allocation); every call
- *     leaves its counters zero again, so one workspace serves any number of later
- *     calls of any shape that fits it.  Calls that share a workspace must not
- *     overlap in time (use one stream, or one workspace per stream).
+ *   - Workspace: each operation needs device scratch memory of the size its
+ *     *_workspace_size() reports (partial results between the kernels of one
+ *     call).  Its contents on entry do not matter.  Calls that share a workspace
+ *     must not overlap in time (use one stream, or one workspace per stream).
  *   - Row-major layouts throughout; "[a, b, c]" lists dimensions outermost first.
  */
 #ifndef SD_BLOCK_H
@@ -72,13 +70,6 @@ const char *sd_last_error(void);
 /* Library version string, e.g. "sdblock 0.1 gfx950". */
 const char *sd_version(void);
 
-/*
- * Zero-fill `bytes` bytes of device memory at `workspace` on `stream` (a fill
- * kernel, so it may be recorded into a HIP graph).  `workspace` must be 16-byte
- * aligned; `bytes` a multiple of 4.
- */
-int sd_workspace_init(void *workspace, size_t bytes, void *stream);
-
 /* ==========================================================================
  * Block attention (Sec. 2.1: the drafter generates the B block tokens in parallel
  * by block-level diffusion; the target verifies the block in parallel).
@@ -114,7 +105,7 @@ int sd_block_attn_workspace_size(const sd_attn_shape *shape, size_t *bytes);
  *   block_lens      [S] int32                  block length B_s, 0 <= B_s <= max_block (0: no rows)
  *   q_offsets       [S + 1] int32              exclusive prefix sum of block_lens, q_offsets[S] = total_q
  *   mask_mode       SD_MASK_*
- *   workspace       >= sd_block_attn_workspace_size() bytes, 256-byte aligned, zeroed before first use
+ *   workspace       >= sd_block_attn_workspace_size() bytes, 256-byte aligned
  *
  * Host-checked preconditions: q, caches and out 16-byte aligned; max_ctx + max_block
  * <= Lmax; total_q <= S * max_block; (Hq/Hkv) * max_block <= 256.

@@ -18,7 +18,7 @@ SD_OK, SD_ERR_INVALID_ARG, SD_ERR_UNSUPPORTED, SD_ERR_WORKSPACE, SD_ERR_HIP = ra
 SD_F32, SD_BF16 = 0, 1
 SD_MASK_CAUSAL_IN_BLOCK, SD_MASK_BIDIR_IN_BLOCK = 0, 1
 
-EXPORTS = ["sd_last_error", "sd_version", "sd_workspace_init", "sd_block_attn_workspace_size", "sd_block_attn",
+EXPORTS = ["sd_last_error", "sd_version", "sd_block_attn_workspace_size", "sd_block_attn",
            "sd_accept_workspace_size", "sd_accept"]
 
 
@@ -56,8 +56,6 @@ def lib() -> ctypes.CDLL:
         L.sd_last_error.argtypes = []
         L.sd_version.restype = ctypes.c_char_p
         L.sd_version.argtypes = []
-        L.sd_workspace_init.restype = ctypes.c_int
-        L.sd_workspace_init.argtypes = [P, Z, P]
         L.sd_block_attn_workspace_size.restype = ctypes.c_int
         L.sd_block_attn_workspace_size.argtypes = [ctypes.POINTER(SdAttnShape), ctypes.POINTER(Z)]
         L.sd_block_attn.restype = ctypes.c_int
@@ -107,10 +105,8 @@ def _need(t: torch.Tensor, name: str, dtype=None, device=None):
 
 
 class Workspace:
-    """A zero-initialised device buffer per device, grown on demand.
-
-    The kernels leave their counters zero after every call, so the buffer stays
-    valid across calls; calls sharing it must be ordered (one stream)."""
+    """A device scratch buffer per device, grown on demand; calls sharing it must be
+    ordered (one stream)."""
 
     def __init__(self):
         self._bufs = {}
@@ -119,8 +115,8 @@ class Workspace:
         key = device.index if device.index is not None else torch.cuda.current_device()
         buf = self._bufs.get(key)
         if buf is None or buf.numel() < nbytes:
-            # 256-byte alignment comes from the caching allocator; zero fill is a torch kernel
-            buf = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=device)
+            # 256-byte alignment comes from the caching allocator
+            buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
             self._bufs[key] = buf
         return buf
 

@@ -7,19 +7,22 @@
 // first rejection draw the token from max(0, p_j - q_j); if every draft is accepted
 // draw the bonus token from the last target row.
 //
-// Kernels (gfx950):
-//   accept_stats   grid = (row, vocab chunk) over every target row (and every draft row
-//                  when T > 0).  One streaming pass of 16-byte loads per row chunk:
-//                  T = 0 keeps (max value, lowest index); T > 0 keeps an online
-//                  (max, sum of exp2((x - max) * log2e / T)) with one rescale per batch,
-//                  never per element.  The last chunk of a sequence to finish merges the
-//                  partials, tests every drafted position at once (one lane per position,
-//                  a wavefront ballot finds the first rejection) and writes accept_len,
-//                  and at T = 0 also the next token.
-//   accept_sample  T > 0 only.  grid = (sequence, vocab chunk) over the one row (pair)
-//                  the finalize selected: chunk masses of the residual (and of p for the
-//                  degenerate fallback), then the last chunk to finish locates the chunk
-//                  holding u* times the total and scans it in vocabulary order.
+// Kernels (gfx950); kernel boundaries are the only cross-workgroup synchronisation
+// (an agent-scope fence per workgroup costs an L2 writeback on gfx950):
+//   accept_stats_kernel     grid = (row, vocab chunk) over every target row, and every
+//                           draft row when T > 0.  One streaming pass of 16-byte loads:
+//                           T = 0 keeps (max value, lowest index); T > 0 keeps an online
+//                           (max, sum of exp2((x - max) log2e / T)) with one rescale per
+//                           batch of loads, never per element.
+//   accept_greedy_kernel    T = 0, one wavefront per sequence: merge the chunk partials,
+//                           lane i tests drafted position i, a ballot finds the first
+//                           rejection; writes accept_len and the next token.
+//   accept_sample_kernel    T > 0, grid = (sequence, vocab chunk): every workgroup redoes
+//                           the small per-sequence decision (lane i tests position i,
+//                           ballot), then sums the residual max(0, p - q) (or p at the
+//                           bonus row) over its chunk.
+//   accept_scan_kernel      T > 0, one workgroup per sequence: locate the chunk holding
+//                           u* times the total mass and scan it in vocabulary order.
 #pragma once
 
 #include <limits.h>
@@ -40,8 +43,6 @@ struct AcceptArgs {
   float2 *stats;      // [rows, nch]: (max, sum) at T > 0; (max value, index bits) at T = 0
   float4 *seqinfo;    // [S, 2]: (row, residual?, target max, 1/target sum), (draft max, 1/draft sum, 0, 0)
   double2 *samp;      // [S, nch2]: (residual mass, p mass) per chunk
-  unsigned *cnt1;     // [S]
-  unsigned *cnt2;     // [S]
   int S, V, total_q, nch, nch2;
   float c;            // log2(e) / T (T > 0)
 };
@@ -131,21 +132,16 @@ __device__ __forceinline__ void lse_merge(float &m, float &sum, float m2, float 
 constexpr int kUnroll = 4;  // 16-byte vectors in flight per thread per batch
 
 template <bool BF16, bool SAMPLE>
-__device__ void accept_finalize(const AcceptArgs &a, int s);
-
-template <bool BF16, bool SAMPLE>
 __global__ __launch_bounds__(256) void accept_stats_kernel(AcceptArgs a) {
   constexpr int VEC = BF16 ? 8 : 4;
   __shared__ float sh_v[4];
   __shared__ float sh_s[4];
   __shared__ int sh_i[4];
-  __shared__ int s_last;
 
   const int row = blockIdx.x / a.nch;
   const int c = blockIdx.x % a.nch;
   const bool is_draft = row >= a.total_q;
   const int rr = is_draft ? row - a.total_q : row;
-  const int s = owner_of_row(a.q_offsets, a.S, rr, is_draft ? 1 : 0);
   const void *base = is_draft ? a.draft : a.target;
   const long long a0 = (long long)rr * a.V;
   const RowChunk ch = row_chunk<VEC>(a0, a.V, c, a.nch);
@@ -239,77 +235,90 @@ __global__ __launch_bounds__(256) void accept_stats_kernel(AcceptArgs a) {
     a.stats[(size_t)row * a.nch + c] = SAMPLE ? float2{bv, sum} : float2{bv, __int_as_float(bi)};
   }
 
-  // the last chunk of this sequence to finish runs the decision
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) {
-    const int B = a.block_lens[s];
-    const unsigned rows_s = (unsigned)(SAMPLE ? 2 * B - 1 : B);
-    s_last = (atomicAdd(&a.cnt1[s], 1u) == rows_s * (unsigned)a.nch - 1u);
-  }
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-  if (tid < 64) accept_finalize<BF16, SAMPLE>(a, s);
-  if (tid == 0) atomicExch(&a.cnt1[s], 0u);
 }
 
-// Runs on wavefront 0 of the last workgroup of sequence s: lane i handles block position i.
-template <bool BF16, bool SAMPLE>
-__device__ void accept_finalize(const AcceptArgs &a, int s) {
+// Greedy decision for sequence s on one wavefront: lane i merges the chunk partials of
+// target row i into its lowest-index argmax and tests drafted position i.
+template <bool BF16>
+__global__ __launch_bounds__(64) void accept_greedy_kernel(AcceptArgs a) {
+  const int s = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int B = a.block_lens[s];
+  const int n = B - 1;
+  const int off = a.q_offsets[s];
+  const int tok = (lane < n) ? a.draft_tokens[off - s + lane] : 0;
+  int gi = INT_MAX;
+  if (lane < B) {
+    const float2 *st = a.stats + (size_t)(off + lane) * a.nch;
+    float gv = -INFINITY;
+    for (int c0 = 0; c0 < a.nch; c0 += 8) {
+      float2 v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) v[k] = (c0 + k < a.nch) ? st[c0 + k] : float2{-INFINITY, __int_as_float(INT_MAX)};
+#pragma unroll
+      for (int k = 0; k < 8; ++k) argmax_merge(gv, gi, v[k].x, __float_as_int(v[k].y));
+    }
+    if (gi == INT_MAX) gi = 0;  // every logit -inf: all tie, lowest index
+  }
+  const bool rejects = (lane < n) && (tok != gi);
+  const unsigned long long rej = __ballot(rejects);
+  const int acc = rej ? (__ffsll((long long)rej) - 1) : max(n, 0);
+  const int next = __shfl(gi, acc, 64);
+  if (lane == 0) {
+    a.accept_len[s] = acc;
+    a.next_token[s] = next;
+  }
+}
+
+// Merge a row's chunk partials (max, sum) with the loads issued in batches of 8.
+__device__ __forceinline__ void merge_lse_partials(const float2 *st, int nch, float c, float &m, float &sum) {
+  for (int c0 = 0; c0 < nch; c0 += 8) {
+    float2 v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = (c0 + k < nch) ? st[c0 + k] : float2{-INFINITY, 0.f};
+#pragma unroll
+    for (int k = 0; k < 8; ++k) lse_merge(m, sum, v[k].x, v[k].y, c);
+  }
+}
+
+// Sampling decision for sequence s on one wavefront (lane i = block position i).
+// Returns, in every lane, the accepted length and the normalisers of the selected row.
+struct SampleSel {
+  int acc;
+  bool residual;
+  float tm, ts, qm, qs;
+};
+
+template <bool BF16>
+__device__ SampleSel sampling_decision(const AcceptArgs &a, int s) {
   const int lane = threadIdx.x & 63;
   const int B = a.block_lens[s];
   const int n = B - 1;
   const int off = a.q_offsets[s];
   const int doff = off - s;
+  float tm = -INFINITY, ts = 0.f, qm = -INFINITY, qs = 0.f;
   bool rejects = false;
-  float tm = -INFINITY, ts = 0.f;  // target row stats (SAMPLE)
-  float qm = -INFINITY, qs = 0.f;  // draft row stats (SAMPLE)
-  int gi = INT_MAX;                 // target row argmax (greedy)
-  if (lane < B) {
-    const float2 *st = a.stats + (size_t)(off + lane) * a.nch;
-    if constexpr (SAMPLE) {
-      for (int cc = 0; cc < a.nch; ++cc) lse_merge(tm, ts, st[cc].x, st[cc].y, a.c);
-    } else {
-      float gv = -INFINITY;
-      for (int cc = 0; cc < a.nch; ++cc) argmax_merge(gv, gi, st[cc].x, __float_as_int(st[cc].y));
-      if (gi == INT_MAX) gi = 0;  // every logit -inf: all tie, lowest index
-    }
-  }
+  // issue the draft token load first: the two logit gathers depend on it
+  const int d = (lane < n) ? a.draft_tokens[doff + lane] : 0;
+  if (lane < B) merge_lse_partials(a.stats + (size_t)(off + lane) * a.nch, a.nch, a.c, tm, ts);
   if (lane < n) {
-    const int d = a.draft_tokens[doff + lane];
-    if constexpr (SAMPLE) {
-      const float2 *sq = a.stats + (size_t)(a.total_q + doff + lane) * a.nch;
-      for (int cc = 0; cc < a.nch; ++cc) lse_merge(qm, qs, sq[cc].x, sq[cc].y, a.c);
-      const float td = load_elem<BF16>(a.target, (long long)(off + lane) * a.V + d);
-      const float dd = load_elem<BF16>(a.draft, (long long)(doff + lane) * a.V + d);
-      // rho = p(d) / q(d) = exp2((td - tm) c - (dd - qm) c) * qs / ts
-      const double lr = (double)((td - tm) * a.c) - (double)((dd - qm) * a.c);
-      const double rho = (qs > 0.f && dd != -INFINITY) ? exp2(lr) * (double)qs / (double)ts : INFINITY;
-      rejects = !((double)a.uniforms[off + lane] < rho);
-    } else {
-      rejects = (d != gi);
-    }
+    merge_lse_partials(a.stats + (size_t)(a.total_q + doff + lane) * a.nch, a.nch, a.c, qm, qs);
+    const float td = load_elem<BF16>(a.target, (long long)(off + lane) * a.V + d);
+    const float dd = load_elem<BF16>(a.draft, (long long)(doff + lane) * a.V + d);
+    // rho = p(d) / q(d) = exp2((td - tm) c - (dd - qm) c) * qs / ts; q(d) = 0 accepts
+    const double lr = (double)((td - tm) * a.c) - (double)((dd - qm) * a.c);
+    const double rho = (dd != -INFINITY) ? exp2(lr) * (double)qs / (double)ts : INFINITY;
+    rejects = !((double)a.uniforms[off + lane] < rho);
   }
   const unsigned long long rej = __ballot(rejects);
-  const int acc = rej ? (__ffsll((long long)rej) - 1) : max(n, 0);
-  if constexpr (SAMPLE) {
-    // hand the selected row's normalisers to the sampling pass
-    const float tm_j = __shfl(tm, acc, 64), ts_j = __shfl(ts, acc, 64);
-    const float qm_j = __shfl(qm, acc, 64), qs_j = __shfl(qs, acc, 64);
-    if (lane == 0) {
-      a.accept_len[s] = acc;
-      const bool residual = acc < n;
-      a.seqinfo[2 * s] = float4{__int_as_float(acc), residual ? 1.f : 0.f, tm_j, 1.f / ts_j};
-      a.seqinfo[2 * s + 1] = float4{residual ? qm_j : 0.f, residual ? 1.f / qs_j : 0.f, 0.f, 0.f};
-    }
-  } else {
-    const int next = __shfl(gi, acc, 64);
-    if (lane == 0) {
-      a.accept_len[s] = acc;
-      a.next_token[s] = next;
-    }
-  }
+  SampleSel r;
+  r.acc = rej ? (__ffsll((long long)rej) - 1) : max(n, 0);
+  r.residual = r.acc < n;
+  r.tm = __shfl(tm, r.acc, 64);
+  r.ts = __shfl(ts, r.acc, 64);
+  r.qm = __shfl(qm, r.acc, 64);
+  r.qs = __shfl(qs, r.acc, 64);
+  return r;
 }
 
 // Residual / target mass of one element in the sampling pass.  si0 = (row, residual?,
@@ -329,16 +338,27 @@ template <bool BF16>
 __global__ __launch_bounds__(256) void accept_sample_kernel(AcceptArgs a) {
   constexpr int VEC = BF16 ? 8 : 4;
   __shared__ double sh_r[4], sh_p[4];
-  __shared__ double sh_scan[256];
-  __shared__ int sh_lp[4];
-  __shared__ int s_last, s_chunk, s_use_p, s_found;
-  __shared__ double s_target;
+  __shared__ float4 sh_si[2];
 
   const int s = blockIdx.x / a.nch2;
   const int c = blockIdx.x % a.nch2;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int B = a.block_lens[s];
-  const float4 si0 = a.seqinfo[2 * s], si1 = a.seqinfo[2 * s + 1];
+  if (wave == 0) {
+    const SampleSel sel = sampling_decision<BF16>(a, s);
+    if (lane == 0) {
+      const float4 si0{__int_as_float(sel.acc), sel.residual ? 1.f : 0.f, sel.tm, 1.f / sel.ts};
+      const float4 si1{sel.residual ? sel.qm : 0.f, sel.residual ? 1.f / sel.qs : 0.f, 0.f, 0.f};
+      sh_si[0] = si0;
+      sh_si[1] = si1;
+      if (c == 0) {
+        a.accept_len[s] = sel.acc;
+        a.seqinfo[2 * s] = si0;
+        a.seqinfo[2 * s + 1] = si1;
+      }
+    }
+  }
+  __syncthreads();
+  const float4 si0 = sh_si[0], si1 = sh_si[1];
   const int j = __float_as_int(si0.x);
   const int off = a.q_offsets[s];
   const long long ta0 = (long long)(off + j) * a.V;
@@ -358,7 +378,7 @@ __global__ __launch_bounds__(256) void accept_sample_kernel(AcceptArgs a) {
     }
   };
   scalar_range(ch.hb, ch.he);
-  // The draft row shares the target row's vector alignment only when (da0 - ta0) is a
+  // The draft row shares the target row's vector alignment only when (ta0 - da0) is a
   // multiple of VEC; otherwise its elements are read one by one.
   const bool draft_vec = ((ta0 - da0) % VEC) == 0;
   const u32x4 *tv = reinterpret_cast<const u32x4 *>(a.target);
@@ -398,95 +418,140 @@ __global__ __launch_bounds__(256) void accept_sample_kernel(AcceptArgs a) {
   if (tid == 0)
     a.samp[(size_t)s * a.nch2 + c] =
         double2{sh_r[0] + sh_r[1] + sh_r[2] + sh_r[3], sh_p[0] + sh_p[1] + sh_p[2] + sh_p[3]};
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) s_last = (atomicAdd(&a.cnt2[s], 1u) == (unsigned)a.nch2 - 1u);
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
+}
 
-  // ---- last chunk of this sequence: locate the chunk holding u* times the total ----
+constexpr int kScanRun = 24;  // elements per thread in the final scan (chunks hold <= 4096 + 7)
+
+// Block-wide inclusive scan of one double per thread (256 threads): wavefront shuffles,
+// then the wavefront totals through LDS.  Returns the inclusive prefix; *total gets the sum.
+__device__ __forceinline__ double block_scan_incl(double v, double *sh4, double *total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const double u = __shfl_up(v, o, 64);
+    if (lane >= o) v += u;
+  }
+  if (lane == 63) sh4[wave] = v;
+  __syncthreads();
+  double before = 0.0;
+  for (int w2 = 0; w2 < wave; ++w2) before += sh4[w2];
+  *total = sh4[0] + sh4[1] + sh4[2] + sh4[3];
+  __syncthreads();
+  return v + before;
+}
+
+// Final inverse-CDF draw for sequence s: locate the chunk holding u* times the total
+// mass (block-wide scan of the chunk masses), then scan that chunk in vocabulary order
+// with a contiguous run of elements per thread, held in registers.
+template <bool BF16>
+__global__ __launch_bounds__(256) void accept_scan_kernel(AcceptArgs a) {
+  constexpr int VEC = BF16 ? 8 : 4;
+  __shared__ double sh4[4];
+  __shared__ int s_chunk, s_lastpos, s_found;
+
+  const int s = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int B = a.block_lens[s];
+  const int off = a.q_offsets[s];
+  const float4 si0 = a.seqinfo[2 * s], si1 = a.seqinfo[2 * s + 1];
+  const int j = __float_as_int(si0.x);
+  const bool residual = si0.y != 0.f;
+  const long long ta0 = (long long)(off + j) * a.V;
+  const long long da0 = (long long)(off - s + j) * a.V;
+  const double2 *cs = a.samp + (size_t)s * a.nch2;
+  const double ustar = (double)a.uniforms[off + B - 1];
+
+  // totals of the residual and of p (p is the fallback when the residual has no mass)
+  double tr = 0.0, tp = 0.0;
+  for (int k = tid; k < a.nch2; k += 256) {
+    const double2 c = cs[k];
+    tr += c.x;
+    tp += c.y;
+  }
+  double tot_r, tot_p;
+  block_scan_incl(tr, sh4, &tot_r);
+  block_scan_incl(tp, sh4, &tot_p);
+  const bool use_p = !(tot_r > 0.0);
+  const double tot = use_p ? tot_p : tot_r;
+  const double tgt = ustar * tot;
   if (tid == 0) {
-    const double2 *cs = a.samp + (size_t)s * a.nch2;
-    double tot = 0.0;
-    for (int k = 0; k < a.nch2; ++k) tot += cs[k].x;
-    const int use_p = !(tot > 0.0);  // residual without mass (rounding only): draw from p
-    if (use_p) {
-      tot = 0.0;
-      for (int k = 0; k < a.nch2; ++k) tot += cs[k].y;
-    }
-    const double tgt = (double)a.uniforms[off + B - 1] * tot;
-    double pre = 0.0;
-    int cstar = -1, lastpos = 0;
-    for (int k = 0; k < a.nch2; ++k) {
-      const double m = use_p ? cs[k].y : cs[k].x;
-      if (m > 0.0) lastpos = k;
-      if (cstar < 0 && pre + m > tgt) {
-        cstar = k;
-        s_target = tgt - pre;
-      }
-      pre += m;
-    }
-    if (cstar < 0) {  // rounding put u* S at or past the total: last token with mass
-      cstar = lastpos;
-      s_target = INFINITY;
-    }
-    s_chunk = cstar;
-    s_use_p = use_p;
+    s_chunk = INT_MAX;
+    s_lastpos = 0;
     s_found = INT_MAX;
   }
   __syncthreads();
+  // locate the chunk: first k whose cumulative mass exceeds tgt
+  double carry = 0.0, chunk_excl = 0.0;
+  for (int base = 0; base < a.nch2; base += 256) {
+    const int k = base + tid;
+    const double m = (k < a.nch2) ? (use_p ? cs[k].y : cs[k].x) : 0.0;
+    double seg;
+    const double incl = block_scan_incl(m, sh4, &seg) + carry;
+    if (m > 0.0) {
+      atomicMax(&s_lastpos, k);
+      if (incl - m <= tgt && tgt < incl) atomicMin(&s_chunk, k);
+    }
+    carry += seg;
+  }
+  __syncthreads();
+  const bool found_chunk = s_chunk != INT_MAX;
+  const int cstar = found_chunk ? s_chunk : s_lastpos;  // rounding: last chunk with mass
+  // mass before chunk cstar (recomputed the same way by every thread)
+  {
+    double before = 0.0;
+    for (int k = tid; k < cstar; k += 256) before += use_p ? cs[k].y : cs[k].x;
+    double t;
+    block_scan_incl(before, sh4, &t);
+    chunk_excl = t;
+  }
+  const double ctgt = found_chunk ? tgt - chunk_excl : INFINITY;
 
-  // ---- scan that chunk in vocabulary order: contiguous runs per thread ----
-  const bool use_q = residual && !s_use_p;
-  const RowChunk cc = row_chunk<VEC>(ta0, a.V, s_chunk, a.nch2);
+  // scan chunk cstar: this thread's contiguous run, masses kept in registers
+  const bool use_q = residual && !use_p;
+  const RowChunk cc = row_chunk<VEC>(ta0, a.V, cstar, a.nch2);
   const int len = cc.e1 - cc.e0;
-  const int run = (len + 255) / 256;
+  const int run = (len + 255) / 256;  // <= kScanRun for chunks of at most 4096 + 7 elements
   const int e_beg = min(cc.e0 + tid * run, cc.e1), e_end = min(e_beg + run, cc.e1);
-  auto mass = [&](int e) -> float {
-    const float t = load_elem<BF16>(a.target, ta0 + e);
-    const float q = use_q ? load_elem<BF16>(a.draft, da0 + e) : 0.f;
-    float r, p;
-    sample_masses(t, q, si0, use_q ? si1 : si1, a.c, r, p);
-    return use_q ? r : p;
-  };
+  float mass[kScanRun];
   double own = 0.0;
   int last_pos_own = -1;
-  for (int e = e_beg; e < e_end; ++e) {
-    const float m = mass(e);
-    own += (double)m;
-    if (m > 0.f) last_pos_own = e;
-  }
-  sh_scan[tid] = own;  // inclusive Hillis-Steele scan of the per-thread masses
-  __syncthreads();
-  for (int st = 1; st < 256; st <<= 1) {
-    const double v = (tid >= st) ? sh_scan[tid - st] : 0.0;
-    __syncthreads();
-    sh_scan[tid] += v;
-    __syncthreads();
-  }
-  const double incl = sh_scan[tid];
-  const double excl = incl - own;
-  const double tgt = s_target;
-  if (tgt != INFINITY && excl <= tgt && tgt < incl) {
-    double cum = excl;
-    int found = last_pos_own;
-    for (int e = e_beg; e < e_end; ++e) {
-      cum += (double)mass(e);
-      if (cum > tgt) { found = e; break; }
+#pragma unroll
+  for (int k = 0; k < kScanRun; ++k) {
+    const int e = e_beg + k;
+    float t = 0.f, q = 0.f;
+    if (e < e_end) {
+      t = load_elem<BF16>(a.target, ta0 + e);
+      if (use_q) q = load_elem<BF16>(a.draft, da0 + e);
     }
+    float r, p;
+    sample_masses(t, q, si0, si1, a.c, r, p);
+    mass[k] = (e < e_end) ? (use_q ? r : p) : 0.f;
+    own += (double)mass[k];
+    if (mass[k] > 0.f) last_pos_own = e;
+  }
+  double dummy;
+  const double incl = block_scan_incl(own, sh4, &dummy);
+  const double excl = incl - own;
+  if (ctgt != INFINITY && excl <= ctgt && ctgt < incl) {
+    double cum = excl;
+    int found = -1;
+#pragma unroll
+    for (int k = 0; k < kScanRun; ++k) {
+      cum += (double)mass[k];
+      if (found < 0 && cum > ctgt && e_beg + k < e_end) found = e_beg + k;
+    }
+    if (found < 0) found = last_pos_own;  // rounding: the run's last token with mass
     if (found >= 0) atomicMin(&s_found, found);
   }
   int lp = last_pos_own;
 #pragma unroll
   for (int msk = 1; msk < 64; msk <<= 1) lp = max(lp, __shfl_xor(lp, msk, 64));
-  if (lane == 0) sh_lp[wave] = lp;
+  if (lane == 0) sh4[wave] = (double)lp;
   __syncthreads();
   if (tid == 0) {
     int tok = s_found;
-    if (tok == INT_MAX) tok = max(max(sh_lp[0], sh_lp[1]), max(sh_lp[2], sh_lp[3]));
+    if (tok == INT_MAX) tok = (int)fmax(fmax(sh4[0], sh4[1]), fmax(sh4[2], sh4[3]));
     a.next_token[s] = tok;
-    atomicExch(&a.cnt2[s], 0u);
   }
 }
 

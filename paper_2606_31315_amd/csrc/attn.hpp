@@ -17,9 +17,12 @@
 //     O^T += V^T P^T MFMA needs, so P never leaves registers.
 //   * Online softmax in the log2 domain (scale * log2 e folded into one FMA), with
 //     per-lane partial row sums reduced once at the end.
-//   * Splits of one (sequence, kv head) are dealt to one XCD; the last split to finish
-//     (agent-scope fence + counter) merges the fp32 partials and writes the output, so
-//     one launch does the whole operation.
+//   * A sequence whose keys fit one split writes its output directly.  Otherwise each
+//     split writes fp32 partials (unnormalised O, row max, row sum) and a second launch,
+//     block_attn_merge_kernel, combines them.  The kernel boundary is the only
+//     cross-workgroup synchronisation: an in-kernel "last workgroup merges" scheme needs
+//     agent-scope release fences, which on gfx950 write back the XCD's L2 and cost far
+//     more than the second launch.
 #pragma once
 
 #include "common.hpp"
@@ -36,7 +39,6 @@ struct AttnArgs {
   const int *q_offsets;
   float *part_o;      // [n_work, Mpad, D] unnormalised partial outputs
   float2 *part_ml;    // [n_work, Mpad]    (row max in log2 units, row sum)
-  unsigned *counters; // [S * Hkv] splits finished, reset to 0 by the merging workgroup
   int S, Hq, Hkv, G, Lmax;
   int split_len;      // keys per split, multiple of the key tile
   int max_splits;     // splits per (sequence, kv head) at the host-known maximum length
@@ -67,11 +69,10 @@ __device__ __forceinline__ void load_k_tile(u32x4 (&kr)[(AttnCfg<BF16>::KT * D *
   for (int j = 0; j < N; ++j) {
     const int c = tid + 256 * j;
     const int row = c / CPR, col = c % CPR;
-    const int key = key0 + row;
-    if (key < key_end)
-      kr[j] = *reinterpret_cast<const u32x4 *>(kbase + ((size_t)key * D) * AttnCfg<BF16>::EB + col * 16);
-    else
-      kr[j] = u32x4{0, 0, 0, 0};
+    // keys past the split end re-read the last valid key: finite data whose score the
+    // mask removes, and no branch around the load
+    const int key = min(key0 + row, key_end - 1);
+    kr[j] = *reinterpret_cast<const u32x4 *>(kbase + ((size_t)key * D) * AttnCfg<BF16>::EB + col * 16);
   }
 }
 
@@ -107,15 +108,10 @@ __device__ __forceinline__ void load_v_tile(VItem<BF16, D> &vi, const char *vbas
   const int kg = tid / (D / 8), col = tid % (D / 8);
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
-    const int key = key0 + kg * 4 + r;
+    const int key = min(key0 + kg * 4 + r, key_end - 1);  // masked keys get weight 0
 #pragma unroll
-    for (int h = 0; h < VPK; ++h) {
-      if (key < key_end)
-        vi.r[r * VPK + h] =
-            *reinterpret_cast<const u32x4 *>(vbase + ((size_t)key * D + col * 8) * C::EB + h * 16);
-      else
-        vi.r[r * VPK + h] = u32x4{0, 0, 0, 0};
-    }
+    for (int h = 0; h < VPK; ++h)
+      vi.r[r * VPK + h] = *reinterpret_cast<const u32x4 *>(vbase + ((size_t)key * D + col * 8) * C::EB + h * 16);
   }
 }
 
@@ -169,7 +165,6 @@ __global__ __launch_bounds__(256) void block_attn_kernel(AttnArgs a) {
   constexpr int NDT = D / 16;                  // 16-wide output column tiles
   __shared__ __attribute__((aligned(16))) char ks[KT * KPITCH];
   __shared__ __attribute__((aligned(16))) char vts[D * VPITCH];
-  __shared__ int s_last;
 
   const int w = xcd_logical_id(blockIdx.x, a.per_xcd);
   if (w >= a.n_work) return;
@@ -212,7 +207,7 @@ __global__ __launch_bounds__(256) void block_attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) oacc[j][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     const bool valid = (mt < nmt) && (m < M);
-    row_i[j] = valid ? m / a.G : 0x3fffffff;
+    row_i[j] = valid ? m / a.G : 0;
     const char *qrow = valid ? reinterpret_cast<const char *>(a.q) +
                                    ((size_t)(qoff + m / a.G) * a.Hq + g * a.G + m % a.G) * D * EB
                              : nullptr;
@@ -262,8 +257,7 @@ __global__ __launch_bounds__(256) void block_attn_kernel(AttnArgs a) {
           const bf16x8 av = *reinterpret_cast<const bf16x8 *>(krow + (st * 32 + kgrp * 8) * EB);
 #pragma unroll
           for (int j = 0; j < MT; ++j)
-            if (wave + 4 * j < nmt)
-              sacc[j][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qop[j].v[st], sacc[j][sb], 0, 0, 0);
+            sacc[j][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qop[j].v[st], sacc[j][sb], 0, 0, 0);
         }
       } else {
 #pragma unroll
@@ -273,16 +267,16 @@ __global__ __launch_bounds__(256) void block_attn_kernel(AttnArgs a) {
           for (int e = 0; e < 4; ++e)
 #pragma unroll
             for (int j = 0; j < MT; ++j)
-              if (wave + 4 * j < nmt)
-                sacc[j][sb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[e], qop[j].v[t4][e], sacc[j][sb], 0, 0, 0);
+              sacc[j][sb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[e], qop[j].v[t4][e], sacc[j][sb], 0, 0, 0);
         }
       }
     }
 
     // mask + online softmax (log2 domain); P kept in registers
+    // every m-tile slot runs the same code; slots past the sequence's rows hold zero
+    // queries and are never written out
 #pragma unroll
     for (int j = 0; j < MT; ++j) {
-      if (wave + 4 * j >= nmt) continue;
       const int lim = a.causal ? min(k1, ctx + row_i[j] + 1) : k1;  // keys < lim are visible
       float tmax = -INFINITY;
 #pragma unroll
@@ -335,8 +329,7 @@ __global__ __launch_bounds__(256) void block_attn_kernel(AttnArgs a) {
           const bf16x8 av = __builtin_bit_cast(bf16x8, (u32x4{lo.x, lo.y, hi.x, hi.y}));
 #pragma unroll
           for (int j = 0; j < MT; ++j)
-            if (wave + 4 * j < nmt)
-              oacc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, pb[j], oacc[j][dt], 0, 0, 0);
+            oacc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, pb[j], oacc[j][dt], 0, 0, 0);
         }
       }
     } else {
@@ -349,8 +342,7 @@ __global__ __launch_bounds__(256) void block_attn_kernel(AttnArgs a) {
           for (int r = 0; r < 4; ++r)
 #pragma unroll
             for (int j = 0; j < MT; ++j)
-              if (wave + 4 * j < nmt)
-                oacc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[r], sacc[j][sb][r], oacc[j][dt], 0, 0, 0);
+              oacc[j][dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[r], sacc[j][sb][r], oacc[j][dt], 0, 0, 0);
         }
     }
   }
@@ -387,7 +379,7 @@ __global__ __launch_bounds__(256) void block_attn_kernel(AttnArgs a) {
     return;
   }
 
-  // ---- several splits: write this split's partials, last one merges ----
+  // ---- several splits: write this split's partials for the merge launch ----
   const size_t wrow = (size_t)w * a.Mpad;
 #pragma unroll
   for (int j = 0; j < MT; ++j) {
@@ -399,36 +391,48 @@ __global__ __launch_bounds__(256) void block_attn_kernel(AttnArgs a) {
     for (int dt = 0; dt < NDT; ++dt) *reinterpret_cast<f32x4 *>(prow + dt * 16 + kgrp * 4) = oacc[j][dt];
     if (kgrp == 0) a.part_ml[wrow + m] = float2{m_run[j], l_run[j]};
   }
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) s_last = (atomicAdd(&a.counters[sg], 1u) == (unsigned)(nsplit - 1));
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
+}
 
-  const size_t wbase = (size_t)(sg * a.max_splits) * a.Mpad;  // work item of split 0
-  constexpr int D4 = D / 4;
-  for (int idx = tid; idx < M * D4; idx += 256) {
-    const int m = idx / D4, d = (idx % D4) * 4;
-    float mx = -INFINITY;
-    for (int sp = 0; sp < nsplit; ++sp) mx = fmaxf(mx, a.part_ml[wbase + (size_t)sp * a.Mpad + m].x);
-    float lsum = 0.f;
-    f32x4 acc{0.f, 0.f, 0.f, 0.f};
-    for (int sp = 0; sp < nsplit; ++sp) {
-      const size_t r = wbase + (size_t)sp * a.Mpad + m;
-      const float2 ml = a.part_ml[r];
-      const float wgt = (ml.x == -INFINITY) ? 0.f : fast_exp2(ml.x - mx);
-      lsum += wgt * ml.y;
-      acc += wgt * *reinterpret_cast<const f32x4 *>(a.part_o + r * D + d);
-    }
-    const f32x4 o = acc * (1.f / lsum);
-    char *orow = out_row_ptr(m);
-    if constexpr (BF16)
-      *reinterpret_cast<uint2 *>(orow + d * EB) = uint2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
-    else
-      *reinterpret_cast<f32x4 *>(orow + d * EB) = o;
+// Merge of the split partials: workgroup (s, g, row block) combines
+//   O = sum_sp 2^(m_sp - M) O_sp / sum_sp 2^(m_sp - M) l_sp,  M = max_sp m_sp
+// for RB rows of the (sequence, kv head) group, D/4 threads per row, one float4 each.
+template <bool BF16, int D>
+__global__ __launch_bounds__(256) void block_attn_merge_kernel(AttnArgs a) {
+  constexpr int EB = BF16 ? 2 : 4;
+  constexpr int TPR = D / 4;       // threads per row
+  constexpr int RB = 256 / TPR;    // rows per workgroup
+  const int nrb = a.Mpad / RB + ((a.Mpad % RB) ? 1 : 0);
+  const int rb = blockIdx.x % nrb;
+  const int sg = blockIdx.x / nrb;
+  const int s = sg / a.Hkv, g = sg % a.Hkv;
+  const int ctx = a.ctx_lens[s];
+  const int B = a.block_lens[s];
+  if (B <= 0) return;
+  const int nsplit = (ctx + B + a.split_len - 1) / a.split_len;
+  if (nsplit <= 1) return;  // written directly by the split kernel
+  const int M = a.G * B;
+  const int m = rb * RB + threadIdx.x / TPR;
+  if (m >= M) return;
+  const int d = (threadIdx.x % TPR) * 4;
+  const size_t wbase = (size_t)sg * a.max_splits * a.Mpad + m;  // row m of split 0
+  float mx = -INFINITY;
+  for (int sp = 0; sp < nsplit; ++sp) mx = fmaxf(mx, a.part_ml[wbase + (size_t)sp * a.Mpad].x);
+  float lsum = 0.f;
+  f32x4 acc{0.f, 0.f, 0.f, 0.f};
+  for (int sp = 0; sp < nsplit; ++sp) {
+    const size_t r = wbase + (size_t)sp * a.Mpad;
+    const float2 ml = a.part_ml[r];
+    const float wgt = (ml.x == -INFINITY) ? 0.f : fast_exp2(ml.x - mx);
+    lsum += wgt * ml.y;
+    acc += wgt * *reinterpret_cast<const f32x4 *>(a.part_o + r * D + d);
   }
-  if (tid == 0) atomicExch(&a.counters[sg], 0u);
+  const f32x4 o = acc * (1.f / lsum);
+  const int qoff = a.q_offsets[s];
+  char *orow = reinterpret_cast<char *>(a.out) + ((size_t)(qoff + m / a.G) * a.Hq + g * a.G + m % a.G) * D * EB;
+  if constexpr (BF16)
+    *reinterpret_cast<uint2 *>(orow + d * EB) = uint2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
+  else
+    *reinterpret_cast<f32x4 *>(orow + d * EB) = o;
 }
 
 }  // namespace sdb

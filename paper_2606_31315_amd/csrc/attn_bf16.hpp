@@ -1,0 +1,343 @@
+// attn_bf16.hpp -- bf16 block attention kernel built around gfx950's asynchronous
+// global-to-LDS loads.
+//
+// Same operation and work decomposition as block_attn_kernel (one workgroup per
+// (sequence, kv head, KV split); all G*B_s query rows of the kv-head group packed into
+// 16-row MFMA tiles), with the memory pipeline rebuilt for bandwidth:
+//   * 8 wavefronts; wavefront w owns m-tiles w, w+8 (so up to 128 query rows per
+//     m-tile slot).
+//   * K and V tiles (64 keys each) are fetched with global_load_lds_dwordx4 straight
+//     into a 4-stage LDS ring (128 KB at D = 128): three tiles stay in flight while one
+//     is consumed, and no VGPRs hold data in transit.  One barrier per tile.
+//   * Rows in LDS are XOR-swizzled at 16-byte granularity (the swizzle is applied to
+//     the global address each lane fetches, since a load-to-LDS instruction writes 1 KB
+//     contiguously): K rows by (row mod 16) so the 16 rows an MFMA A-operand read
+//     touches fall in distinct banks; V rows by 2*(row mod 8) for the transposed reads.
+//   * The P.V contraction needs V^T operands (8 keys of one head dim per lane); they
+//     come straight from the row-major V tile with ds_read_b64_tr_b16, which transposes
+//     4x4 blocks of 16-bit elements across each 16-lane group.
+//   * Tiles every row can see entirely skip the per-element mask; the O rescale is
+//     skipped when no row's running maximum moved.
+#pragma once
+
+#include "attn.hpp"
+
+namespace sdb {
+
+#define SDB_LDS __attribute__((address_space(3)))
+
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+typedef float f32x2v __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+// Two fp32 -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
+  const f32x2v v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2v));
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// ds_read_b64_tr_b16 issued as inline assembly: the intrinsic form makes the compiler
+// assume it may alias the in-flight load-to-LDS writes and wait for all of them (the
+// explicit vmcnt wait and barrier at the top of each tile already order these reads).
+// The result is only valid after wait_lds_tr() below, which takes it as an operand.
+template <int OFF>
+__device__ __forceinline__ s16x4 ds_read_tr16(unsigned lds_addr) {
+  s16x4 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(lds_addr), "n"(OFF) : "memory");
+  return r;
+}
+
+// Wait for outstanding LDS reads; the registers pass through the asm so no use of them
+// can be scheduled before the wait.
+template <int NDT>
+__device__ __forceinline__ void wait_lds_tr(s16x4 (&v)[NDT][2]) {
+  if constexpr (NDT == 8) {
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(v[0][0]), "+v"(v[0][1]), "+v"(v[1][0]), "+v"(v[1][1]), "+v"(v[2][0]), "+v"(v[2][1]),
+                   "+v"(v[3][0]), "+v"(v[3][1]), "+v"(v[4][0]), "+v"(v[4][1]), "+v"(v[5][0]), "+v"(v[5][1]),
+                   "+v"(v[6][0]), "+v"(v[6][1]), "+v"(v[7][0]), "+v"(v[7][1])::"memory");
+  } else {
+    static_assert(NDT == 4, "head_dim 64 or 128");
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(v[0][0]), "+v"(v[0][1]), "+v"(v[1][0]), "+v"(v[1][1]), "+v"(v[2][0]), "+v"(v[2][1]),
+                   "+v"(v[3][0]), "+v"(v[3][1])::"memory");
+  }
+}
+
+template <int D>
+struct Bf16Tile {
+  static constexpr int KT = 64;                 // keys per tile
+  static constexpr int ROWB = D * 2;            // bytes per key row
+  static constexpr int CPR = ROWB / 16;         // 16-byte chunks per row
+  static constexpr int TILEB = KT * ROWB;       // bytes of one K (or V) tile
+  static constexpr int RPI = 1024 / ROWB;       // rows written by one 1 KB load instruction
+  static constexpr int LPI = TILEB / 1024;      // load instructions per K (or V) tile
+  static constexpr int NW = 8;                  // wavefronts per workgroup
+  static constexpr int LPW = 2 * LPI / NW;      // load instructions per wavefront per tile
+  static constexpr int NS = 4;                  // ring stages
+  static constexpr int STAGEB = 2 * TILEB;      // K tile then V tile
+  static_assert((2 * LPI) % NW == 0 && LPI % LPW == 0, "K and V loads split evenly over wavefronts");
+  __device__ static int swz_k(int r) { return r % CPR; }
+  __device__ static int swz_v(int r) { return (2 * r) % CPR; }
+};
+
+// Per-lane source offsets of this wavefront's share of one tile's loads (row*ROWB +
+// swizzled chunk*16, relative to the tile's first key row).  Wavefronts 0-3 fetch K,
+// 4-7 fetch V.
+template <int D>
+struct TileLoads {
+  using T = Bf16Tile<D>;
+  int row[T::LPW];
+  unsigned src[T::LPW];
+  bool isv;
+  __device__ void init(int wave, int lane) {
+    isv = wave * T::LPW >= T::LPI;  // uniform per wavefront
+#pragma unroll
+    for (int q = 0; q < T::LPW; ++q) {
+      const int li = wave * T::LPW + q - (isv ? T::LPI : 0);
+      row[q] = li * T::RPI + lane / T::CPR;
+      const int chunk = (lane % T::CPR) ^ (isv ? T::swz_v(row[q]) : T::swz_k(row[q]));
+      src[q] = row[q] * T::ROWB + chunk * 16;
+    }
+  }
+  // Issue the loads of the tile starting at key0 into `stage`; rows past key_last
+  // re-read key_last (only the split's last tile can need that).
+  __device__ void issue(char SDB_LDS *stage, const char *kbase, const char *vbase, int key0, int key_last,
+                        int wave) const {
+    const char *base = (isv ? vbase : kbase) + (size_t)key0 * T::ROWB;
+    char SDB_LDS *dst = stage + (isv ? T::TILEB : 0) + (wave * T::LPW - (isv ? T::LPI : 0)) * 1024;
+    if (key0 + T::KT - 1 <= key_last) {
+#pragma unroll
+      for (int q = 0; q < T::LPW; ++q)
+        __builtin_amdgcn_global_load_lds((const void *)(base + src[q]), (SDB_LDS void *)(dst + q * 1024), 16, 0, 0);
+    } else {
+#pragma unroll
+      for (int q = 0; q < T::LPW; ++q) {
+        const int shift = min(row[q], key_last - key0) - row[q];  // <= 0: back to the last valid key
+        __builtin_amdgcn_global_load_lds((const void *)(base + src[q] + shift * T::ROWB), (SDB_LDS void *)(dst + q * 1024),
+                                         16, 0, 0);
+      }
+    }
+  }
+};
+
+// One 32-key step (keys KK*32 .. KK*32+31 of the tile) of O^T += V^T P^T.  P comes from
+// the score registers (keys KK*32 + h*16 + kgrp*4 + r, h = 0,1); the matching V^T operand
+// from two transposed LDS reads per head-dim tile.
+template <int KK, int NDT>
+__device__ __forceinline__ void pv_step(const f32x4 (&p)[4], unsigned stage, const unsigned (&voff)[NDT],
+                                        f32x4 (&oacc)[NDT]) {
+  constexpr int ROWB = NDT * 32;  // bytes per key row (D * 2)
+  const u32x4 praw{cvt_pk_bf16(p[2 * KK][0], p[2 * KK][1]), cvt_pk_bf16(p[2 * KK][2], p[2 * KK][3]),
+                   cvt_pk_bf16(p[2 * KK + 1][0], p[2 * KK + 1][1]), cvt_pk_bf16(p[2 * KK + 1][2], p[2 * KK + 1][3])};
+  const bf16x8 pb = __builtin_bit_cast(bf16x8, praw);
+  s16x4 vv[NDT][2];
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) {
+    vv[dt][0] = ds_read_tr16<(KK * 32 + 0) * ROWB>(stage + voff[dt]);
+    vv[dt][1] = ds_read_tr16<(KK * 32 + 16) * ROWB>(stage + voff[dt]);
+  }
+  wait_lds_tr<NDT>(vv);
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) {
+    typedef short s16x8 __attribute__((ext_vector_type(8)));
+    const s16x8 v8 = {vv[dt][0][0], vv[dt][0][1], vv[dt][0][2], vv[dt][0][3],
+                      vv[dt][1][0], vv[dt][1][1], vv[dt][1][2], vv[dt][1][3]};
+    oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, v8), pb, oacc[dt], 0, 0, 0);
+  }
+}
+
+template <int D, int MT>
+__global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
+  using T = Bf16Tile<D>;
+  constexpr int KT = T::KT, NS = T::NS, NDT = D / 16, NST = D / 32;
+  constexpr int EB = 2;
+  __shared__ __attribute__((aligned(1024))) char ring_raw[NS * T::STAGEB];
+  char SDB_LDS *ring = (char SDB_LDS *)(SDB_LDS void *)ring_raw;
+
+  const int w = xcd_logical_id(blockIdx.x, a.per_xcd);
+  if (w >= a.n_work) return;
+  const int split = w % a.max_splits;
+  const int sg = w / a.max_splits;
+  const int g = sg % a.Hkv;
+  const int s = sg / a.Hkv;
+  const int ctx = a.ctx_lens[s];
+  const int B = a.block_lens[s];
+  if (B <= 0) return;
+  const int L = ctx + B;
+  const int nsplit = (L + a.split_len - 1) / a.split_len;
+  if (split >= nsplit) return;
+  const int k0 = split * a.split_len;
+  const int k1 = min(k0 + a.split_len, L);
+  const int M = a.G * B;
+  const int qoff = a.q_offsets[s];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int l16 = lane & 15;
+  const int kgrp = lane >> 4;
+  const int nmt = (M + 15) >> 4;
+
+  const char *kbase = reinterpret_cast<const char *>(a.k) + ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
+  const char *vbase = reinterpret_cast<const char *>(a.v) + ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
+
+  // ---- query operands: element e of step st is dim st*32 + kgrp*8 + e of row m ----
+  bf16x8 qop[MT][NST];
+  f32x4 oacc[MT][NDT];
+  float m_run[MT], l_run[MT];
+  int row_i[MT];
+  bool act[MT];
+#pragma unroll
+  for (int j = 0; j < MT; ++j) {
+    const int mt = wave + T::NW * j;
+    const int m = mt * 16 + l16;
+    act[j] = mt < nmt;
+    m_run[j] = -INFINITY;
+    l_run[j] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) oacc[j][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const bool valid = act[j] && m < M;
+    row_i[j] = valid ? m / a.G : 0;
+    const char *qrow = reinterpret_cast<const char *>(a.q) +
+                       ((size_t)(qoff + (valid ? m / a.G : 0)) * a.Hq + g * a.G + (valid ? m % a.G : 0)) * D * EB;
+#pragma unroll
+    for (int st = 0; st < NST; ++st) {
+      const u32x4 raw = valid ? *reinterpret_cast<const u32x4 *>(qrow + (st * 32 + kgrp * 8) * EB) : u32x4{0, 0, 0, 0};
+      qop[j][st] = __builtin_bit_cast(bf16x8, raw);
+    }
+  }
+
+  // ---- per-lane LDS offsets, fixed for the whole loop ----
+  // K operand of sub-tile sb, step st: row sb*16 + l16, chunk (st*4 + kgrp) swizzled by the
+  // row (the swizzle only depends on l16); sb*16 rows are an immediate offset.
+  unsigned koff[NST];
+#pragma unroll
+  for (int st = 0; st < NST; ++st) koff[st] = l16 * T::ROWB + (((st * 4 + kgrp) ^ T::swz_k(l16)) << 4);
+  // V^T operand for head-dim tile dt: source row kgrp*4 + l16/4 (plus kk*32 + h*16 keys as
+  // an immediate), head dims dt*16 + 4*(l16%4) .. +3 (swizzle depends only on the row mod 8).
+  const int vrow = kgrp * 4 + (l16 >> 2);
+  unsigned voff[NDT];
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt)
+    voff[dt] = T::TILEB + vrow * T::ROWB + (((2 * dt + ((l16 & 3) >> 1)) ^ T::swz_v(vrow)) << 4) + ((l16 & 1) << 3);
+
+  TileLoads<D> ld;
+  ld.init(wave, lane);
+
+  // ---- pipeline prologue: tiles 0 .. NS-2 in flight ----
+  const int ntiles = (k1 - k0 + KT - 1) / KT;
+#pragma unroll
+  for (int t = 0; t < NS - 1; ++t)
+    if (t < ntiles) ld.issue(ring + t * T::STAGEB, kbase, vbase, k0 + t * KT, k1 - 1, wave);
+  // keys every row can see: all of [k0, k1) when bidirectional, keys <= ctx when causal
+  const int vis_all = a.causal ? min(k1, ctx + 1) : k1;
+  const float sl2 = a.scale_log2;
+
+  for (int t = 0; t < ntiles; ++t) {
+    const int kt = k0 + t * KT;
+    const int ahead = min(ntiles - 1 - t, NS - 2);  // tiles issued after tile t
+    if (ahead >= 2) wait_vmcnt<2 * T::LPW>();
+    else if (ahead == 1) wait_vmcnt<T::LPW>();
+    else wait_vmcnt<0>();
+    __syncthreads();  // tile t landed for every wavefront; stage (t-1) % NS is free again
+    if (t + NS - 1 < ntiles)
+      ld.issue(ring + ((t + NS - 1) % NS) * T::STAGEB, kbase, vbase, kt + (NS - 1) * KT, k1 - 1, wave);
+    const unsigned stage = (unsigned)(uintptr_t)(ring + (t % NS) * T::STAGEB);
+    const bool full = kt + KT <= vis_all;  // uniform: no key of this tile is masked for any row
+
+#pragma unroll
+    for (int j = 0; j < MT; ++j) {
+      if (!act[j]) continue;  // uniform per wavefront
+      // S^T = K Q^T: sacc[sb][r] is key kt + sb*16 + kgrp*4 + r of row l16 (unscaled)
+      f32x4 sacc[4];
+#pragma unroll
+      for (int sb = 0; sb < 4; ++sb) sacc[sb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < NST; ++st) {
+        const char SDB_LDS *kp = (const char SDB_LDS *)(uintptr_t)(stage + koff[st]);
+#pragma unroll
+        for (int sb = 0; sb < 4; ++sb) {
+          const bf16x8 av = *(const bf16x8 SDB_LDS *)(kp + sb * 16 * T::ROWB);
+          sacc[sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qop[j][st], sacc[sb], 0, 0, 0);
+        }
+      }
+      // online softmax in the log2 domain: max of the raw scores, then one FMA per score
+      if (!full) {
+        const int lim = a.causal ? min(k1, ctx + row_i[j] + 1) : k1;
+#pragma unroll
+        for (int sb = 0; sb < 4; ++sb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (kt + sb * 16 + kgrp * 4 + r >= lim) sacc[sb][r] = -INFINITY;
+      }
+      float tmax = fmaxf(fmaxf(fmaxf(sacc[0][0], sacc[0][1]), fmaxf(sacc[0][2], sacc[0][3])),
+                         fmaxf(fmaxf(sacc[1][0], sacc[1][1]), fmaxf(sacc[1][2], sacc[1][3])));
+      tmax = fmaxf(tmax, fmaxf(fmaxf(fmaxf(sacc[2][0], sacc[2][1]), fmaxf(sacc[2][2], sacc[2][3])),
+                               fmaxf(fmaxf(sacc[3][0], sacc[3][1]), fmaxf(sacc[3][2], sacc[3][3]))));
+      tmax = fmaxf(tmax, shfl_xor_f(tmax, 16));
+      tmax = fmaxf(tmax, shfl_xor_f(tmax, 32));
+      const float mnew = fmaxf(m_run[j], tmax * sl2);
+      const float muse = (mnew == -INFINITY) ? 0.f : mnew;
+      float psum = 0.f;
+#pragma unroll
+      for (int sb = 0; sb < 4; ++sb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          sacc[sb][r] = fast_exp2(fmaf(sacc[sb][r], sl2, -muse));
+          psum += sacc[sb][r];
+        }
+      if (__any(mnew != m_run[j])) {
+        const float alpha = fast_exp2(m_run[j] - muse);
+        l_run[j] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) oacc[j][dt] *= alpha;
+      }
+      m_run[j] = mnew;
+      l_run[j] += psum;
+
+      // O^T += V^T P^T over the tile's 64 keys in two 32-key steps
+      pv_step<0, NDT>(sacc, stage, voff, oacc[j]);
+      pv_step<1, NDT>(sacc, stage, voff, oacc[j]);
+    }
+  }
+
+  // ---- epilogue: row sums over the four key groups, then output or partials ----
+#pragma unroll
+  for (int j = 0; j < MT; ++j) {
+    l_run[j] += shfl_xor_f(l_run[j], 16);
+    l_run[j] += shfl_xor_f(l_run[j], 32);
+  }
+  if (nsplit == 1) {
+#pragma unroll
+    for (int j = 0; j < MT; ++j) {
+      const int m = (wave + T::NW * j) * 16 + l16;
+      if (!act[j] || m >= M) continue;
+      const float inv = 1.f / l_run[j];
+      char *orow = reinterpret_cast<char *>(a.out) + ((size_t)(qoff + m / a.G) * a.Hq + g * a.G + m % a.G) * D * EB;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) {
+        const f32x4 o = oacc[j][dt] * inv;
+        *reinterpret_cast<uint2 *>(orow + (dt * 16 + kgrp * 4) * EB) = uint2{cvt_pk_bf16(o[0], o[1]), cvt_pk_bf16(o[2], o[3])};
+      }
+    }
+    return;
+  }
+  const size_t wrow = (size_t)w * a.Mpad;
+#pragma unroll
+  for (int j = 0; j < MT; ++j) {
+    const int m = (wave + T::NW * j) * 16 + l16;
+    if (!act[j] || m >= M) continue;
+    float *prow = a.part_o + (wrow + m) * D;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) *reinterpret_cast<f32x4 *>(prow + dt * 16 + kgrp * 4) = oacc[j][dt];
+    if (kgrp == 0) a.part_ml[wrow + m] = float2{m_run[j], l_run[j]};
+  }
+}
+
+}  // namespace sdb

