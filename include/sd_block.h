@@ -125,7 +125,7 @@ int sd_block_attn(const sd_attn_shape *shape, const void *q, const void *k_cache
  * ========================================================================== */
 typedef struct sd_accept_shape {
   int32_t num_seqs;  /* S >= 0 */
-  int32_t vocab;     /* V >= 1 */
+  int32_t vocab;     /* 1 <= V <= 2^28 */
   int32_t total_q;   /* sum_s B_s */
   int32_t max_block; /* host-known bound on B_s, 1 <= max_block <= 64 */
   int32_t dtype;     /* SD_BF16 or SD_F32: element type of both logit arrays */
@@ -139,7 +139,8 @@ int sd_accept_workspace_size(const sd_accept_shape *shape, float temperature, si
  *   draft_logits  [total_q - S, V]   row q_offsets[s] - s + j: drafter logits for block position
  *                                    j + 1, j < B_s - 1 (read only when temperature > 0; may be NULL
  *                                    at temperature 0)
- *   draft_tokens  [total_q - S] int32  drafted token of block position j + 1, in [0, V)
+ *   draft_tokens  [total_q - S] int32  drafted token of block position j + 1, in [0, V) (a token
+ *                                    outside that range is never accepted)
  *   uniforms      [total_q] fp32 in [0, 1): slot q_offsets[s] + j drives acceptance test j;
  *                                    slot q_offsets[s] + B_s - 1 drives the single final draw
  *                                    (read only when temperature > 0; may be NULL at 0)
@@ -156,9 +157,9 @@ int sd_accept_workspace_size(const sd_accept_shape *shape, float temperature, si
  *   next_token    [S] int32 out      bonus or resampled token
  *
  * Host-checked preconditions: logits 16-byte aligned; temperature finite and >= 0;
- * S <= total_q <= S * max_block.  Statistics are fp32 (softmax sums fp32 per thread, fp64
- * across threads); decisions within about 1e-6 of a boundary may differ from an fp64
- * evaluation.
+ * S <= total_q <= S * max_block; vocab <= 2^28.  Softmax statistics and per-chunk masses are
+ * accumulated in fp32, the acceptance ratio and the final draw's cumulative sums in fp64;
+ * decisions within about 1e-6 of a boundary may differ from an fp64 evaluation.
  * Errors: SD_ERR_INVALID_ARG, SD_ERR_WORKSPACE, SD_ERR_HIP.  S == 0 returns SD_OK.
  */
 int sd_accept(const sd_accept_shape *shape, const void *target_logits, const void *draft_logits,

@@ -7,25 +7,30 @@
 // first rejection draw the token from max(0, p_j - q_j); if every draft is accepted
 // draw the bonus token from the last target row.
 //
-// Kernels (gfx950); kernel boundaries are the only cross-workgroup synchronisation
-// (an agent-scope fence per workgroup costs an L2 writeback on gfx950):
-//   accept_stats_kernel     grid = (row, vocab chunk) over every target row, and every
-//                           draft row when T > 0.  One streaming pass of 16-byte loads:
-//                           T = 0 keeps (max value, lowest index); T > 0 keeps an online
-//                           (max, sum of exp2((x - max) log2e / T)) with one rescale per
-//                           batch of loads, never per element.
-//   accept_greedy_kernel    T = 0, one wavefront per sequence: merge the chunk partials,
-//                           lane i tests drafted position i, a ballot finds the first
-//                           rejection; writes accept_len and the next token.
-//   accept_sample_kernel    T > 0, grid = (sequence, vocab chunk): every workgroup redoes
-//                           the small per-sequence decision (lane i tests position i,
-//                           ballot), then sums the residual max(0, p - q) (or p at the
-//                           bonus row) over its chunk.
-//   accept_scan_kernel      T > 0, one workgroup per sequence: locate the chunk holding
-//                           u* times the total mass and scan it in vocabulary order.
+// Kernels (gfx950).  An agent-scope fence per workgroup costs an L2 write-back on gfx950
+// and one workgroup streams a row far below HBM speed, so every phase that needs a whole
+// row spreads it over many workgroups and hands results on across a kernel boundary:
+//   accept_stats_kernel     persistent grid over (row, vocab chunk) items of every target
+//                           row, and every draft row when T > 0.  One streaming pass of
+//                           16-byte loads: T = 0 keeps (max value, lowest index); T > 0 keeps
+//                           an online (max, sum of exp2((x - max) log2e / T)) with one
+//                           rescale per batch of loads.  Each item's record is filed under
+//                           (sequence, block position) with the drafted token's logit (or
+//                           the token itself at T = 0) and the position's uniform, so the
+//                           decision needs one parallel round of loads.
+//   accept_greedy_kernel    T = 0, one wavefront per sequence: lane i merges the records of
+//                           position i, a ballot finds the first rejection.
+//   accept_mass_kernel      T > 0, grid = (sequence, vocab chunk): every workgroup makes the
+//                           small per-sequence decision, then sums the residual
+//                           max(0, p_j - q_j) and p_j over its chunk of the selected row.
+//   accept_locate_kernel    T > 0, one workgroup per sequence: scans the chunk sums for the
+//                           chunk holding u* times the total mass, then scans that chunk in
+//                           vocabulary order.
 #pragma once
 
 #include <limits.h>
+
+#include <type_traits>
 
 #include "common.hpp"
 
@@ -40,17 +45,23 @@ struct AcceptArgs {
   const int *q_offsets;
   int *accept_len;
   int *next_token;
-  float2 *stats;      // [rows, nch]: (max, sum) at T > 0; (max value, index bits) at T = 0
-  float4 *seqinfo;    // [S, 2]: (row, residual?, target max, 1/target sum), (draft max, 1/draft sum, 0, 0)
-  double2 *samp;      // [S, nch2]: (residual mass, p mass) per chunk
-  int S, V, total_q, nch, nch2;
+  // Records [kinds * S * mb, nch], kind 0 = target position, kind 1 = draft position (T > 0),
+  // index (kind * S + s) * mb + j:
+  //   T > 0: (max, sum, logit at the drafted token or NaN, uniform u_j)
+  //   T = 0: (max value, index bits, drafted token bits or -1, -)
+  float4 *stats;
+  double2 *samp;      // [S, nch2]: (residual mass, p mass) per sampling chunk (T > 0)
+  float4 *seqinfo;    // [S, 2]: (accept_len bits, residual?, target max, 1/target sum),
+                      //         (draft max, 1/draft sum, u*, -)   (T > 0)
+  int S, V, total_q, rows, mb, nch, nch2;
   float c;            // log2(e) / T (T > 0)
 };
 
 // Chunk `c` of `nch` of a row that starts at absolute element a0 and holds V elements.
-// Elements are grouped in 16-byte vectors of VEC elements on absolute boundaries; the
-// unaligned head goes to chunk 0 and the tail to the last chunk.  Every chunk is a
-// contiguous element range [e0, e1) of the row.
+// Elements are grouped in 16-byte vectors of VEC elements on absolute boundaries, spread
+// evenly over the chunks (sizes differ by at most one, so no chunk is empty while the row
+// has at least nch whole vectors); the unaligned head goes to chunk 0 and the tail to the
+// last chunk.  Every chunk is a contiguous element range [e0, e1) of the row.
 struct RowChunk {
   long long vb, ve;  // absolute vector range
   int hb, he;        // scalar head (relative elements)
@@ -73,9 +84,8 @@ __device__ __forceinline__ RowChunk row_chunk(long long a0, int V, int c, int nc
     return r;
   }
   const long long nv = o1 - o0;
-  const long long per = (nv + nch - 1) / nch;
-  r.vb = min(o0 + per * c, o1);
-  r.ve = min(r.vb + per, o1);
+  r.vb = o0 + nv * c / nch;
+  r.ve = o0 + nv * (c + 1) / nch;
   r.hb = 0;
   r.he = (c == 0) ? (int)(o0 * VEC - a0) : 0;
   r.tb = (int)(o1 * VEC - a0);
@@ -105,12 +115,13 @@ __device__ __forceinline__ void unpack(const u32x4 &v, float *x) {
   }
 }
 
-// Largest s with key(s) <= r, where key(s) = q_offsets[s] - s*draft (non-decreasing).
+// Largest s with key(s) <= r, where key(s) = q_offsets[s] - s*draft (non-decreasing);
+// r is uniform across the workgroup.
 __device__ __forceinline__ int owner_of_row(const int *off, int S, int r, int draft) {
   int lo = 0, hi = S - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    if (off[mid] - mid * draft <= r) lo = mid; else hi = mid - 1;
+    if (ld_uniform(off, mid) - mid * draft <= r) lo = mid; else hi = mid - 1;
   }
   return lo;
 }
@@ -129,132 +140,238 @@ __device__ __forceinline__ void lse_merge(float &m, float &sum, float m2, float 
   m = mn;
 }
 
-constexpr int kUnroll = 4;  // 16-byte vectors in flight per thread per batch
+constexpr int kStatsVecs = 8;     // 16-byte vectors per thread per stats item
+constexpr int kMassVecs = 4;      // vectors per thread per batch in the mass kernel
+constexpr int kLocThreads = 256;  // locate kernel workgroup
+constexpr int kLocVecs = 8;       // vectors per thread kept in registers by the locate kernel
+constexpr int kMaxChunks2 = 4096; // sampling chunks per sequence
 
-template <bool BF16, bool SAMPLE>
-__global__ __launch_bounds__(256) void accept_stats_kernel(AcceptArgs a) {
+// One stats item in flight: its loads, issued together, and what processing it needs.  A
+// statistics chunk is kStatsChunk whole vectors of the row (the last chunk holds the rest
+// and may be empty), plus the row's unaligned head (chunk 0) and tail (last chunk).
+constexpr int kStatsChunk = 256 * kStatsVecs;
+
+template <int NV>
+struct StatsItem {
+  u32x4 v[NV];   // this thread's vectors (clamped loads; padding applied when processed)
+  float xh, xt;  // head and tail element (or element tid of a tiny row)
+  float uj;      // uniform of the position (target rows, T > 0)
+  int rec, tok;  // record index (-1: not recorded), drafted token or -1
+  int c;         // chunk index
+  int e0;        // row-relative element of the chunk's first whole vector
+  int nvc;       // whole vectors in the chunk
+  int nh, ntl;   // head / tail elements handled by this chunk
+  int tb;        // row-relative start of the tail
+};
+
+// Issue every load of `item`: this thread's vectors (uniform chunk base, 32-bit offsets) and
+// one head and one tail element, first and unconditionally -- loads past the end are clamped
+// onto valid addresses and replaced by padding when the item is processed, because a load
+// under a branch makes the compiler wait for it.  Then the row's (sequence, position), its
+// drafted token and uniform, through scalar loads, which do not wait for the vectors in
+// flight.  VECS: every row holds a whole vector (V >= 2 VEC - 1);
+// otherwise the vocabulary is below 256 elements, there is one chunk, and each thread loads
+// element tid of the row.
+template <bool BF16, bool SAMPLE, bool VECS>
+__device__ __forceinline__ void stats_issue(const AcceptArgs &a, int item, StatsItem<kStatsVecs> &it) {
   constexpr int VEC = BF16 ? 8 : 4;
-  __shared__ float sh_v[4];
-  __shared__ float sh_s[4];
-  __shared__ int sh_i[4];
-
-  const int row = blockIdx.x / a.nch;
-  const int c = blockIdx.x % a.nch;
+  const int tid = threadIdx.x;
+  const int row = item / a.nch;
+  it.c = item - row * a.nch;
   const bool is_draft = row >= a.total_q;
   const int rr = is_draft ? row - a.total_q : row;
-  const void *base = is_draft ? a.draft : a.target;
-  const long long a0 = (long long)rr * a.V;
-  const RowChunk ch = row_chunk<VEC>(a0, a.V, c, a.nch);
-  const int tid = threadIdx.x;
+  const char *base = reinterpret_cast<const char *>(is_draft ? a.draft : a.target);
+  const unsigned long long a0 = (unsigned long long)rr * (unsigned)a.V;
+  const int h = (int)((VEC - (unsigned)(a0 % VEC)) % VEC);  // head elements before the first whole vector
+  const int nv = (a.V - h) / VEC;                           // whole vectors in the row
+  const int v0 = it.c * kStatsChunk;
+  it.nvc = max(0, min(kStatsChunk, nv - v0));
+  it.e0 = h + v0 * VEC;
+  it.tb = h + nv * VEC;
+  const bool last = it.c == a.nch - 1;
+  it.nh = (it.c == 0) ? h : 0;
+  it.ntl = last ? a.V - it.tb : 0;
+  if constexpr (VECS) {
+    // the chunk's vectors; an empty chunk reads the row's last whole vector and discards it
+    const char *cb = base + (a0 + h) * (BF16 ? 2 : 4) + (unsigned)min(v0, nv - 1) * 16u;
+    const unsigned lastv = (unsigned)max(it.nvc, 1) - 1u;
+#pragma unroll
+    for (int u = 0; u < kStatsVecs; ++u)
+      it.v[u] = *reinterpret_cast<const u32x4 *>(cb + min((unsigned)tid + 256u * u, lastv) * 16u);
+    it.xh = load_elem<BF16>(base, a0 + min(tid, a.V - 1));
+    it.xt = load_elem<BF16>(base, a0 + min(it.tb + tid, a.V - 1));
+  } else {
+    it.xh = load_elem<BF16>(base, a0 + min(tid, a.V - 1));
+    it.xt = 0.f;
+  }
 
-  float bv = -INFINITY;  // greedy: best value / SAMPLE: running max
+  int sq, j, tok = -1;
+  it.uj = 0.f;
+  if (is_draft) {
+    sq = owner_of_row(a.q_offsets, a.S, rr, 1);
+    j = rr - (ld_uniform(a.q_offsets, sq) - sq);
+    if (SAMPLE) tok = ld_uniform(a.draft_tokens, rr);
+  } else {
+    sq = owner_of_row(a.q_offsets, a.S, rr, 0);
+    j = rr - ld_uniform(a.q_offsets, sq);
+    if (rr + 1 < ld_uniform(a.q_offsets, sq + 1)) tok = ld_uniform(a.draft_tokens, rr - sq);
+    if (SAMPLE) it.uj = ld_uniform(a.uniforms, rr);
+  }
+  it.rec = (j >= 0 && j < a.mb) ? ((is_draft ? a.S : 0) + sq) * a.mb + j : -1;
+  it.tok = tok;
+}
+
+// Reduce one landed item to its record: T > 0 (max, sum of exp2((x - max) c)) with one
+// rescale per item, and the drafted token's logit taken from the register that holds it;
+// T = 0 (max, lowest index).
+template <bool BF16, bool SAMPLE, bool VECS>
+__device__ __forceinline__ void stats_process(const AcceptArgs &a, StatsItem<kStatsVecs> &it, float *sh_v,
+                                              float *sh_s, int *sh_i) {
+  constexpr int VEC = BF16 ? 8 : 4;
+  constexpr uint32_t kPad = BF16 ? 0xff80ff80u : 0xff800000u;  // -inf in every element
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // head / tail elements this thread holds (row-relative index), or -inf
+  const bool hv = VECS ? tid < it.nh : tid < a.V;
+  const bool tv = VECS && tid < it.ntl;
+  const int eh = tid, et = it.tb + tid;
+  const float xh = hv ? it.xh : -INFINITY;
+  const float xt = tv ? it.xt : -INFINITY;
+  float bv = -INFINITY;  // greedy: best value / SAMPLE: the wavefront's max
   int bi = INT_MAX;      // greedy: index of best
   float sum = 0.f;       // SAMPLE: sum of exp2((x - bv) c)
-
-  // scalar head and tail
-  for (int e = ch.hb + tid; e < ch.he; e += 256) {
-    const float x = load_elem<BF16>(base, a0 + e);
-    if constexpr (SAMPLE) lse_merge(bv, sum, x, 1.f, a.c);
-    else if (x > bv) { bv = x; bi = e; }
-  }
-  // vectors: full batches of kUnroll loads in flight per thread, then single vectors
-  const u32x4 *vbase = reinterpret_cast<const u32x4 *>(base);
-  long long v = ch.vb + tid;
-  for (; v + 256LL * (kUnroll - 1) < ch.ve; v += 256LL * kUnroll) {
-    u32x4 buf[kUnroll];
+  // a full chunk needs no padding: its arithmetic runs without the per-vector selects
+  auto reduce = [&](auto padc) {
+    constexpr bool PAD = decltype(padc)::value;
+    auto vec_at = [&](int u) {
+      return (!PAD || (VECS && tid + 256 * u < it.nvc)) ? it.v[u] : u32x4{kPad, kPad, kPad, kPad};
+    };
+    float bm = fmaxf(xh, xt);
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) buf[u] = vbase[v + 256LL * u];
-    float x[kUnroll][VEC];
+    for (int u = 0; u < kStatsVecs; ++u) {
+      float x[VEC];
+      unpack<BF16>(vec_at(u), x);
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) unpack<BF16>(buf[u], x[u]);
+      for (int e = 0; e < VEC; e += 2) bm = fmaxf(bm, fmaxf(x[e], x[e + 1]));
+    }
+    // re-unpack in the second pass rather than keep every unpacked value live across it
+#pragma unroll
+    for (int u = 0; u < kStatsVecs; ++u) reg_barrier(it.v[u]);
     if constexpr (SAMPLE) {
-      float bm = -INFINITY;
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u)
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) bm = fmaxf(bm, x[u][e]);
-      if (bm > bv) {
-        sum = (bv == -INFINITY) ? 0.f : sum * fast_exp2((bv - bm) * a.c);
-        bv = bm;
-      }
+      bv = wave_max_f(bm);  // the wavefront's reference maximum
       if (bv != -INFINITY) {
         const float off = -bv * a.c;
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
+        for (int u = 0; u < kStatsVecs; ++u) {
+          float x[VEC];
+          unpack<BF16>(vec_at(u), x);
 #pragma unroll
-          for (int e = 0; e < VEC; ++e) sum += fast_exp2(fmaf(x[u][e], a.c, off));
+          for (int e = 0; e < VEC; ++e) sum += fast_exp2(fmaf(x[e], a.c, off));
+        }
+        sum += fast_exp2(fmaf(xh, a.c, off)) + fast_exp2(fmaf(xt, a.c, off));
       }
-    } else {
+    } else if (bm != -INFINITY) {  // first index of the maximum among this thread's elements
+      int idx = INT_MAX;
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int e0 = (int)((v + 256LL * u) * VEC - a0);
+      for (int u = kStatsVecs - 1; u >= 0; --u) {
+        float x[VEC];
+        unpack<BF16>(vec_at(u), x);
+        const int eb = it.e0 + (tid + 256 * u) * VEC;
 #pragma unroll
-        for (int e = 0; e < VEC; ++e)
-          if (x[u][e] > bv) { bv = x[u][e]; bi = e0 + e; }
+        for (int e = VEC - 1; e >= 0; --e)
+          if (x[e] == bm) idx = eb + e;
       }
+      if (tv && xt == bm) idx = min(idx, et);
+      if (hv && xh == bm) idx = min(idx, eh);
+      bv = bm;
+      bi = idx;
     }
-  }
-  for (; v < ch.ve; v += 256) {
-    float x[VEC];
-    unpack<BF16>(vbase[v], x);
-    const int e0 = (int)(v * VEC - a0);
+  };
+
+  float xd = NAN;  // T > 0: the drafted token's logit, in the one thread holding it
+  if (SAMPLE && it.tok >= 0) {
+    const int t = it.tok;
+    if (hv && eh == t) xd = xh;
+    if (tv && et == t) xd = xt;
+    if (VECS) {
+      const int r = t - it.e0;  // element offset into the chunk's vectors
+      if (r >= 0 && r < it.nvc * VEC && ((r / VEC) & 255) == tid) {
+        const int ut = (r / VEC) >> 8, et2 = r % VEC;
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) {
-      if constexpr (SAMPLE) lse_merge(bv, sum, x[e], 1.f, a.c);
-      else if (x[e] > bv) { bv = x[e]; bi = e0 + e; }
-    }
-  }
-  if (ch.tb < ch.te) {
-    for (int e = ch.tb + tid; e < ch.te; e += 256) {
-      const float x = load_elem<BF16>(base, a0 + e);
-      if constexpr (SAMPLE) lse_merge(bv, sum, x, 1.f, a.c);
-      else argmax_merge(bv, bi, x, e);
+        for (int u = 0; u < kStatsVecs; ++u)
+          if (u == ut) {
+            float x[VEC];
+            unpack<BF16>(it.v[u], x);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+              if (e == et2) xd = x[e];
+          }
+      }
     }
   }
 
-  // wavefront then workgroup reduction
-  const int lane = tid & 63, wave = tid >> 6;
+  if (VECS && it.nvc == kStatsChunk) reduce(std::false_type{});
+  else reduce(std::true_type{});
+  if constexpr (SAMPLE) {
+    sum = wave_sum_f(sum);
+    xd = wave_max_f(xd);
+  } else {
 #pragma unroll
-  for (int msk = 1; msk < 64; msk <<= 1) {
-    const float ov = __shfl_xor(bv, msk, 64);
-    if constexpr (SAMPLE) {
-      const float os = __shfl_xor(sum, msk, 64);
-      lse_merge(bv, sum, ov, os, a.c);
-    } else {
+    for (int msk = 1; msk < 64; msk <<= 1) {
+      const float ov = __shfl_xor(bv, msk, 64);
       const int oi = __shfl_xor(bi, msk, 64);
       argmax_merge(bv, bi, ov, oi);
     }
   }
-  if (lane == 0) { sh_v[wave] = bv; sh_s[wave] = sum; sh_i[wave] = bi; }
+
+  if (lane == 0) { sh_v[wave] = bv; sh_s[wave] = sum; sh_i[wave] = bi; if (SAMPLE) sh_v[4 + wave] = xd; }
   __syncthreads();
   if (tid == 0) {
     for (int w2 = 1; w2 < 4; ++w2) {
-      if constexpr (SAMPLE) lse_merge(bv, sum, sh_v[w2], sh_s[w2], a.c);
-      else argmax_merge(bv, bi, sh_v[w2], sh_i[w2]);
+      if constexpr (SAMPLE) {
+        lse_merge(bv, sum, sh_v[w2], sh_s[w2], a.c);
+        xd = fmaxf(xd, sh_v[4 + w2]);
+      } else {
+        argmax_merge(bv, bi, sh_v[w2], sh_i[w2]);
+      }
     }
-    a.stats[(size_t)row * a.nch + c] = SAMPLE ? float2{bv, sum} : float2{bv, __int_as_float(bi)};
+    if (it.rec >= 0)
+      a.stats[(size_t)it.rec * a.nch + it.c] =
+          SAMPLE ? float4{bv, sum, xd, it.uj} : float4{bv, __int_as_float(bi), __int_as_float(it.tok), 0.f};
   }
-
 }
 
-// Greedy decision for sequence s on one wavefront: lane i merges the chunk partials of
-// target row i into its lowest-index argmax and tests drafted position i.
-template <bool BF16>
+// One (row, vocab chunk) item per workgroup.  Measured on MI355X, this beats keeping a
+// second item's loads in flight per workgroup: the pass is as much arithmetic as traffic,
+// and more resident workgroups hide both.
+template <bool BF16, bool SAMPLE, bool VECS>
+__global__ __launch_bounds__(256) void accept_stats_kernel(AcceptArgs a) {
+  __shared__ float sh_v[8];
+  __shared__ float sh_s[4];
+  __shared__ int sh_i[4];
+  StatsItem<kStatsVecs> it;
+  stats_issue<BF16, SAMPLE, VECS>(a, blockIdx.x, it);
+  stats_process<BF16, SAMPLE, VECS>(a, it, sh_v, sh_s, sh_i);
+}
+
+// Greedy decision for sequence s on one wavefront: lane i merges the records of block
+// position i into its lowest-index argmax and tests the drafted token there.
 __global__ __launch_bounds__(64) void accept_greedy_kernel(AcceptArgs a) {
   const int s = blockIdx.x;
   const int lane = threadIdx.x;
-  const int B = a.block_lens[s];
+  const int B = ld_uniform(a.block_lens, s);
   const int n = B - 1;
-  const int off = a.q_offsets[s];
-  const int tok = (lane < n) ? a.draft_tokens[off - s + lane] : 0;
-  int gi = INT_MAX;
-  if (lane < B) {
-    const float2 *st = a.stats + (size_t)(off + lane) * a.nch;
+  int gi = INT_MAX, tok = -1;
+  if (lane < a.mb) {  // issued before B arrives; positions >= B are ignored below
+    const float4 *st = a.stats + (size_t)(s * a.mb + lane) * a.nch;
     float gv = -INFINITY;
     for (int c0 = 0; c0 < a.nch; c0 += 8) {
-      float2 v[8];
+      float4 v[8];
 #pragma unroll
-      for (int k = 0; k < 8; ++k) v[k] = (c0 + k < a.nch) ? st[c0 + k] : float2{-INFINITY, __int_as_float(INT_MAX)};
+      for (int k = 0; k < 8; ++k) v[k] = st[min(c0 + k, a.nch - 1)];  // clamped: no per-load branch
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (c0 + k >= a.nch) v[k] = float4{-INFINITY, __int_as_float(INT_MAX), __int_as_float(-1), 0.f};
+      if (c0 == 0) tok = __float_as_int(v[0].z);
 #pragma unroll
       for (int k = 0; k < 8; ++k) argmax_merge(gv, gi, v[k].x, __float_as_int(v[k].y));
     }
@@ -270,45 +387,69 @@ __global__ __launch_bounds__(64) void accept_greedy_kernel(AcceptArgs a) {
   }
 }
 
-// Merge a row's chunk partials (max, sum) with the loads issued in batches of 8.
-__device__ __forceinline__ void merge_lse_partials(const float2 *st, int nch, float c, float &m, float &sum) {
-  for (int c0 = 0; c0 < nch; c0 += 8) {
-    float2 v[8];
+// Merge the chunk records (max, sum, captured logit, u) of one target position and one
+// draft position: every load of a batch of kRecBatch chunks of both issued together, then
+// the maximum over chunks and one exp2 per chunk against it.  Exactly one chunk holds the
+// captured logit; the others carry NaN, which fmaxf drops.
+constexpr int kRecBatch = 8;
+
+__device__ __forceinline__ void merge_one(const float4 *v, int k0, int nch, float c, float &m, float &sum,
+                                          float &x) {
+  float bm = -INFINITY;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) v[k] = (c0 + k < nch) ? st[c0 + k] : float2{-INFINITY, 0.f};
+  for (int k = 0; k < kRecBatch; ++k) bm = fmaxf(bm, v[k].x);
+  const float mn = fmaxf(m, bm);
+  if (mn == -INFINITY) return;
+  float acc = (m == -INFINITY) ? 0.f : sum * fast_exp2((m - mn) * c);
 #pragma unroll
-    for (int k = 0; k < 8; ++k) lse_merge(m, sum, v[k].x, v[k].y, c);
+  for (int k = 0; k < kRecBatch; ++k) {
+    if (k0 + k < nch) acc += v[k].y * fast_exp2((v[k].x - mn) * c);  // exp2(-inf) = 0
+    x = fmaxf(x, v[k].z);
+  }
+  m = mn;
+  sum = acc;
+}
+
+__device__ __forceinline__ void merge_records2(const float4 *st, const float4 *sd, int nch, float c, float &tm,
+                                               float &ts, float &td, float &u, float &qm, float &qs, float &dd) {
+  for (int c0 = 0; c0 < nch; c0 += kRecBatch) {
+    float4 v[kRecBatch], w[kRecBatch];
+#pragma unroll
+    for (int k = 0; k < kRecBatch; ++k) {  // clamped: no per-load branch
+      v[k] = st[min(c0 + k, nch - 1)];
+      w[k] = sd[min(c0 + k, nch - 1)];
+    }
+#pragma unroll
+    for (int k = 0; k < kRecBatch; ++k)
+      if (c0 + k >= nch) v[k] = w[k] = float4{-INFINITY, 0.f, NAN, 0.f};
+    if (c0 == 0) u = v[0].w;
+    merge_one(v, c0, nch, c, tm, ts, td);
+    merge_one(w, c0, nch, c, qm, qs, dd);
   }
 }
 
-// Sampling decision for sequence s on one wavefront (lane i = block position i).
-// Returns, in every lane, the accepted length and the normalisers of the selected row.
+// Sampling decision for sequence s on one wavefront (lane i = block position i).  Every
+// lane returns the accepted length, the normalisers of the selected row and u*.
 struct SampleSel {
   int acc;
   bool residual;
-  float tm, ts, qm, qs;
+  float tm, ts, qm, qs, ustar;
 };
 
-template <bool BF16>
-__device__ SampleSel sampling_decision(const AcceptArgs &a, int s) {
+__device__ SampleSel sampling_decision(const AcceptArgs &a, int s, int B) {
   const int lane = threadIdx.x & 63;
-  const int B = a.block_lens[s];
   const int n = B - 1;
-  const int off = a.q_offsets[s];
-  const int doff = off - s;
-  float tm = -INFINITY, ts = 0.f, qm = -INFINITY, qs = 0.f;
+  float tm = -INFINITY, ts = 0.f, qm = -INFINITY, qs = 0.f, td = NAN, dd = NAN, u = 0.f;
+  if (lane < a.mb)  // issued before B arrives; positions >= B are ignored below
+    merge_records2(a.stats + (size_t)(s * a.mb + lane) * a.nch, a.stats + (size_t)((a.S + s) * a.mb + lane) * a.nch,
+                   a.nch, a.c, tm, ts, td, u, qm, qs, dd);
   bool rejects = false;
-  // issue the draft token load first: the two logit gathers depend on it
-  const int d = (lane < n) ? a.draft_tokens[doff + lane] : 0;
-  if (lane < B) merge_lse_partials(a.stats + (size_t)(off + lane) * a.nch, a.nch, a.c, tm, ts);
   if (lane < n) {
-    merge_lse_partials(a.stats + (size_t)(a.total_q + doff + lane) * a.nch, a.nch, a.c, qm, qs);
-    const float td = load_elem<BF16>(a.target, (long long)(off + lane) * a.V + d);
-    const float dd = load_elem<BF16>(a.draft, (long long)(doff + lane) * a.V + d);
-    // rho = p(d) / q(d) = exp2((td - tm) c - (dd - qm) c) * qs / ts; q(d) = 0 accepts
+    // rho = p(d) / q(d) = exp2((td - tm) c - (dd - qm) c) * qs / ts; q(d) = 0 accepts.  A token
+    // outside the vocabulary leaves td, dd NaN and is rejected.
     const double lr = (double)((td - tm) * a.c) - (double)((dd - qm) * a.c);
     const double rho = (dd != -INFINITY) ? exp2(lr) * (double)qs / (double)ts : INFINITY;
-    rejects = !((double)a.uniforms[off + lane] < rho);
+    rejects = !((double)u < rho);
   }
   const unsigned long long rej = __ballot(rejects);
   SampleSel r;
@@ -318,240 +459,323 @@ __device__ SampleSel sampling_decision(const AcceptArgs &a, int s) {
   r.ts = __shfl(ts, r.acc, 64);
   r.qm = __shfl(qm, r.acc, 64);
   r.qs = __shfl(qs, r.acc, 64);
+  r.ustar = __shfl(u, B - 1, 64);
   return r;
 }
 
-// Residual / target mass of one element in the sampling pass.  si0 = (row, residual?,
-// target max, 1/target sum), si1 = (draft max, 1/draft sum, -, -).
-__device__ __forceinline__ void sample_masses(float t, float q, const float4 &si0, const float4 &si1, float c,
-                                              float &r, float &p) {
-  p = fast_exp2((t - si0.z) * c) * si0.w;
-  if (si0.y != 0.f) {
-    const float qq = fast_exp2((q - si1.x) * c) * si1.y;
+// Normalised sampling mass of one element: p = exp2((t - tm) c) / ts, and at a rejection the
+// residual max(0, p - q) with q = exp2((d - qm) c) / qs.  Both sampling kernels call this one
+// function, so a chunk's mass and its rescan agree.
+struct SampleParams {
+  float tm, inv_ts, qm, inv_qs, c;
+};
+
+__device__ __forceinline__ void elem_masses(float t, float q, const SampleParams &sp, bool residual, float &r,
+                                            float &p) {
+  p = fast_exp2((t - sp.tm) * sp.c) * sp.inv_ts;
+  if (residual) {
+    const float qq = fast_exp2((q - sp.qm) * sp.c) * sp.inv_qs;
     r = fmaxf(p - qq, 0.f);
   } else {
     r = p;
   }
 }
 
+// Sampling masses, grid = (sequence, vocab chunk).  Every workgroup makes the decision,
+// then sums the residual (or p at the bonus row) and p over its chunk of the selected row.
 template <bool BF16>
-__global__ __launch_bounds__(256) void accept_sample_kernel(AcceptArgs a) {
+__global__ __launch_bounds__(256) void accept_mass_kernel(AcceptArgs a) {
   constexpr int VEC = BF16 ? 8 : 4;
-  __shared__ double sh_r[4], sh_p[4];
   __shared__ float4 sh_si[2];
-
+  __shared__ double sh_r[4], sh_p[4];
   const int s = blockIdx.x / a.nch2;
   const int c = blockIdx.x % a.nch2;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int B = ld_uniform(a.block_lens, s);
+  const int off = ld_uniform(a.q_offsets, s);
   if (wave == 0) {
-    const SampleSel sel = sampling_decision<BF16>(a, s);
+    const SampleSel sel = sampling_decision(a, s, B);
     if (lane == 0) {
-      const float4 si0{__int_as_float(sel.acc), sel.residual ? 1.f : 0.f, sel.tm, 1.f / sel.ts};
-      const float4 si1{sel.residual ? sel.qm : 0.f, sel.residual ? 1.f / sel.qs : 0.f, 0.f, 0.f};
-      sh_si[0] = si0;
-      sh_si[1] = si1;
+      const float4 s0{__int_as_float(sel.acc), sel.residual ? 1.f : 0.f, sel.tm, 1.f / sel.ts};
+      const float4 s1{sel.residual ? sel.qm : 0.f, sel.residual ? 1.f / sel.qs : 0.f, sel.ustar, 0.f};
+      sh_si[0] = s0;
+      sh_si[1] = s1;
       if (c == 0) {
         a.accept_len[s] = sel.acc;
-        a.seqinfo[2 * s] = si0;
-        a.seqinfo[2 * s + 1] = si1;
+        a.seqinfo[2 * s] = s0;
+        a.seqinfo[2 * s + 1] = s1;
       }
     }
   }
   __syncthreads();
   const float4 si0 = sh_si[0], si1 = sh_si[1];
   const int j = __float_as_int(si0.x);
-  const int off = a.q_offsets[s];
-  const long long ta0 = (long long)(off + j) * a.V;
-  const long long da0 = (long long)(off - s + j) * a.V;  // read only for a residual draw
   const bool residual = si0.y != 0.f;
+  const SampleParams sp{si0.z, si0.w, si1.x, si1.y, a.c};
+  const long long ta0 = (long long)(off + j) * a.V;
+  const long long da0 = (long long)(off - s + j) * a.V;  // read only at a rejection
   const RowChunk ch = row_chunk<VEC>(ta0, a.V, c, a.nch2);
+  // the draft row shares the target row's vector alignment iff (ta0 - da0) % VEC == 0
+  const bool dvec = ((ta0 - da0) % VEC) == 0;
 
-  float sr = 0.f, sp = 0.f;
-  auto scalar_range = [&](int e0, int e1) {
-    for (int e = e0 + tid; e < e1; e += 256) {
-      const float t = load_elem<BF16>(a.target, ta0 + e);
-      const float q = residual ? load_elem<BF16>(a.draft, da0 + e) : 0.f;
-      float r, p;
-      sample_masses(t, q, si0, si1, a.c, r, p);
-      sr += r;
-      sp += p;
-    }
-  };
-  scalar_range(ch.hb, ch.he);
-  // The draft row shares the target row's vector alignment only when (ta0 - da0) is a
-  // multiple of VEC; otherwise its elements are read one by one.
-  const bool draft_vec = ((ta0 - da0) % VEC) == 0;
-  const u32x4 *tv = reinterpret_cast<const u32x4 *>(a.target);
-  for (long long v = ch.vb + tid; v < ch.ve; v += 256) {
-    float t8[VEC], q8[VEC];
-    unpack<BF16>(tv[v], t8);
-    const long long rel = v * VEC - ta0;
-    if (residual) {
-      if (draft_vec) {
-        unpack<BF16>(reinterpret_cast<const u32x4 *>(a.draft)[(da0 + rel) / VEC], q8);
-      } else {
+  float sr = 0.f, spm = 0.f;
+  const char *tbase = reinterpret_cast<const char *>(a.target) + ch.vb * 16;
+  const char *dbase = reinterpret_cast<const char *>(a.draft) + (ch.vb + (da0 - ta0) / VEC) * 16;
+  const unsigned nvc = (unsigned)(ch.ve - ch.vb);
+  for (unsigned r0 = tid; r0 < nvc; r0 += 256u * kMassVecs) {
+    u32x4 tb[kMassVecs], qb[kMassVecs];
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) q8[e] = load_elem<BF16>(a.draft, da0 + rel + e);
+    for (int u = 0; u < kMassVecs; ++u) {  // clamped: no per-load branch (r0 < nvc here)
+      const unsigned r = min(r0 + 256u * u, nvc - 1u);
+      tb[u] = *reinterpret_cast<const u32x4 *>(tbase + r * 16u);
+      qb[u] = u32x4{0u, 0u, 0u, 0u};
+    }
+    if (residual && dvec) {
+#pragma unroll
+      for (int u = 0; u < kMassVecs; ++u)
+        qb[u] = *reinterpret_cast<const u32x4 *>(dbase + min(r0 + 256u * u, nvc - 1u) * 16u);
+    }
+#pragma unroll
+    for (int u = 0; u < kMassVecs; ++u) {
+      const unsigned r = r0 + 256u * u;
+      float t[VEC], q[VEC];
+      unpack<BF16>(tb[u], t);
+      unpack<BF16>(qb[u], q);
+      if (residual && !dvec && r < nvc) {
+        const long long e = (ch.vb + r) * VEC - ta0 + da0;
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) q[i] = load_elem<BF16>(a.draft, e + i);
       }
-    } else {
+      float vr = 0.f, vp = 0.f;
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) q8[e] = 0.f;
-    }
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) {
-      float r, p;
-      sample_masses(t8[e], q8[e], si0, si1, a.c, r, p);
-      sr += r;
-      sp += p;
+      for (int i = 0; i < VEC; ++i) {
+        float er, ep;
+        elem_masses(t[i], q[i], sp, residual, er, ep);
+        vr += er;
+        vp += ep;
+      }
+      if (r < nvc) {
+        sr += vr;
+        spm += vp;
+      }
     }
   }
-  scalar_range(ch.tb, ch.te);
-
-  double dr = sr, dp = sp;
-#pragma unroll
-  for (int msk = 1; msk < 64; msk <<= 1) {
-    dr += __shfl_xor(dr, msk, 64);
-    dp += __shfl_xor(dp, msk, 64);
+  // scalar head (chunk 0) and tail (last chunk): fewer than 2 * VEC elements each
+  for (int e = ch.hb + tid; e < ch.he; e += 256) {
+    float er, ep;
+    elem_masses(load_elem<BF16>(a.target, ta0 + e), residual ? load_elem<BF16>(a.draft, da0 + e) : 0.f, sp,
+                residual, er, ep);
+    sr += er;
+    spm += ep;
   }
-  if (lane == 0) { sh_r[wave] = dr; sh_p[wave] = dp; }
+  for (int e = ch.tb + tid; e < ch.te; e += 256) {
+    float er, ep;
+    elem_masses(load_elem<BF16>(a.target, ta0 + e), residual ? load_elem<BF16>(a.draft, da0 + e) : 0.f, sp,
+                residual, er, ep);
+    sr += er;
+    spm += ep;
+  }
+  const float wr = wave_sum_f(sr), wp = wave_sum_f(spm);
+  if (lane == 0) { sh_r[wave] = wr; sh_p[wave] = wp; }
   __syncthreads();
   if (tid == 0)
-    a.samp[(size_t)s * a.nch2 + c] =
-        double2{sh_r[0] + sh_r[1] + sh_r[2] + sh_r[3], sh_p[0] + sh_p[1] + sh_p[2] + sh_p[3]};
+    a.samp[(size_t)s * a.nch2 + c] = double2{sh_r[0] + sh_r[1] + sh_r[2] + sh_r[3], sh_p[0] + sh_p[1] + sh_p[2] + sh_p[3]};
 }
 
-constexpr int kScanRun = 24;  // elements per thread in the final scan (chunks hold <= 4096 + 7)
-
-// Block-wide inclusive scan of one double per thread (256 threads): wavefront shuffles,
-// then the wavefront totals through LDS.  Returns the inclusive prefix; *total gets the sum.
-__device__ __forceinline__ double block_scan_incl(double v, double *sh4, double *total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const double u = __shfl_up(v, o, 64);
-    if (lane >= o) v += u;
-  }
-  if (lane == 63) sh4[wave] = v;
-  __syncthreads();
-  double before = 0.0;
-  for (int w2 = 0; w2 < wave; ++w2) before += sh4[w2];
-  *total = sh4[0] + sh4[1] + sh4[2] + sh4[3];
-  __syncthreads();
-  return v + before;
-}
-
-// Final inverse-CDF draw for sequence s: locate the chunk holding u* times the total
-// mass (block-wide scan of the chunk masses), then scan that chunk in vocabulary order
-// with a contiguous run of elements per thread, held in registers.
+// Final draw for sequence s (T > 0), one workgroup per sequence.  Wavefront 0 scans the
+// chunk sums for the chunk whose cumulative-mass interval holds u* times the total; then each
+// thread takes a contiguous run of that chunk's vectors (thread 0 also the unaligned head,
+// the last thread the tail), the runs' masses are scanned across the workgroup, and the one
+// thread whose interval holds the target walks its run in vocabulary order.  A residual with
+// no mass (rounding only) draws from p instead.
 template <bool BF16>
-__global__ __launch_bounds__(256) void accept_scan_kernel(AcceptArgs a) {
+__global__ __launch_bounds__(kLocThreads) void accept_locate_kernel(AcceptArgs a) {
   constexpr int VEC = BF16 ? 8 : 4;
-  __shared__ double sh4[4];
-  __shared__ int s_chunk, s_lastpos, s_found;
-
+  constexpr int NW = kLocThreads / 64;
+  __shared__ double sh_w[NW];
+  __shared__ double sh_cex, sh_tgt;
+  __shared__ int sh_kc, sh_usep, sh_hit;
+  __shared__ int sh_last[NW];
   const int s = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int B = a.block_lens[s];
-  const int off = a.q_offsets[s];
-  const float4 si0 = a.seqinfo[2 * s], si1 = a.seqinfo[2 * s + 1];
+  const float4 si0 = ld_uniform4(a.seqinfo, 2 * s), si1 = ld_uniform4(a.seqinfo, 2 * s + 1);
+  const int off = ld_uniform(a.q_offsets, s);
   const int j = __float_as_int(si0.x);
   const bool residual = si0.y != 0.f;
+  const SampleParams sp{si0.z, si0.w, si1.x, si1.y, a.c};
+  const double ustar = (double)si1.z;
+
+  if (wave == 0) {
+    // chunk search, 64 chunks per pass; consecutive intervals meet exactly across passes
+    const double2 *cs = a.samp + (size_t)s * a.nch2;
+    auto chunk_sums = [&](int k0) {  // clamped: no per-load branch
+      double2 cm = cs[min(k0 + lane, a.nch2 - 1)];
+      if (k0 + lane >= a.nch2) cm = double2{0.0, 0.0};
+      return cm;
+    };
+    const double2 cm0 = chunk_sums(0);
+    bool any_r = __ballot(cm0.x > 0.0) != 0;
+    for (int k0 = 64; k0 < a.nch2; k0 += 64) any_r |= __ballot(chunk_sums(k0).x > 0.0) != 0;
+    const bool use_p = !any_r;  // residual without mass (rounding only): draw from p
+    double carry = 0.0;
+    for (int k0 = 0; k0 < a.nch2; k0 += 64) {
+      const double2 cm = k0 ? chunk_sums(k0) : cm0;
+      double ex;
+      const double in = wave_scan_d(use_p ? cm.y : cm.x, &ex);
+      carry += readlane_d(in, 63);
+    }
+    const double tgt = ustar * carry;
+    int kc = -1, klast = -1;
+    double cex = 0.0;
+    carry = 0.0;
+    for (int k0 = 0; k0 < a.nch2; k0 += 64) {
+      const double2 cm = k0 ? chunk_sums(k0) : cm0;
+      const double m = use_p ? cm.y : cm.x;
+      double ex;
+      const double in = wave_scan_d(m, &ex);
+      const double lo = carry + ex, hi = carry + in;
+      const unsigned long long hit = __ballot(m > 0.0 && lo <= tgt && tgt < hi);
+      if (hit && kc < 0) {
+        const int l = __ffsll((long long)hit) - 1;
+        kc = k0 + l;
+        cex = readlane_d(lo, l);
+      }
+      const unsigned long long pos = __ballot(m > 0.0);
+      if (pos) klast = k0 + 63 - __clzll((long long)pos);
+      carry = carry + readlane_d(in, 63);
+    }
+    if (lane == 0) {
+      sh_kc = kc >= 0 ? kc : max(klast, 0);  // rounding: the last chunk with mass
+      sh_cex = kc >= 0 ? cex : INFINITY;     // INFINITY: take its last token with mass
+      sh_tgt = tgt;
+      sh_usep = use_p;
+      sh_hit = 0;
+    }
+  }
+  __syncthreads();
+  const int kc = sh_kc;
+  const double cex = sh_cex, tgt = sh_tgt;
+  const bool use_q = residual && !sh_usep;
+
+  // this thread's run of chunk kc: vectors [v0, v1) relative to the chunk, plus the head
+  // (thread 0) and the tail (last thread) elements
   const long long ta0 = (long long)(off + j) * a.V;
   const long long da0 = (long long)(off - s + j) * a.V;
-  const double2 *cs = a.samp + (size_t)s * a.nch2;
-  const double ustar = (double)a.uniforms[off + B - 1];
-
-  // totals of the residual and of p (p is the fallback when the residual has no mass)
-  double tr = 0.0, tp = 0.0;
-  for (int k = tid; k < a.nch2; k += 256) {
-    const double2 c = cs[k];
-    tr += c.x;
-    tp += c.y;
-  }
-  double tot_r, tot_p;
-  block_scan_incl(tr, sh4, &tot_r);
-  block_scan_incl(tp, sh4, &tot_p);
-  const bool use_p = !(tot_r > 0.0);
-  const double tot = use_p ? tot_p : tot_r;
-  const double tgt = ustar * tot;
-  if (tid == 0) {
-    s_chunk = INT_MAX;
-    s_lastpos = 0;
-    s_found = INT_MAX;
-  }
-  __syncthreads();
-  // locate the chunk: first k whose cumulative mass exceeds tgt
-  double carry = 0.0, chunk_excl = 0.0;
-  for (int base = 0; base < a.nch2; base += 256) {
-    const int k = base + tid;
-    const double m = (k < a.nch2) ? (use_p ? cs[k].y : cs[k].x) : 0.0;
-    double seg;
-    const double incl = block_scan_incl(m, sh4, &seg) + carry;
-    if (m > 0.0) {
-      atomicMax(&s_lastpos, k);
-      if (incl - m <= tgt && tgt < incl) atomicMin(&s_chunk, k);
-    }
-    carry += seg;
-  }
-  __syncthreads();
-  const bool found_chunk = s_chunk != INT_MAX;
-  const int cstar = found_chunk ? s_chunk : s_lastpos;  // rounding: last chunk with mass
-  // mass before chunk cstar (recomputed the same way by every thread)
-  {
-    double before = 0.0;
-    for (int k = tid; k < cstar; k += 256) before += use_p ? cs[k].y : cs[k].x;
-    double t;
-    block_scan_incl(before, sh4, &t);
-    chunk_excl = t;
-  }
-  const double ctgt = found_chunk ? tgt - chunk_excl : INFINITY;
-
-  // scan chunk cstar: this thread's contiguous run, masses kept in registers
-  const bool use_q = residual && !use_p;
-  const RowChunk cc = row_chunk<VEC>(ta0, a.V, cstar, a.nch2);
-  const int len = cc.e1 - cc.e0;
-  const int run = (len + 255) / 256;  // <= kScanRun for chunks of at most 4096 + 7 elements
-  const int e_beg = min(cc.e0 + tid * run, cc.e1), e_end = min(e_beg + run, cc.e1);
-  float mass[kScanRun];
-  double own = 0.0;
-  int last_pos_own = -1;
-#pragma unroll
-  for (int k = 0; k < kScanRun; ++k) {
-    const int e = e_beg + k;
-    float t = 0.f, q = 0.f;
-    if (e < e_end) {
-      t = load_elem<BF16>(a.target, ta0 + e);
-      if (use_q) q = load_elem<BF16>(a.draft, da0 + e);
-    }
+  const RowChunk cc = row_chunk<VEC>(ta0, a.V, kc, a.nch2);
+  const int nvc = (int)(cc.ve - cc.vb);
+  const int rv = (nvc + kLocThreads - 1) / kLocThreads;
+  const int v0 = min(tid * rv, nvc), v1 = min(v0 + rv, nvc);
+  const bool dvec = ((ta0 - da0) % VEC) == 0;
+  auto mass_at = [&](float t, float q) {
     float r, p;
-    sample_masses(t, q, si0, si1, a.c, r, p);
-    mass[k] = (e < e_end) ? (use_q ? r : p) : 0.f;
-    own += (double)mass[k];
-    if (mass[k] > 0.f) last_pos_own = e;
-  }
-  double dummy;
-  const double incl = block_scan_incl(own, sh4, &dummy);
-  const double excl = incl - own;
-  if (ctgt != INFINITY && excl <= ctgt && ctgt < incl) {
-    double cum = excl;
-    int found = -1;
-#pragma unroll
-    for (int k = 0; k < kScanRun; ++k) {
-      cum += (double)mass[k];
-      if (found < 0 && cum > ctgt && e_beg + k < e_end) found = e_beg + k;
+    elem_masses(t, q, sp, use_q, r, p);
+    return use_q ? r : p;
+  };
+  auto scalar_mass = [&](int e) {
+    return mass_at(load_elem<BF16>(a.target, ta0 + e), use_q ? load_elem<BF16>(a.draft, da0 + e) : 0.f);
+  };
+  double own = 0.0;
+  int elast = -1;
+  if (tid == 0)
+    for (int e = cc.hb; e < cc.he; ++e) {
+      const float m = scalar_mass(e);
+      own += (double)m;
+      if (m > 0.f) elast = e;
     }
-    if (found < 0) found = last_pos_own;  // rounding: the run's last token with mass
-    if (found >= 0) atomicMin(&s_found, found);
-  }
-  int lp = last_pos_own;
+  float mreg[kLocVecs * VEC];
+  const char *tb = reinterpret_cast<const char *>(a.target) + cc.vb * 16;
+  const char *db = reinterpret_cast<const char *>(a.draft) + (cc.vb + (da0 - ta0) / VEC) * 16;
+  if (rv <= kLocVecs) {
+    u32x4 tv[kLocVecs], qv[kLocVecs];
 #pragma unroll
-  for (int msk = 1; msk < 64; msk <<= 1) lp = max(lp, __shfl_xor(lp, msk, 64));
-  if (lane == 0) sh4[wave] = (double)lp;
+    for (int u = 0; u < kLocVecs; ++u) tv[u] = qv[u] = u32x4{0u, 0u, 0u, 0u};
+    if (nvc > 0) {  // clamped: no per-load branch
+      const bool ld_q = use_q && dvec;
+#pragma unroll
+      for (int u = 0; u < kLocVecs; ++u) {
+        const unsigned r = (unsigned)min(v0 + u, nvc - 1);
+        tv[u] = *reinterpret_cast<const u32x4 *>(tb + r * 16u);
+        if (ld_q) qv[u] = *reinterpret_cast<const u32x4 *>(db + r * 16u);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kLocVecs; ++u) {
+      float t[VEC], q[VEC];
+      unpack<BF16>(tv[u], t);
+      unpack<BF16>(qv[u], q);
+      const int eb = (int)((cc.vb + v0 + u) * VEC - ta0);
+      if (use_q && !dvec && v0 + u < v1) {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) q[i] = load_elem<BF16>(a.draft, da0 + eb + i);
+      }
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) {
+        const float m = (v0 + u < v1) ? mass_at(t[i], q[i]) : 0.f;
+        mreg[u * VEC + i] = m;
+        own += (double)m;
+        if (m > 0.f) elast = eb + i;
+      }
+    }
+  } else {  // runs longer than the register window: masses recomputed by the walk below
+    for (int v = v0; v < v1; ++v) {
+      const int eb = (int)((cc.vb + v) * VEC - ta0);
+      for (int i = 0; i < VEC; ++i) {
+        const float m = scalar_mass(eb + i);
+        own += (double)m;
+        if (m > 0.f) elast = eb + i;
+      }
+    }
+  }
+  if (tid == kLocThreads - 1)
+    for (int e = cc.tb; e < cc.te; ++e) {
+      const float m = scalar_mass(e);
+      own += (double)m;
+      if (m > 0.f) elast = e;
+    }
+
+  // workgroup scan of the run masses; consecutive intervals meet exactly
+  double ex;
+  const double in = wave_scan_d(own, &ex);
+  if (lane == 63) sh_w[wave] = in;
   __syncthreads();
-  if (tid == 0) {
-    int tok = s_found;
-    if (tok == INT_MAX) tok = (int)fmax(fmax(sh4[0], sh4[1]), fmax(sh4[2], sh4[3]));
-    a.next_token[s] = tok;
+  double before = 0.0;
+  for (int w2 = 0; w2 < wave; ++w2) before += sh_w[w2];
+  const double lo = cex + (before + ex), hi = cex + (before + in);
+  if (own > 0.0 && lo <= tgt && tgt < hi) {  // at most one thread: walk its run
+    double cum = lo;
+    int found = -1;
+    auto step = [&](int e, float m) {
+      if (found < 0 && m > 0.f) {
+        if (cum + (double)m > tgt) found = e;
+        cum += (double)m;
+      }
+    };
+    if (tid == 0)
+      for (int e = cc.hb; e < cc.he; ++e) step(e, scalar_mass(e));
+    if (rv <= kLocVecs) {
+#pragma unroll
+      for (int u = 0; u < kLocVecs; ++u)
+#pragma unroll
+        for (int i = 0; i < VEC; ++i)
+          if (v0 + u < v1) step((int)((cc.vb + v0 + u) * VEC - ta0) + i, mreg[u * VEC + i]);
+    } else {
+      for (int v = v0; v < v1; ++v) {
+        const int eb = (int)((cc.vb + v) * VEC - ta0);
+        for (int i = 0; i < VEC; ++i) step(eb + i, scalar_mass(eb + i));
+      }
+    }
+    if (tid == kLocThreads - 1)
+      for (int e = cc.tb; e < cc.te; ++e) step(e, scalar_mass(e));
+    a.next_token[s] = found >= 0 ? found : elast;  // rounding: the run's last token with mass
+    sh_hit = 1;
+  }
+  const int wl = wave_max_i(elast);
+  if (lane == 0) sh_last[wave] = wl;
+  __syncthreads();
+  if (tid == 0 && !sh_hit) {  // rounding: the chunk's last token with mass (0 if none)
+    int t = -1;
+    for (int w2 = 0; w2 < NW; ++w2) t = max(t, sh_last[w2]);
+    a.next_token[s] = max(t, 0);
   }
 }
 

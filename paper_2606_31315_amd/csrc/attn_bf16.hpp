@@ -36,11 +36,6 @@ __device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2v));
 }
 
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-
 // ds_read_b64_tr_b16 issued as inline assembly: the intrinsic form makes the compiler
 // assume it may alias the in-flight load-to-LDS writes and wait for all of them (the
 // explicit vmcnt wait and barrier at the top of each tile already order these reads).

@@ -135,15 +135,15 @@ void launch_attn_all(const sdb::AttnArgs &a, int grid, int MT, hipStream_t st) {
 // acceptance planning
 // ---------------------------------------------------------------------------
 struct AcceptPlan {
-  int rows, nch, nch2;
-  size_t off_stats, off_info, off_samp, total;
+  int rows, nch, nch2, stats_grid;
+  size_t off_stats, off_samp, off_seq, total;
 };
 
 int accept_plan(const sd_accept_shape *sh, float temperature, AcceptPlan *p) {
   if (!sh) return fail(SD_ERR_INVALID_ARG, "sd_accept: shape is NULL");
   const int S = sh->num_seqs, V = sh->vocab;
   if (S < 0) return fail(SD_ERR_INVALID_ARG, "num_seqs must be >= 0 (got %d)", S);
-  if (V < 1) return fail(SD_ERR_INVALID_ARG, "vocab must be >= 1 (got %d)", V);
+  if (V < 1 || V > (1 << 28)) return fail(SD_ERR_INVALID_ARG, "vocab must be in [1, 2^28] (got %d)", V);
   if (sh->dtype != SD_BF16 && sh->dtype != SD_F32) return fail(SD_ERR_INVALID_ARG, "unknown dtype %d", sh->dtype);
   if (sh->max_block < 1 || sh->max_block > 64)
     return fail(SD_ERR_INVALID_ARG, "max_block must be in [1, 64] (got %d)", sh->max_block);
@@ -156,29 +156,31 @@ int accept_plan(const sd_accept_shape *sh, float temperature, AcceptPlan *p) {
   if (rows * (long long)V > (1LL << 46)) return fail(SD_ERR_INVALID_ARG, "problem too large");
   const int VEC = (sh->dtype == SD_BF16) ? 8 : 4;
   const long long vecs = V / VEC;
-  const long long max_ch = vecs / 256 > 0 ? vecs / 256 : 1;  // at least one vector per thread
-  // statistics chunks: about 1024 workgroups of tens of KB each
-  long long nch = rows > 0 ? (1024 + rows - 1) / rows : 1;
-  if (nch > max_ch) nch = max_ch;
+  // statistics chunks: kStatsChunk whole vectors each (one load of kStatsVecs vectors per
+  // thread); a row holds vecs or vecs - 1 whole vectors, the last chunk takes the rest
+  long long nch = (vecs + sdb::kStatsChunk - 1) / sdb::kStatsChunk;
   if (nch < 1) nch = 1;
-  // sampling chunks: about 512 workgroups, and at most 4096 elements per chunk so the
-  // final scan's per-thread runs stay short
+  // sampling chunks: about 512 workgroups in the mass kernel, and chunks short enough for
+  // the locate kernel to hold one run of at most kLocVecs vectors per thread in registers
   long long nch2 = S > 0 ? (512 + S - 1) / S : 1;
-  if (nch2 < (V + 4095) / 4096) nch2 = (V + 4095) / 4096;
-  if (nch2 > max_ch) nch2 = max_ch;
+  const long long loc_cap = (long long)sdb::kLocThreads * sdb::kLocVecs - 2;  // vectors per chunk
+  if (nch2 < (vecs + loc_cap - 1) / loc_cap) nch2 = (vecs + loc_cap - 1) / loc_cap;
+  if (nch2 > sdb::kMaxChunks2) nch2 = sdb::kMaxChunks2;
   if (nch2 < 1) nch2 = 1;
-  if (rows * nch > (1LL << 30) || (long long)S * nch2 > (1LL << 30))
-    return fail(SD_ERR_INVALID_ARG, "problem too large");
+  if (rows * nch > (1LL << 30)) return fail(SD_ERR_INVALID_ARG, "problem too large");
+  const long long items = rows * nch;
   p->rows = (int)rows;
   p->nch = (int)nch;
   p->nch2 = (int)nch2;
+  p->stats_grid = (int)(items > 0 ? items : 1);
+  const size_t kinds = sample ? 2 : 1;
   size_t off = 0;
   p->off_stats = off;
-  off = align256(off + (size_t)rows * nch * sizeof(float2));
-  p->off_info = off;
-  off = align256(off + (size_t)S * 2 * sizeof(float4));
+  off = align256(off + kinds * (size_t)S * sh->max_block * nch * sizeof(float4));
   p->off_samp = off;
   if (sample) off = align256(off + (size_t)S * nch2 * sizeof(double2));
+  p->off_seq = off;
+  if (sample) off = align256(off + (size_t)S * 2 * sizeof(float4));
   p->total = off > 0 ? off : 256;
   return ok();
 }
@@ -293,38 +295,45 @@ int sd_accept(const sd_accept_shape *sh, const void *target_logits, const void *
   a.accept_len = accept_len;
   a.next_token = next_token;
   char *ws = (char *)workspace;
-  a.stats = (float2 *)(ws + p.off_stats);
-  a.seqinfo = (float4 *)(ws + p.off_info);
+  a.stats = (float4 *)(ws + p.off_stats);
   a.samp = (double2 *)(ws + p.off_samp);
+  a.seqinfo = (float4 *)(ws + p.off_seq);
   a.S = sh->num_seqs;
   a.V = sh->vocab;
   a.total_q = sh->total_q;
+  a.rows = p.rows;
+  a.mb = sh->max_block;
   a.nch = p.nch;
   a.nch2 = p.nch2;
   a.c = sample ? (float)(1.4426950408889634 / (double)temperature) : 0.f;
   hipStream_t st = (hipStream_t)stream;
   const bool bf = sh->dtype == SD_BF16;
-  const unsigned g1 = (unsigned)(p.rows * p.nch);
+  const unsigned g1 = (unsigned)p.stats_grid;
   const unsigned S = (unsigned)sh->num_seqs;
+  // every statistics chunk holds a whole 16-byte vector unless the vocabulary is tiny (then
+  // there is one chunk and at most 2 VEC - 2 < 256 elements per row)
+  const bool vecs = sh->vocab >= 2 * (bf ? 8 : 4) - 1;
+#define SDB_STATS(BF, SMP)                                                                                    \
+  do {                                                                                                       \
+    if (vecs) hipLaunchKernelGGL((sdb::accept_stats_kernel<BF, SMP, true>), dim3(g1), dim3(256), 0, st, a);  \
+    else hipLaunchKernelGGL((sdb::accept_stats_kernel<BF, SMP, false>), dim3(g1), dim3(256), 0, st, a);      \
+  } while (0)
   if (sample) {
     if (bf) {
-      hipLaunchKernelGGL((sdb::accept_stats_kernel<true, true>), dim3(g1), dim3(256), 0, st, a);
-      hipLaunchKernelGGL((sdb::accept_sample_kernel<true>), dim3(S * p.nch2), dim3(256), 0, st, a);
-      hipLaunchKernelGGL((sdb::accept_scan_kernel<true>), dim3(S), dim3(256), 0, st, a);
+      SDB_STATS(true, true);
+      hipLaunchKernelGGL((sdb::accept_mass_kernel<true>), dim3(S * p.nch2), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((sdb::accept_locate_kernel<true>), dim3(S), dim3(sdb::kLocThreads), 0, st, a);
     } else {
-      hipLaunchKernelGGL((sdb::accept_stats_kernel<false, true>), dim3(g1), dim3(256), 0, st, a);
-      hipLaunchKernelGGL((sdb::accept_sample_kernel<false>), dim3(S * p.nch2), dim3(256), 0, st, a);
-      hipLaunchKernelGGL((sdb::accept_scan_kernel<false>), dim3(S), dim3(256), 0, st, a);
+      SDB_STATS(false, true);
+      hipLaunchKernelGGL((sdb::accept_mass_kernel<false>), dim3(S * p.nch2), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((sdb::accept_locate_kernel<false>), dim3(S), dim3(sdb::kLocThreads), 0, st, a);
     }
   } else {
-    if (bf) {
-      hipLaunchKernelGGL((sdb::accept_stats_kernel<true, false>), dim3(g1), dim3(256), 0, st, a);
-      hipLaunchKernelGGL((sdb::accept_greedy_kernel<true>), dim3(S), dim3(64), 0, st, a);
-    } else {
-      hipLaunchKernelGGL((sdb::accept_stats_kernel<false, false>), dim3(g1), dim3(256), 0, st, a);
-      hipLaunchKernelGGL((sdb::accept_greedy_kernel<false>), dim3(S), dim3(64), 0, st, a);
-    }
+    if (bf) SDB_STATS(true, false);
+    else SDB_STATS(false, false);
+    hipLaunchKernelGGL(sdb::accept_greedy_kernel, dim3(S), dim3(64), 0, st, a);
   }
+#undef SDB_STATS
   return check_launch("sd_accept");
 }
 
