@@ -135,3 +135,24 @@ def test_repeated_calls_reuse_workspace():
     G.compare_accept(small, als, nts, ref)
     a2 = G.run_accept(big, d, workspace=ws)
     assert (a1[0] == a2[0]).all() and (a1[1] == a2[1]).all()
+
+
+def test_one_workspace_shared_with_attention():
+    """One scratch buffer, holding arbitrary bytes on entry, serves attention and acceptance at
+    T = 0 and T = 1 in turn; every acceptance result follows the parity rule."""
+    import paper_2606_31315_amd as sd
+    pa = W.c3_ragged(temperatures=(), dtype="bf16").attn
+    da = G.attn_to_device(pa)
+    probs = [_many_seq_problem(71, 12, 151936, (1, 24), "bf16", T, target_sigma=3.0, noise_sigma=1.0,
+                               name=f"shared_T{T:g}") for T in (0.0, 1.0)]
+    dev_p = [G.accept_to_device(p) for p in probs]
+    refs = [G.oracle_accept(p) for p in probs]
+    n = max([sd.attn_workspace_size(sd.attn_shape(da["q"], da["k"], pa.max_ctx, pa.max_block))] +
+            [sd.accept_workspace_size(sd.accept_shape(d["t"], p.S, p.max_block), p.temperature)
+             for p, d in zip(probs, dev_p)])
+    ws = torch.randint(0, 256, (n,), dtype=torch.uint8, device=G.dev())
+    for it in range(3):
+        G.run_attn(pa, da, workspace=ws)
+        for p, d, ref in zip(probs, dev_p, refs):
+            al, nt = G.run_accept(p, d, workspace=ws)
+            G.compare_accept(p, al, nt, ref)

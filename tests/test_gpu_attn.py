@@ -105,3 +105,34 @@ def test_repeated_calls_reuse_workspace():
     assert np.abs(o_small - ref).max() < 2e-2
     o2 = G.run_attn(big, d, workspace=ws)
     assert torch.equal(o1, o2)
+
+
+def test_alternating_calls_arbitrary_workspace():
+    """A workspace filled with arbitrary bytes, then shared by calls of different shapes in
+    turn, gives the oracle's answer on every call and bit-identical outputs for repeated
+    inputs (nothing is carried between calls through the workspace)."""
+    import oracle
+    import paper_2606_31315_amd as sd
+    rs = W._streams(606)
+    pa = W.make_attn(rs, S=4, Hq=32, Hkv=8, D=128, ctx_lens=[4000, 1500, 2600, 3333], block_lens=[24, 8, 13, 16],
+                     dtype="bf16", mask_mode=CAUSAL, name="alt_a")
+    pb = W.make_attn(rs, S=2, Hq=16, Hkv=4, D=128, ctx_lens=[5000, 700], block_lens=[32, 5], dtype="f32",
+                     mask_mode=BIDIR, name="alt_b")
+    da, db = G.attn_to_device(pa), G.attn_to_device(pb)
+    n = max(sd.attn_workspace_size(sd.attn_shape(da["q"], da["k"], pa.max_ctx, pa.max_block)),
+            sd.attn_workspace_size(sd.attn_shape(db["q"], db["k"], pb.max_ctx, pb.max_block)))
+    ws = torch.randint(0, 256, (n,), dtype=torch.uint8, device=G.dev())
+    refs = {}
+    for p in (pa, pb):
+        refs[p.name] = oracle.block_attn(p.q, p.k_cache, p.v_cache, p.ctx_lens, p.block_lens, p.q_offsets,
+                                         p.mask_mode)
+    first = {}
+    for it in range(6):
+        p, d = (pa, da) if it % 2 == 0 else (pb, db)
+        o = G.run_attn(p, d, workspace=ws).float().cpu()
+        err = np.abs(o.numpy().astype(np.float64) - refs[p.name]).max()
+        assert err <= G.ATTN_TOL[p.dtype], (it, p.name, err)
+        if p.name in first:
+            assert torch.equal(first[p.name], o), (it, p.name)
+        else:
+            first[p.name] = o
