@@ -415,16 +415,30 @@ __global__ __launch_bounds__(256) void block_attn_merge_kernel(AttnArgs a) {
   if (m >= M) return;
   const int d = (threadIdx.x % TPR) * 4;
   const size_t wbase = (size_t)sg * a.max_splits * a.Mpad + m;  // row m of split 0
-  float mx = -INFINITY;
-  for (int sp = 0; sp < nsplit; ++sp) mx = fmaxf(mx, a.part_ml[wbase + (size_t)sp * a.Mpad].x);
-  float lsum = 0.f;
+  // online merge over batches of SB splits whose loads are issued together (clamped, no
+  // per-load branch): one memory round trip per batch instead of one per split
+  constexpr int SB = 4;
+  float mx = -INFINITY, lsum = 0.f;
   f32x4 acc{0.f, 0.f, 0.f, 0.f};
-  for (int sp = 0; sp < nsplit; ++sp) {
-    const size_t r = wbase + (size_t)sp * a.Mpad;
-    const float2 ml = a.part_ml[r];
-    const float wgt = (ml.x == -INFINITY) ? 0.f : fast_exp2(ml.x - mx);
-    lsum += wgt * ml.y;
-    acc += wgt * *reinterpret_cast<const f32x4 *>(a.part_o + r * D + d);
+  for (int s0 = 0; s0 < nsplit; s0 += SB) {
+    float2 ml[SB];
+    f32x4 po[SB];
+#pragma unroll
+    for (int k = 0; k < SB; ++k) {
+      const size_t r = wbase + (size_t)min(s0 + k, nsplit - 1) * a.Mpad;
+      ml[k] = a.part_ml[r];
+      po[k] = *reinterpret_cast<const f32x4 *>(a.part_o + r * D + d);
+    }
+#pragma unroll
+    for (int k = 0; k < SB; ++k) {
+      if (s0 + k >= nsplit || ml[k].x == -INFINITY) continue;  // a split with no visible key
+      const float mn = fmaxf(mx, ml[k].x);
+      const float wo = (mx == -INFINITY) ? 0.f : fast_exp2(mx - mn);
+      const float wn = fast_exp2(ml[k].x - mn);
+      lsum = lsum * wo + ml[k].y * wn;
+      acc = acc * wo + po[k] * wn;
+      mx = mn;
+    }
   }
   const f32x4 o = acc * (1.f / lsum);
   const int qoff = a.q_offsets[s];
