@@ -16,8 +16,11 @@ exceeds 1 GB so the 256 MB Infinity Cache cannot serve them.  Prints one JSON li
 from __future__ import annotations
 
 import argparse
+import glob
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -65,6 +68,40 @@ def cpu_baseline(work, T, seconds):
             "sample": f"the full step (attention for all {a.total_q} block rows x {a.Hq} heads + acceptance of "
                       f"{a.S} sequences at T={T:g}), {reps} repetition(s), {per_step * 1e3:.1f} ms per step",
             "ms_per_step": per_step * 1e3}
+
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+COUNTERS = os.path.join(ROOT, "profiles", "counters_qwen3_4b_ragged_S8_ctx4096_T1.txt")
+
+
+def kernel_source_hash() -> str:
+    """sha256 over the kernel sources and the public header (file names and contents)."""
+    h = hashlib.sha256()
+    files = sorted(glob.glob(os.path.join(ROOT, "paper_2606_31315_amd", "csrc", "*")))
+    files.append(os.path.join(ROOT, "include", "sd_block.h"))
+    for f in files:
+        h.update(os.path.relpath(f, ROOT).encode())
+        h.update(b"\0")
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+        h.update(b"\0")
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per sd_block_attn call from the committed counter runs (FETCH_SIZE and
+    WRITE_SIZE scaled by a plain copy), or None once the kernel sources have changed since
+    those counters were taken."""
+    try:
+        with open(COUNTERS) as fh:
+            text = fh.read()
+    except OSError:
+        return None
+    m_b = re.search(r"^traffic-bytes-per-call: (\d+)$", text, re.M)
+    m_h = re.search(r"^source-sha256: ([0-9a-f]{64})$", text, re.M)
+    if not (m_b and m_h) or m_h.group(1) != kernel_source_hash():
+        return None
+    return int(m_b.group(1))
 
 
 def copy_calibration(torch, dev, nbytes=1 << 29, reps=3):
@@ -189,10 +226,10 @@ def main():
         "committed_tokens_per_s": round(float((al_h + 1).sum()) / (ms_per_step * 1e-3), 1),
         "mean_accept_len": float(al_h.mean()),
         "copy_calibration": copy_cal,
-        "roofline": {"bound": "hbm", "kernel": "block_attn_bf16_kernel (the whole sd_block_attn call)",
+        "roofline": {"bound": "hbm", "kernel": "block_attn_bf16_kernel + block_attn_merge_kernel (one sd_block_attn call)",
                      "achieved": round(attn_gbps, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
-                     "traffic": None},
+                     "traffic": measured_traffic()},
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(work, T, args.cpu_seconds)
