@@ -20,6 +20,8 @@
 //     skipped when no row's running maximum moved.
 #pragma once
 
+#include <type_traits>
+
 #include "attn.hpp"
 
 namespace sdb {
@@ -64,9 +66,9 @@ __device__ __forceinline__ void wait_lds_tr(s16x4 (&v)[NDT][2]) {
   }
 }
 
-template <int D>
+template <int D, int KT_, int NS_>
 struct Bf16Tile {
-  static constexpr int KT = 64;                 // keys per tile
+  static constexpr int KT = KT_;                // keys per tile
   static constexpr int ROWB = D * 2;            // bytes per key row
   static constexpr int CPR = ROWB / 16;         // 16-byte chunks per row
   static constexpr int TILEB = KT * ROWB;       // bytes of one K (or V) tile
@@ -74,7 +76,7 @@ struct Bf16Tile {
   static constexpr int LPI = TILEB / 1024;      // load instructions per K (or V) tile
   static constexpr int NW = 8;                  // wavefronts per workgroup
   static constexpr int LPW = 2 * LPI / NW;      // load instructions per wavefront per tile
-  static constexpr int NS = 4;                  // ring stages
+  static constexpr int NS = NS_;                // ring stages
   static constexpr int STAGEB = 2 * TILEB;      // K tile then V tile
   static_assert((2 * LPI) % NW == 0 && LPI % LPW == 0, "K and V loads split evenly over wavefronts");
   __device__ static int swz_k(int r) { return r % CPR; }
@@ -84,9 +86,9 @@ struct Bf16Tile {
 // Per-lane source offsets of this wavefront's share of one tile's loads (row*ROWB +
 // swizzled chunk*16, relative to the tile's first key row).  Wavefronts 0-3 fetch K,
 // 4-7 fetch V.
-template <int D>
+template <int D, int KT, int NS>
 struct TileLoads {
-  using T = Bf16Tile<D>;
+  using T = Bf16Tile<D, KT, NS>;
   int row[T::LPW];
   unsigned src[T::LPW];
   bool isv;
@@ -124,8 +126,8 @@ struct TileLoads {
 // One 32-key step (keys KK*32 .. KK*32+31 of the tile) of O^T += V^T P^T.  P comes from
 // the score registers (keys KK*32 + h*16 + kgrp*4 + r, h = 0,1); the matching V^T operand
 // from two transposed LDS reads per head-dim tile.
-template <int KK, int NDT>
-__device__ __forceinline__ void pv_step(const f32x4 (&p)[4], unsigned stage, const unsigned (&voff)[NDT],
+template <int KK, int NDT, int NSB>
+__device__ __forceinline__ void pv_step(const f32x4 (&p)[NSB], unsigned stage, const unsigned (&voff)[NDT],
                                         f32x4 (&oacc)[NDT]) {
   constexpr int ROWB = NDT * 32;  // bytes per key row (D * 2)
   const u32x4 praw{cvt_pk_bf16(p[2 * KK][0], p[2 * KK][1]), cvt_pk_bf16(p[2 * KK][2], p[2 * KK][3]),
@@ -147,10 +149,12 @@ __device__ __forceinline__ void pv_step(const f32x4 (&p)[4], unsigned stage, con
   }
 }
 
-template <int D, int MT>
+template <int D, int MT, int KT_, int NS_>
 __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
-  using T = Bf16Tile<D>;
-  constexpr int KT = T::KT, NS = T::NS, NDT = D / 16, NST = D / 32;
+  using T = Bf16Tile<D, KT_, NS_>;
+  constexpr int KT = T::KT, NS = T::NS, NDT = D / 16, NST = D / 32, NSB = KT / 16;
+  static_assert(NS >= 2 && NS <= 5, "ring depth");
+  static_assert(KT == 64 || KT == 128, "key tile of 64 or 128 keys");
   constexpr int EB = 2;
   __shared__ __attribute__((aligned(1024))) char ring_raw[NS * T::STAGEB];
   char SDB_LDS *ring = (char SDB_LDS *)(SDB_LDS void *)ring_raw;
@@ -222,7 +226,7 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   for (int dt = 0; dt < NDT; ++dt)
     voff[dt] = T::TILEB + vrow * T::ROWB + (((2 * dt + ((l16 & 3) >> 1)) ^ T::swz_v(vrow)) << 4) + ((l16 & 1) << 3);
 
-  TileLoads<D> ld;
+  TileLoads<D, KT, NS> ld;
   ld.init(wave, lane);
 
   // ---- pipeline prologue: tiles 0 .. NS-2 in flight ----
@@ -237,27 +241,27 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   for (int t = 0; t < ntiles; ++t) {
     const int kt = k0 + t * KT;
     const int ahead = min(ntiles - 1 - t, NS - 2);  // tiles issued after tile t
-    if (ahead >= 2) wait_vmcnt<2 * T::LPW>();
-    else if (ahead == 1) wait_vmcnt<T::LPW>();
+    if (NS > 4 && ahead >= 3) wait_vmcnt<3 * T::LPW>();
+    else if (NS > 3 && ahead >= 2) wait_vmcnt<2 * T::LPW>();
+    else if (NS > 2 && ahead >= 1) wait_vmcnt<T::LPW>();
     else wait_vmcnt<0>();
     __syncthreads();  // tile t landed for every wavefront; stage (t-1) % NS is free again
     if (t + NS - 1 < ntiles)
       ld.issue(ring + ((t + NS - 1) % NS) * T::STAGEB, kbase, vbase, kt + (NS - 1) * KT, k1 - 1, wave);
     const unsigned stage = (unsigned)(uintptr_t)(ring + (t % NS) * T::STAGEB);
     const bool full = kt + KT <= vis_all;  // uniform: no key of this tile is masked for any row
-
 #pragma unroll
     for (int j = 0; j < MT; ++j) {
       if (!act[j]) continue;  // uniform per wavefront
       // S^T = K Q^T: sacc[sb][r] is key kt + sb*16 + kgrp*4 + r of row l16 (unscaled)
-      f32x4 sacc[4];
+      f32x4 sacc[NSB];
 #pragma unroll
-      for (int sb = 0; sb < 4; ++sb) sacc[sb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int sb = 0; sb < NSB; ++sb) sacc[sb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int st = 0; st < NST; ++st) {
         const char SDB_LDS *kp = (const char SDB_LDS *)(uintptr_t)(stage + koff[st]);
 #pragma unroll
-        for (int sb = 0; sb < 4; ++sb) {
+        for (int sb = 0; sb < NSB; ++sb) {
           const bf16x8 av = *(const bf16x8 SDB_LDS *)(kp + sb * 16 * T::ROWB);
           sacc[sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qop[j][st], sacc[sb], 0, 0, 0);
         }
@@ -266,22 +270,22 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
       if (!full) {
         const int lim = a.causal ? min(k1, ctx + row_i[j] + 1) : k1;
 #pragma unroll
-        for (int sb = 0; sb < 4; ++sb)
+        for (int sb = 0; sb < NSB; ++sb)
 #pragma unroll
           for (int r = 0; r < 4; ++r)
             if (kt + sb * 16 + kgrp * 4 + r >= lim) sacc[sb][r] = -INFINITY;
       }
-      float tmax = fmaxf(fmaxf(fmaxf(sacc[0][0], sacc[0][1]), fmaxf(sacc[0][2], sacc[0][3])),
-                         fmaxf(fmaxf(sacc[1][0], sacc[1][1]), fmaxf(sacc[1][2], sacc[1][3])));
-      tmax = fmaxf(tmax, fmaxf(fmaxf(fmaxf(sacc[2][0], sacc[2][1]), fmaxf(sacc[2][2], sacc[2][3])),
-                               fmaxf(fmaxf(sacc[3][0], sacc[3][1]), fmaxf(sacc[3][2], sacc[3][3]))));
+      float tmax = -INFINITY;
+#pragma unroll
+      for (int sb = 0; sb < NSB; ++sb)
+        tmax = fmaxf(tmax, fmaxf(fmaxf(sacc[sb][0], sacc[sb][1]), fmaxf(sacc[sb][2], sacc[sb][3])));
       tmax = fmaxf(tmax, shfl_xor_f(tmax, 16));
       tmax = fmaxf(tmax, shfl_xor_f(tmax, 32));
       const float mnew = fmaxf(m_run[j], tmax * sl2);
       const float muse = (mnew == -INFINITY) ? 0.f : mnew;
       float psum = 0.f;
 #pragma unroll
-      for (int sb = 0; sb < 4; ++sb)
+      for (int sb = 0; sb < NSB; ++sb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           sacc[sb][r] = fast_exp2(fmaf(sacc[sb][r], sl2, -muse));
@@ -296,9 +300,13 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
       m_run[j] = mnew;
       l_run[j] += psum;
 
-      // O^T += V^T P^T over the tile's 64 keys in two 32-key steps
-      pv_step<0, NDT>(sacc, stage, voff, oacc[j]);
-      pv_step<1, NDT>(sacc, stage, voff, oacc[j]);
+      // O^T += V^T P^T over the tile's keys in 32-key steps
+      pv_step<0, NDT, NSB>(sacc, stage, voff, oacc[j]);
+      pv_step<1, NDT, NSB>(sacc, stage, voff, oacc[j]);
+      if constexpr (NSB > 4) {
+        pv_step<2, NDT, NSB>(sacc, stage, voff, oacc[j]);
+        pv_step<3, NDT, NSB>(sacc, stage, voff, oacc[j]);
+      }
     }
   }
 

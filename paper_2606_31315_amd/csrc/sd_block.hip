@@ -44,6 +44,13 @@ int check_launch(const char *what) {
   return ok();
 }
 
+// bf16 key tile and LDS ring depth: KT keys of K and of V per stage, NS stages
+#ifndef SDB_BF16_KT
+#define SDB_BF16_KT 64
+#define SDB_BF16_NS 4
+#endif
+constexpr int kBf16KT = SDB_BF16_KT, kBf16NS = SDB_BF16_NS;
+
 // ---------------------------------------------------------------------------
 // attention planning
 // ---------------------------------------------------------------------------
@@ -74,7 +81,7 @@ int attn_plan(const sd_attn_shape *sh, AttnPlan *p) {
   if (!(sh->scale >= 0.f) || isinf(sh->scale)) return fail(SD_ERR_INVALID_ARG, "scale must be finite and >= 0");
 
   p->G = G;
-  p->KT = (sh->dtype == SD_BF16) ? 64 : 32;
+  p->KT = (sh->dtype == SD_BF16) ? kBf16KT : 32;
   const long long max_L = (long long)sh->max_ctx + sh->max_block;
   const long long pairs = (long long)S * Hkv;
   // Split the keys so that, at the maximum length, the grid is one wave: one workgroup per
@@ -121,8 +128,10 @@ void launch_attn(const sdb::AttnArgs &a, int grid, hipStream_t st) {
 template <bool BF16, int D>
 void launch_attn_all(const sdb::AttnArgs &a, int grid, int MT, hipStream_t st) {
   if constexpr (BF16) {
-    if (MT == 1) hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 1>), dim3(grid), dim3(512), 0, st, a);
-    else hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 2>), dim3(grid), dim3(512), 0, st, a);
+    if (MT == 1)
+      hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 1, kBf16KT, kBf16NS>), dim3(grid), dim3(512), 0, st, a);
+    else
+      hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 2, kBf16KT, kBf16NS>), dim3(grid), dim3(512), 0, st, a);
   } else {
     if (MT == 1) launch_attn<BF16, D, 1>(a, grid, st);
     else if (MT == 2) launch_attn<BF16, D, 2>(a, grid, st);
