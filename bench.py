@@ -39,6 +39,9 @@ def parse():
     ap.add_argument("--copies", type=int, default=0, help="input copies to rotate (0: enough for >= 1 GB)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="bound on the oracle timing")
+    ap.add_argument("--verify-layers", type=int, default=36,
+                    help="layers of the whole verify step timed after the main measurement (0: skip)")
+    ap.add_argument("--verify-steps", type=int, default=20)
     return ap.parse_args()
 
 
@@ -122,6 +125,60 @@ def copy_calibration(torch, dev, nbytes=1 << 29, reps=3):
     del src, dst
     return {"bytes_read": nbytes, "bytes_written": nbytes, "us": round(ms * 1e3, 2),
             "gbps_read_plus_write": round(2 * nbytes / (ms * 1e-3) / 1e9, 1)}
+
+
+def verify_step_run(torch, sd, work, T, layers, steps, warmup=3):
+    """The whole verify step through sd_verify_step: for every layer the block's keys and values
+    are appended to that layer's cache and the block attends over it; then acceptance and the
+    commit.  Consecutive decode steps: ctx starts at the workload's 4096 and advances by
+    accept_len + 1 each step.  Caches and block inputs are random bf16 on the device."""
+    a, acc = work.attn, work.accept[T]
+    dev = torch.device("cuda:0")
+    S, Hq, Hkv, D = a.S, a.Hq, a.Hkv, a.D
+    mb = int(a.max_block)
+    Lmax = int(a.max_ctx) + mb * (steps + warmup + 1)
+    g = torch.Generator(device=dev).manual_seed(7)
+    tq = a.total_q
+    L = []
+    for _ in range(layers):
+        L.append(dict(q=torch.randn(tq, Hq, D, device=dev, generator=g).to(torch.bfloat16),
+                      k_new=torch.randn(tq, Hkv, D, device=dev, generator=g).to(torch.bfloat16),
+                      v_new=torch.randn(tq, Hkv, D, device=dev, generator=g).to(torch.bfloat16),
+                      k_cache=torch.randn(S, Hkv, Lmax, D, device=dev, generator=g).to(torch.bfloat16),
+                      v_cache=torch.randn(S, Hkv, Lmax, D, device=dev, generator=g).to(torch.bfloat16),
+                      out=torch.empty(tq, Hq, D, device=dev, dtype=torch.bfloat16)))
+    ctx = torch.from_numpy(a.ctx_lens).to(dev)
+    bl, off = torch.from_numpy(a.block_lens).to(dev), torch.from_numpy(a.q_offsets).to(dev)
+    t_ = acc.target.to(dev)
+    d_ = acc.draft.to(dev) if acc.draft is not None else None
+    tok = torch.from_numpy(acc.draft_tokens).to(dev)
+    u = torch.from_numpy(acc.uniforms).to(dev)
+    al = torch.empty(S, dtype=torch.int32, device=dev)
+    nt = torch.empty(S, dtype=torch.int32, device=dev)
+    max_ctx = int(a.max_ctx)
+
+    def one(max_ctx):
+        sd.verify_step(L, ctx, bl, off, a.mask_mode, t_, d_, tok, u, T, max_ctx=max_ctx, max_block=mb,
+                       accept_len=al, next_token=nt)
+
+    for _ in range(warmup):
+        one(max_ctx)
+        max_ctx += mb
+    torch.cuda.synchronize()
+    ctx0 = int(ctx.max().item())
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(steps):
+        one(max_ctx)
+        max_ctx += mb
+    t1.record()
+    torch.cuda.synchronize()
+    us = t0.elapsed_time(t1) / steps * 1e3
+    return {"layers": layers, "steps": steps, "us_per_step": round(us, 1),
+            "verified_draft_tokens_per_s": round(work.verified_draft_tokens() / (us * 1e-6), 1),
+            "ctx_start": ctx0, "ctx_end": int(ctx.max().item()),
+            "what": "sd_verify_step: per layer sd_kv_append + sd_block_attn, then sd_accept (T=%g) and sd_commit; "
+                    "consecutive decode steps" % T}
 
 
 def main():
@@ -231,6 +288,8 @@ def main():
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
                      "traffic": measured_traffic()},
     }
+    if args.verify_layers > 0:
+        res["verify_step"] = verify_step_run(torch, sd, work, T, args.verify_layers, args.verify_steps)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(work, T, args.cpu_seconds)
     print(json.dumps(res), flush=True)

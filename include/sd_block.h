@@ -167,6 +167,66 @@ int sd_accept(const sd_accept_shape *shape, const void *target_logits, const voi
               const int32_t *q_offsets, float temperature, int32_t *accept_len, int32_t *next_token,
               void *workspace, size_t workspace_bytes, void *stream);
 
+/* ==========================================================================
+ * The step around verification.  One speculative step writes the block's keys and
+ * values, verifies the block in every layer, accepts the longest consistent prefix
+ * and commits it (Sec. 2.1; Fig. 1 caption).  The block size of a sequence is fixed
+ * for the whole decoding (Sec. 2.4), so block_lens and q_offsets do not change from
+ * step to step; only ctx_lens advances, on the device, with no host round trip.
+ * ========================================================================== */
+
+/*
+ * k_cache[s, h, ctx_s + i, :] = k_new[q_offsets[s] + i, h, :] and the same for v, for every
+ * block position i < B_s and kv head h.
+ *
+ *   k_new, v_new    [total_q, Hkv, D]   dtype (shape->dtype); the block's new keys and values
+ *   k_cache,v_cache [S, Hkv, Lmax, D]   dtype, written in place
+ *   ctx_lens        [S] int32           committed length before this step
+ *   q_offsets       [S + 1] int32       exclusive prefix sum of the block lengths
+ * Only num_seqs, num_q_heads, num_kv_heads, head_dim, max_kv_len, total_q and dtype of the
+ * shape are used.  A row that would land at or past Lmax (ctx_s + i >= Lmax) is skipped, not
+ * written.  Buffers 16-byte aligned.  Errors: SD_ERR_INVALID_ARG, SD_ERR_UNSUPPORTED, SD_ERR_HIP.
+ */
+int sd_kv_append(const sd_attn_shape *shape, const void *k_new, const void *v_new, void *k_cache, void *v_cache,
+                 const int32_t *ctx_lens, const int32_t *q_offsets, void *stream);
+
+/*
+ * ctx_lens[s] += accept_len[s] + 1: the block's anchor and its accepted drafts are now part of
+ * the cached context.  Rows of rejected drafts remain past the new length and are overwritten by
+ * the next sd_kv_append, so no rollback work is needed.  Both arrays are device int32 [S].
+ * Errors: SD_ERR_INVALID_ARG, SD_ERR_HIP.
+ */
+int sd_commit(int32_t num_seqs, const int32_t *accept_len, int32_t *ctx_lens, void *stream);
+
+/* Device buffers of one layer for sd_verify_step (a host array of these is passed). */
+typedef struct sd_layer_buffers {
+  const void *q;     /* [total_q, Hq, D]      queries of the block rows */
+  const void *k_new; /* [total_q, Hkv, D]     the block's new keys */
+  const void *v_new; /* [total_q, Hkv, D]     the block's new values */
+  void *k_cache;     /* [S, Hkv, Lmax, D]     this layer's caches */
+  void *v_cache;
+  void *out;         /* [total_q, Hq, D]      attention output */
+} sd_layer_buffers;
+
+/* Workspace bytes sd_verify_step needs: the larger of the two operations' (host-only). */
+int sd_verify_step_workspace_size(const sd_attn_shape *attn_shape, const sd_accept_shape *accept_shape,
+                                  float temperature, size_t *bytes);
+
+/*
+ * One verify step, enqueued on `stream` with no host synchronisation: for every layer l,
+ * sd_kv_append then sd_block_attn (layers[l]); then sd_accept on the given logits; then
+ * sd_commit (ctx_lens advances by accept_len + 1).  The logits are the caller's (the model's
+ * head after the last layer); every other argument has the meaning given above.  The two
+ * shapes must agree on num_seqs, total_q and max_block; attn_shape->max_ctx bounds ctx_lens
+ * before the step.  All pointers are checked before any work is enqueued.
+ * Errors: those of the four calls, SD_ERR_WORKSPACE.
+ */
+int sd_verify_step(const sd_attn_shape *attn_shape, int32_t num_layers, const sd_layer_buffers *layers,
+                   int32_t *ctx_lens, const int32_t *block_lens, const int32_t *q_offsets, int32_t mask_mode,
+                   const sd_accept_shape *accept_shape, const void *target_logits, const void *draft_logits,
+                   const int32_t *draft_tokens, const float *uniforms, float temperature, int32_t *accept_len,
+                   int32_t *next_token, void *workspace, size_t workspace_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

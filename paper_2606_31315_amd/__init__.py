@@ -7,11 +7,16 @@ include/sd_block.h:
               KV cache (causal-in-block or bidirectional-in-block mask);
   accept      vocabulary-wide speculative acceptance (greedy at T=0, lossless
               rejection sampling at T>0) returning accept_len and the next token.
+
+and the step around them: kv_append (the block's keys and values into the cache),
+commit (ctx += accept_len + 1) and verify_step (append + attention per layer,
+acceptance, commit, in one native call).
 """
 from ._lib import (SD_BF16, SD_F32, SD_MASK_BIDIR_IN_BLOCK, SD_MASK_CAUSAL_IN_BLOCK, SdError, Workspace,
-                   accept, accept_shape, accept_workspace_size, attn_shape, attn_workspace_size, block_attn, lib,
-                   version)
+                   accept, accept_shape, accept_workspace_size, attn_shape, attn_workspace_size, block_attn, commit,
+                   kv_append, lib, verify_step, version)
 
-__all__ = ["block_attn", "accept", "attn_shape", "accept_shape", "attn_workspace_size", "accept_workspace_size",
+__all__ = ["block_attn", "accept", "kv_append", "commit", "verify_step", "attn_shape", "accept_shape",
+           "attn_workspace_size", "accept_workspace_size",
            "Workspace", "SdError", "lib", "version", "SD_BF16", "SD_F32", "SD_MASK_CAUSAL_IN_BLOCK",
            "SD_MASK_BIDIR_IN_BLOCK"]

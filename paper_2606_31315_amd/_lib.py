@@ -19,7 +19,8 @@ SD_F32, SD_BF16 = 0, 1
 SD_MASK_CAUSAL_IN_BLOCK, SD_MASK_BIDIR_IN_BLOCK = 0, 1
 
 EXPORTS = ["sd_last_error", "sd_version", "sd_block_attn_workspace_size", "sd_block_attn",
-           "sd_accept_workspace_size", "sd_accept"]
+           "sd_accept_workspace_size", "sd_accept", "sd_kv_append", "sd_commit", "sd_verify_step_workspace_size",
+           "sd_verify_step"]
 
 
 class SdAttnShape(ctypes.Structure):
@@ -32,6 +33,11 @@ class SdAttnShape(ctypes.Structure):
 class SdAcceptShape(ctypes.Structure):
     _fields_ = [("num_seqs", ctypes.c_int32), ("vocab", ctypes.c_int32), ("total_q", ctypes.c_int32),
                 ("max_block", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class SdLayerBuffers(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("k_new", ctypes.c_void_p), ("v_new", ctypes.c_void_p),
+                ("k_cache", ctypes.c_void_p), ("v_cache", ctypes.c_void_p), ("out", ctypes.c_void_p)]
 
 
 class SdError(RuntimeError):
@@ -64,6 +70,16 @@ def lib() -> ctypes.CDLL:
         L.sd_accept_workspace_size.argtypes = [ctypes.POINTER(SdAcceptShape), ctypes.c_float, ctypes.POINTER(Z)]
         L.sd_accept.restype = ctypes.c_int
         L.sd_accept.argtypes = [ctypes.POINTER(SdAcceptShape), P, P, P, P, P, P, ctypes.c_float, P, P, P, Z, P]
+        L.sd_kv_append.restype = ctypes.c_int
+        L.sd_kv_append.argtypes = [ctypes.POINTER(SdAttnShape), P, P, P, P, P, P, P]
+        L.sd_commit.restype = ctypes.c_int
+        L.sd_commit.argtypes = [I, P, P, P]
+        L.sd_verify_step_workspace_size.restype = ctypes.c_int
+        L.sd_verify_step_workspace_size.argtypes = [ctypes.POINTER(SdAttnShape), ctypes.POINTER(SdAcceptShape),
+                                                    ctypes.c_float, ctypes.POINTER(Z)]
+        L.sd_verify_step.restype = ctypes.c_int
+        L.sd_verify_step.argtypes = [ctypes.POINTER(SdAttnShape), I, ctypes.POINTER(SdLayerBuffers), P, P, P, I,
+                                     ctypes.POINTER(SdAcceptShape), P, P, P, P, ctypes.c_float, P, P, P, Z, P]
         _lib = L
     return _lib
 
@@ -200,6 +216,75 @@ def accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor], dr
                            _ptr(uniforms if temperature > 0 else None), _ptr(block_lens), _ptr(q_offsets),
                            float(temperature), _ptr(accept_len), _ptr(next_token), _ptr(workspace),
                            workspace.numel() * workspace.element_size(), _stream(stream)))
+    return accept_len, next_token
+
+
+def kv_append(k_new: torch.Tensor, v_new: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+              ctx_lens: torch.Tensor, q_offsets: torch.Tensor, stream=None) -> None:
+    """Write the block's keys and values into the caches at rows [ctx_s, ctx_s + B_s) (sd_kv_append).
+    k_new, v_new [total_q, Hkv, D]; caches [S, Hkv, Lmax, D]; ctx_lens [S], q_offsets [S+1] int32."""
+    dev = k_new.device
+    _need(k_new, "k_new", device=dev)
+    _need(v_new, "v_new", k_new.dtype, dev)
+    _need(k_cache, "k_cache", k_new.dtype, dev)
+    _need(v_cache, "v_cache", k_new.dtype, dev)
+    _need(ctx_lens, "ctx_lens", torch.int32, dev)
+    _need(q_offsets, "q_offsets", torch.int32, dev)
+    S, Hkv, Lmax, D = k_cache.shape
+    shape = SdAttnShape(S, Hkv, Hkv, D, Lmax, k_new.shape[0], 0, 1, _dtype_code(k_new), 0.0)
+    _check(lib().sd_kv_append(ctypes.byref(shape), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache),
+                              _ptr(ctx_lens), _ptr(q_offsets), _stream(stream)))
+
+
+def commit(accept_len: torch.Tensor, ctx_lens: torch.Tensor, stream=None) -> None:
+    """ctx_lens += accept_len + 1 on the device (sd_commit)."""
+    _need(accept_len, "accept_len", torch.int32)
+    _need(ctx_lens, "ctx_lens", torch.int32, accept_len.device)
+    _check(lib().sd_commit(int(ctx_lens.shape[0]), _ptr(accept_len), _ptr(ctx_lens), _stream(stream)))
+
+
+def verify_step(layers, ctx_lens: torch.Tensor, block_lens: torch.Tensor, q_offsets: torch.Tensor, mask_mode: int,
+                target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor], draft_tokens: torch.Tensor,
+                uniforms: Optional[torch.Tensor], temperature: float, *, max_ctx: int, max_block: int,
+                scale: float = 0.0, accept_len: Optional[torch.Tensor] = None,
+                next_token: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """One verify step (sd_verify_step): per layer append + block attention, then acceptance,
+    then commit.  `layers` is a sequence of dicts with q, k_new, v_new, k_cache, v_cache, out."""
+    if len(layers) < 1:
+        raise ValueError("at least one layer")
+    l0 = layers[0]
+    dev = l0["q"].device
+    for i, L_ in enumerate(layers):
+        _need(L_["q"], f"layers[{i}].q", l0["q"].dtype, dev)
+        for key in ("k_new", "v_new", "k_cache", "v_cache", "out"):
+            _need(L_[key], f"layers[{i}].{key}", l0["q"].dtype, dev)
+    for name, t in (("ctx_lens", ctx_lens), ("block_lens", block_lens), ("q_offsets", q_offsets),
+                    ("draft_tokens", draft_tokens)):
+        _need(t, name, torch.int32, dev)
+    _need(target_logits, "target_logits", device=dev)
+    S = block_lens.shape[0]
+    ash = attn_shape(l0["q"], l0["k_cache"], max_ctx, max_block, scale)
+    csh = accept_shape(target_logits, S, max_block)
+    n = ctypes.c_size_t(0)
+    _check(lib().sd_verify_step_workspace_size(ctypes.byref(ash), ctypes.byref(csh), float(temperature),
+                                               ctypes.byref(n)))
+    if workspace is None:
+        workspace = _default_ws.get(n.value, dev)
+    if accept_len is None:
+        accept_len = torch.empty(S, dtype=torch.int32, device=dev)
+    if next_token is None:
+        next_token = torch.empty(S, dtype=torch.int32, device=dev)
+    arr = (SdLayerBuffers * len(layers))(*[SdLayerBuffers(L_["q"].data_ptr(), L_["k_new"].data_ptr(),
+                                                          L_["v_new"].data_ptr(), L_["k_cache"].data_ptr(),
+                                                          L_["v_cache"].data_ptr(), L_["out"].data_ptr())
+                                           for L_ in layers])
+    _check(lib().sd_verify_step(ctypes.byref(ash), len(layers), arr, _ptr(ctx_lens), _ptr(block_lens), _ptr(q_offsets),
+                                int(mask_mode), ctypes.byref(csh), _ptr(target_logits),
+                                _ptr(draft_logits if temperature > 0 else None), _ptr(draft_tokens),
+                                _ptr(uniforms if temperature > 0 else None), float(temperature), _ptr(accept_len),
+                                _ptr(next_token), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                _stream(stream)))
     return accept_len, next_token
 
 

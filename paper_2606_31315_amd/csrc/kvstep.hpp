@@ -1,0 +1,63 @@
+// kvstep.hpp -- the two small steps on either side of verification.
+//
+//   kv_append_kernel  before the verify pass of a layer: the block's new keys and values go to
+//                     cache rows [ctx_s, ctx_s + B_s) of every kv head of sequence s, where the
+//                     block attention reads them (the block is verified in parallel, Sec. 2.1).
+//   commit_kernel     after acceptance: the anchor and the accepted drafts are now cached,
+//                     ctx_s += accept_len_s + 1.  Rows of rejected drafts stay in the cache past
+//                     the new length and are overwritten by the next step's append (the accepted
+//                     prefix is the longest consistent one, Fig. 1 caption).
+//
+// Both are copies or integer updates; they move B_s * Hkv * D elements per sequence and layer.
+#pragma once
+
+#include "common.hpp"
+
+namespace sdb {
+
+struct AppendArgs {
+  const void *k_new;   // [total_q, Hkv, D]
+  const void *v_new;   // [total_q, Hkv, D]
+  void *k_cache;       // [S, Hkv, Lmax, D]
+  void *v_cache;
+  const int *ctx_lens;
+  const int *q_offsets;
+  int S, Hkv, Lmax, total_q;
+  int row_vecs;        // 16-byte vectors per (token, head) row: D * element bytes / 16
+};
+
+// Largest s with off[s] <= r (r < off[S]): the sequence that owns packed row r.
+__device__ __forceinline__ int row_owner(const int *off, int S, int r) {
+  int lo = 0, hi = S - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (ld_uniform(off, mid) <= r) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// grid = (total_q, 2): block (r, kv) copies token row r of K (kv = 0) or V (kv = 1) for every
+// kv head; threads stride over the Hkv * row_vecs 16-byte vectors.  A destination row at or
+// past Lmax (a ctx_len beyond the cache) is skipped rather than written out of bounds.
+__global__ __launch_bounds__(256) void kv_append_kernel(AppendArgs a) {
+  const int r = blockIdx.x;
+  const int kv = blockIdx.y;
+  const int s = row_owner(a.q_offsets, a.S, r);
+  const int pos = ld_uniform(a.ctx_lens, s) + (r - ld_uniform(a.q_offsets, s));
+  if (pos < 0 || pos >= a.Lmax) return;
+  const u32x4 *src = reinterpret_cast<const u32x4 *>(kv ? a.v_new : a.k_new) + (size_t)r * a.Hkv * a.row_vecs;
+  u32x4 *dst = reinterpret_cast<u32x4 *>(kv ? a.v_cache : a.k_cache);
+  const int n = a.Hkv * a.row_vecs;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    const int h = i / a.row_vecs, c = i - h * a.row_vecs;
+    dst[(((size_t)s * a.Hkv + h) * a.Lmax + pos) * a.row_vecs + c] = src[i];
+  }
+}
+
+// ctx_lens[s] += accept_len[s] + 1 for every sequence.
+__global__ __launch_bounds__(256) void commit_kernel(const int *accept_len, int *ctx_lens, int S) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s < S) ctx_lens[s] += accept_len[s] + 1;
+}
+
+}  // namespace sdb

@@ -13,6 +13,7 @@
 #include "accept.hpp"
 #include "attn.hpp"
 #include "attn_bf16.hpp"
+#include "kvstep.hpp"
 #include "sd_block.h"
 
 namespace {
@@ -348,6 +349,105 @@ int sd_accept(const sd_accept_shape *sh, const void *target_logits, const void *
   }
 #undef SDB_STATS
   return check_launch("sd_accept");
+}
+
+// ---------------------------------------------------------------------------
+// the step around verification: append, commit, and the whole verify step
+// ---------------------------------------------------------------------------
+static int check_cache_shape(const sd_attn_shape *sh, const char *what) {
+  if (!sh) return fail(SD_ERR_INVALID_ARG, "%s: shape is NULL", what);
+  if (sh->num_seqs < 0) return fail(SD_ERR_INVALID_ARG, "num_seqs must be >= 0 (got %d)", sh->num_seqs);
+  if (sh->num_q_heads < 1 || sh->num_kv_heads < 1 || sh->num_q_heads % sh->num_kv_heads)
+    return fail(SD_ERR_INVALID_ARG, "head counts must be >= 1 with Hq %% Hkv == 0 (Hq=%d, Hkv=%d)",
+                sh->num_q_heads, sh->num_kv_heads);
+  if (sh->dtype != SD_BF16 && sh->dtype != SD_F32) return fail(SD_ERR_INVALID_ARG, "unknown dtype %d", sh->dtype);
+  if (sh->head_dim != 64 && sh->head_dim != 128)
+    return fail(SD_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", sh->head_dim);
+  if (sh->max_kv_len < 1) return fail(SD_ERR_INVALID_ARG, "max_kv_len must be >= 1 (got %d)", sh->max_kv_len);
+  if (sh->total_q < 0) return fail(SD_ERR_INVALID_ARG, "total_q must be >= 0 (got %d)", sh->total_q);
+  return ok();
+}
+
+int sd_kv_append(const sd_attn_shape *sh, const void *k_new, const void *v_new, void *k_cache, void *v_cache,
+                 const int32_t *ctx_lens, const int32_t *q_offsets, void *stream) {
+  int rc = check_cache_shape(sh, "sd_kv_append");
+  if (rc) return rc;
+  if (sh->num_seqs == 0 || sh->total_q == 0) return ok();
+  if (!k_new || !v_new || !k_cache || !v_cache || !ctx_lens || !q_offsets)
+    return fail(SD_ERR_INVALID_ARG, "sd_kv_append: NULL pointer argument");
+  if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(k_cache) || !aligned16(v_cache))
+    return fail(SD_ERR_INVALID_ARG, "new rows and caches must be 16-byte aligned");
+  sdb::AppendArgs a;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.ctx_lens = ctx_lens;
+  a.q_offsets = q_offsets;
+  a.S = sh->num_seqs;
+  a.Hkv = sh->num_kv_heads;
+  a.Lmax = sh->max_kv_len;
+  a.total_q = sh->total_q;
+  a.row_vecs = sh->head_dim * (sh->dtype == SD_BF16 ? 2 : 4) / 16;
+  hipLaunchKernelGGL(sdb::kv_append_kernel, dim3(sh->total_q, 2), dim3(256), 0, (hipStream_t)stream, a);
+  return check_launch("sd_kv_append");
+}
+
+int sd_commit(int32_t num_seqs, const int32_t *accept_len, int32_t *ctx_lens, void *stream) {
+  if (num_seqs < 0) return fail(SD_ERR_INVALID_ARG, "num_seqs must be >= 0 (got %d)", num_seqs);
+  if (num_seqs == 0) return ok();
+  if (!accept_len || !ctx_lens) return fail(SD_ERR_INVALID_ARG, "sd_commit: NULL pointer argument");
+  hipLaunchKernelGGL(sdb::commit_kernel, dim3((num_seqs + 255) / 256), dim3(256), 0, (hipStream_t)stream,
+                     accept_len, ctx_lens, num_seqs);
+  return check_launch("sd_commit");
+}
+
+int sd_verify_step_workspace_size(const sd_attn_shape *attn_shape, const sd_accept_shape *accept_shape,
+                                  float temperature, size_t *bytes) {
+  if (!bytes) return fail(SD_ERR_INVALID_ARG, "bytes is NULL");
+  size_t wa = 0, wc = 0;
+  int rc = sd_block_attn_workspace_size(attn_shape, &wa);
+  if (rc) return rc;
+  rc = sd_accept_workspace_size(accept_shape, temperature, &wc);
+  if (rc) return rc;
+  *bytes = wa > wc ? wa : wc;
+  return ok();
+}
+
+int sd_verify_step(const sd_attn_shape *ash, int32_t num_layers, const sd_layer_buffers *layers,
+                   int32_t *ctx_lens, const int32_t *block_lens, const int32_t *q_offsets, int32_t mask_mode,
+                   const sd_accept_shape *csh, const void *target_logits, const void *draft_logits,
+                   const int32_t *draft_tokens, const float *uniforms, float temperature, int32_t *accept_len,
+                   int32_t *next_token, void *workspace, size_t workspace_bytes, void *stream) {
+  if (num_layers < 1) return fail(SD_ERR_INVALID_ARG, "num_layers must be >= 1 (got %d)", num_layers);
+  if (!layers) return fail(SD_ERR_INVALID_ARG, "sd_verify_step: layers is NULL");
+  if (!ash || !csh) return fail(SD_ERR_INVALID_ARG, "sd_verify_step: shape is NULL");
+  if (ash->num_seqs != csh->num_seqs || ash->total_q != csh->total_q || ash->max_block != csh->max_block)
+    return fail(SD_ERR_INVALID_ARG, "attention and acceptance shapes disagree on num_seqs, total_q or max_block");
+  for (int l = 0; l < num_layers; ++l) {  // every pointer is checked before any work is enqueued
+    const sd_layer_buffers &L = layers[l];
+    if (!L.q || !L.k_new || !L.v_new || !L.k_cache || !L.v_cache || !L.out)
+      return fail(SD_ERR_INVALID_ARG, "sd_verify_step: NULL pointer in layer %d", l);
+    if (!aligned16(L.q) || !aligned16(L.k_new) || !aligned16(L.v_new) || !aligned16(L.k_cache) ||
+        !aligned16(L.v_cache) || !aligned16(L.out))
+      return fail(SD_ERR_INVALID_ARG, "sd_verify_step: layer %d buffers must be 16-byte aligned", l);
+  }
+  size_t need = 0;
+  int rc = sd_verify_step_workspace_size(ash, csh, temperature, &need);
+  if (rc) return rc;
+  if (workspace_bytes < need) return fail(SD_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
+  for (int l = 0; l < num_layers; ++l) {
+    const sd_layer_buffers &L = layers[l];
+    rc = sd_kv_append(ash, L.k_new, L.v_new, L.k_cache, L.v_cache, ctx_lens, q_offsets, stream);
+    if (rc) return rc;
+    rc = sd_block_attn(ash, L.q, L.k_cache, L.v_cache, ctx_lens, block_lens, q_offsets, mask_mode, L.out, workspace,
+                       workspace_bytes, stream);
+    if (rc) return rc;
+  }
+  rc = sd_accept(csh, target_logits, draft_logits, draft_tokens, uniforms, block_lens, q_offsets, temperature,
+                 accept_len, next_token, workspace, workspace_bytes, stream);
+  if (rc) return rc;
+  return sd_commit(csh->num_seqs, accept_len, ctx_lens, stream);
 }
 
 }  // extern "C"

@@ -332,3 +332,28 @@ def c5_lens(seed=1005, S=32):
     ctx = rs["ctx"].integers(8192, 32768, endpoint=True, size=S).astype(np.int32)
     B = rs["B"].integers(4, 32, endpoint=True, size=S).astype(np.int32)
     return ctx, B
+
+
+# --------------------------------------------------------------------------- #
+# inputs of the step around verification (append, verify in every layer, commit)
+# --------------------------------------------------------------------------- #
+
+def step_caches(rs: dict, *, S, Hkv, D, Lmax, ctx_lens, dtype, tail_fill=float("nan")):
+    """One layer's caches [S, Hkv, Lmax, D]: committed rows [0, ctx_s) ~ N(0,1), the rest
+    ``tail_fill`` (NaN), so a read of an unwritten row poisons the output."""
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    k = torch.full((S, Hkv, Lmax, D), tail_fill, dtype=tdt)
+    v = torch.full((S, Hkv, Lmax, D), tail_fill, dtype=tdt)
+    for s in range(S):
+        n = int(ctx_lens[s])
+        k[s, :, :n] = torch.from_numpy(rs["K"].standard_normal((Hkv, n, D), dtype=np.float32)).to(tdt)
+        v[s, :, :n] = torch.from_numpy(rs["V"].standard_normal((Hkv, n, D), dtype=np.float32)).to(tdt)
+    return k, v
+
+
+def step_block_inputs(rs: dict, *, total_q, Hq, Hkv, D, dtype) -> dict:
+    """One layer's block inputs of one step: q [total_q, Hq, D] and the block's new keys and
+    values [total_q, Hkv, D], all ~ N(0,1)."""
+    return dict(q=_to_dtype(rs["q"].standard_normal((total_q, Hq, D), dtype=np.float32), dtype),
+                k_new=_to_dtype(rs["K"].standard_normal((total_q, Hkv, D), dtype=np.float32), dtype),
+                v_new=_to_dtype(rs["V"].standard_normal((total_q, Hkv, D), dtype=np.float32), dtype))

@@ -1,0 +1,120 @@
+"""GPU parity of the step around verification: sd_kv_append and sd_commit bit-exact against
+the oracle, and sd_verify_step over several steps (every layer's attention, acceptance,
+commit and caches) against the oracle run on the same inputs."""
+import numpy as np
+import pytest
+import torch
+
+import gpu_util as G
+import oracle.step as OS
+import paper_2606_31315_amd as sd
+from paper_2606_31315_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def _same(t: torch.Tensor, x: np.ndarray) -> bool:
+    """Bit-exact equality of a device cache with the oracle's (bf16 and fp32 widen exactly to
+    fp32); NaN rows (never written) compare equal whatever their payload."""
+    return np.array_equal(t.detach().float().cpu().numpy(), np.asarray(x, dtype=np.float32), equal_nan=True)
+
+
+@pytest.mark.parametrize("dtype,D", [("bf16", 128), ("f32", 128), ("bf16", 64)])
+def test_kv_append_bit_exact(dtype, D):
+    rs = W._streams(4101)
+    S, Hkv = 5, 8
+    ctx = np.array([100, 0, 4000, 7, 2047], np.int32)
+    B = np.array([16, 1, 24, 0, 9], np.int32)
+    off = W.offsets_from_lens(B)
+    Lmax = 4100
+    k, v = W.step_caches(rs, S=S, Hkv=Hkv, D=D, Lmax=Lmax, ctx_lens=ctx, dtype=dtype)
+    blk = W.step_block_inputs(rs, total_q=int(off[-1]), Hq=Hkv, Hkv=Hkv, D=D, dtype=dtype)
+    dk, dv = k.to(G.dev()), v.to(G.dev())
+    G.log(f"sd_kv_append S={S} Hkv={Hkv} D={D} dtype={dtype} total_q={int(off[-1])}")
+    sd.kv_append(blk["k_new"].to(G.dev()), blk["v_new"].to(G.dev()), dk, dv, torch.from_numpy(ctx).to(G.dev()),
+                 torch.from_numpy(off).to(G.dev()))
+    torch.cuda.synchronize()
+    rk, rv = OS.kv_append(k, v, blk["k_new"], blk["v_new"], ctx, off)
+    assert _same(dk, rk)
+    assert _same(dv, rv)
+
+
+def test_kv_append_skips_rows_past_capacity():
+    rs = W._streams(4102)
+    ctx = np.array([30, 31], np.int32)
+    B = np.array([4, 3], np.int32)
+    off = W.offsets_from_lens(B)
+    k, v = W.step_caches(rs, S=2, Hkv=2, D=64, Lmax=32, ctx_lens=[30, 31], dtype="bf16")
+    blk = W.step_block_inputs(rs, total_q=7, Hq=2, Hkv=2, D=64, dtype="bf16")
+    dk, dv = k.to(G.dev()), v.to(G.dev())
+    G.log("sd_kv_append rows past Lmax")
+    sd.kv_append(blk["k_new"].to(G.dev()), blk["v_new"].to(G.dev()), dk, dv, torch.from_numpy(ctx).to(G.dev()),
+                 torch.from_numpy(off).to(G.dev()))
+    torch.cuda.synchronize()
+    rk, _ = OS.kv_append(k, v, blk["k_new"], blk["v_new"], ctx, off)
+    assert _same(dk, rk)
+
+
+def test_commit_exact():
+    ctx = torch.tensor([0, 5, 4000, 7], dtype=torch.int32, device=G.dev())
+    al = torch.tensor([0, 3, 23, 1], dtype=torch.int32, device=G.dev())
+    G.log("sd_commit")
+    sd.commit(al, ctx)
+    torch.cuda.synchronize()
+    assert ctx.cpu().tolist() == list(OS.commit([0, 5, 4000, 7], [0, 3, 23, 1]))
+
+
+def _run_steps(T, steps, seed, layers=2, dtype="bf16"):
+    rs = W._streams(seed)
+    S, Hq, Hkv, D, V = 4, 32, 8, 128, 32000
+    B = np.array([12, 16, 5, 24], np.int32)
+    off = W.offsets_from_lens(B)
+    ctx = np.array([1500, 3000, 40, 2200], np.int32)
+    Lmax = int(ctx.max() + steps * B.max())
+    caches = [W.step_caches(rs, S=S, Hkv=Hkv, D=D, Lmax=Lmax, ctx_lens=ctx, dtype=dtype) for _ in range(layers)]
+    dev = G.dev()
+    dcaches = [(k.to(dev), v.to(dev)) for k, v in caches]
+    d_ctx = torch.from_numpy(ctx).to(dev)
+    d_bl, d_off = torch.from_numpy(B).to(dev), torch.from_numpy(off).to(dev)
+    max_ctx = int(ctx.max())
+    for step in range(steps):
+        blks = [W.step_block_inputs(rs, total_q=int(off[-1]), Hq=Hq, Hkv=Hkv, D=D, dtype=dtype)
+                for _ in range(layers)]
+        acc = W.make_accept(rs, block_lens=B, V=V, dtype=dtype, temperature=T, target_sigma=3.0, noise_sigma=0.7)
+        dl = []
+        for (dk, dv), b in zip(dcaches, blks):
+            dl.append(dict(q=b["q"].to(dev), k_new=b["k_new"].to(dev), v_new=b["v_new"].to(dev), k_cache=dk,
+                           v_cache=dv, out=torch.empty_like(b["q"], device=dev)))
+        da = G.accept_to_device(acc)
+        G.log(f"sd_verify_step step {step} T={T} layers={layers} max_ctx={max_ctx}")
+        al, nt = sd.verify_step(dl, d_ctx, d_bl, d_off, W.MASK_CAUSAL_IN_BLOCK, da["t"], da["d"], da["tok"], da["u"],
+                                T, max_ctx=max_ctx, max_block=int(B.max()))
+        torch.cuda.synchronize()
+        ol = [dict(q=b["q"], k_new=b["k_new"], v_new=b["v_new"], k_cache=k, v_cache=v)
+              for (k, v), b in zip(caches, blks)]
+        ref = OS.verify_step(ol, ctx, B, off, W.MASK_CAUSAL_IN_BLOCK, acc.target, acc.draft, acc.draft_tokens,
+                             acc.uniforms, T, band=G.BAND)
+        for l in range(layers):
+            err = np.abs(dl[l]["out"].float().cpu().numpy() - ref.outs[l]).max()
+            assert err <= G.ATTN_TOL[dtype], (step, l, err)
+            assert _same(dl[l]["k_cache"], ref.k_caches[l]), (step, l)
+            assert _same(dl[l]["v_cache"], ref.v_caches[l]), (step, l)
+        G.compare_accept(acc, al.cpu().numpy(), nt.cpu().numpy(), ref.accept)
+        # continue from the device's committed state (equal to the oracle's whenever the decisions
+        # are outside the near-tie band)
+        got_ctx = d_ctx.cpu().numpy()
+        assert np.array_equal(got_ctx, OS.commit(ctx, al.cpu().numpy()))
+        ctx = got_ctx
+        caches = [(torch.from_numpy(rk).to(caches[0][0].dtype), torch.from_numpy(rv).to(caches[0][0].dtype))
+                  for rk, rv in zip(ref.k_caches, ref.v_caches)]
+        max_ctx += int(B.max())
+    return ctx
+
+
+def test_verify_step_greedy_three_steps():
+    ctx = _run_steps(0.0, steps=3, seed=4201)
+    assert (ctx > np.array([1500, 3000, 40, 2200])).all()
+
+
+def test_verify_step_sampling_two_steps():
+    _run_steps(1.0, steps=2, seed=4202)
