@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--verify-layers", type=int, default=36,
                     help="layers of the whole verify step timed after the main measurement (0: skip)")
     ap.add_argument("--verify-steps", type=int, default=20)
+    ap.add_argument("--policy-prompts", type=int, default=1,
+                    help="prompts of the block-size policy timed after the main measurement (0: skip)")
     return ap.parse_args()
 
 
@@ -181,6 +183,38 @@ def verify_step_run(torch, sd, work, T, layers, steps, warmup=3):
                     "consecutive decode steps" % T}
 
 
+def policy_run(torch, sd, prompts, reps=20, V=151936, H=2048, radius=2, base_block=16):
+    """The block-size policy (softmax of the last-token logits, then the two-hidden-layer MLP
+    and the argmax over 2k+1 candidates) on random bf16 weights generated on the device.  The
+    weights (622 MB at V=151936, H=2048) exceed the 256 MB Infinity Cache, so every call reads
+    them from HBM."""
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev).manual_seed(11)
+    C = 2 * radius + 1
+    logits = (torch.randn(prompts, V, device=dev, generator=g) * 3).to(torch.bfloat16)
+    w1 = torch.randn(H, V, device=dev, generator=g).to(torch.bfloat16)
+    w2 = (torch.randn(H, H, device=dev, generator=g) / H ** 0.5).to(torch.bfloat16)
+    w3 = (torch.randn(C, H, device=dev, generator=g) / H ** 0.5).to(torch.bfloat16)
+    b1, b2 = torch.randn(H, device=dev, generator=g) * 0.05, torch.randn(H, device=dev, generator=g) * 0.05
+    b3 = torch.randn(C, device=dev, generator=g) * 0.05
+    for _ in range(3):
+        sd.block_size_policy(logits, w1, b1, w2, b2, w3, b3, base_block)
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(reps):
+        sd.block_size_policy(logits, w1, b1, w2, b2, w3, b3, base_block)
+    t1.record()
+    torch.cuda.synchronize()
+    us = t0.elapsed_time(t1) / reps * 1e3
+    nbytes = 2 * (w1.numel() + w2.numel() + w3.numel()) + logits.numel() * 2
+    return {"prompts": prompts, "vocab": V, "hidden": H, "candidates": C, "us_per_call": round(us, 1),
+            "bytes": nbytes, "gbps": round(nbytes / (us * 1e-6) / 1e9, 1),
+            "hbm_frac": round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+            "what": "sd_block_size_policy: softmax of the last-token logits, W1 (H x V), W2 (H x H), W3 (2k+1 x H), "
+                    "argmax; random bf16 weights"}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -288,6 +322,8 @@ def main():
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
                      "traffic": measured_traffic()},
     }
+    if args.policy_prompts > 0:
+        res["policy"] = policy_run(torch, sd, args.policy_prompts)
     if args.verify_layers > 0:
         res["verify_step"] = verify_step_run(torch, sd, work, T, args.verify_layers, args.verify_steps)
     if not args.no_cpu_baseline:

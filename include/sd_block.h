@@ -227,6 +227,41 @@ int sd_verify_step(const sd_attn_shape *attn_shape, int32_t num_layers, const sd
                    const int32_t *draft_tokens, const float *uniforms, float temperature, int32_t *accept_len,
                    int32_t *next_token, void *workspace, size_t workspace_bytes, void *stream);
 
+/* ==========================================================================
+ * Block-size policy, run once per prompt after prefill (Sec. 2.3-2.4, Eq. 9).  The
+ * predictive distribution of the prompt's last token, p = softmax(z), feeds an MLP
+ * with two hidden layers (width 2048 by default, Sec. 3.1) scoring the 2k+1
+ * candidate block sizes {B-k, ..., B+k}; the chosen size is the argmax:
+ *   h1 = relu(W1 p + b1), h2 = relu(W2 h1 + b2), o = W3 h2 + b3,
+ *   block_size = B - k + argmax_c o_c   (lowest c on ties).
+ * ========================================================================== */
+typedef struct sd_policy_shape {
+  int32_t num_prompts;  /* P >= 0 */
+  int32_t vocab;        /* V, a multiple of 8 */
+  int32_t hidden;       /* H, a multiple of 8 (2048 in the paper) */
+  int32_t radius;       /* k: 2k+1 <= 64 candidates */
+  int32_t base_block;   /* B, the training block size; B - k >= 1 */
+  int32_t logits_dtype; /* SD_BF16 or SD_F32 */
+} sd_policy_shape;
+
+/* Workspace bytes sd_block_size_policy needs (host-only). */
+int sd_policy_workspace_size(const sd_policy_shape *shape, size_t *bytes);
+
+/*
+ *   last_logits  [P, V]     logits_dtype: the target's logits at each prompt's last position
+ *   w1 [H, V], w2 [H, H], w3 [2k+1, H]   bf16, row-major (output dimension first)
+ *   b1 [H], b2 [H], b3 [2k+1]            fp32
+ *   scores       [P, 2k+1]  fp32 out: o
+ *   block_size   [P] int32 out
+ * p and the layer activations are fp32; products accumulate in fp32.  Logits and w1, w2
+ * 16-byte aligned; workspace 256-byte aligned, >= sd_policy_workspace_size().
+ * Errors: SD_ERR_INVALID_ARG, SD_ERR_UNSUPPORTED (vocab or hidden not a multiple of 8),
+ * SD_ERR_WORKSPACE, SD_ERR_HIP.  P == 0 returns SD_OK without touching the device.
+ */
+int sd_block_size_policy(const sd_policy_shape *shape, const void *last_logits, const void *w1, const float *b1,
+                         const void *w2, const float *b2, const void *w3, const float *b3, float *scores,
+                         int32_t *block_size, void *workspace, size_t workspace_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

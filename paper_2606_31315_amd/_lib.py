@@ -20,7 +20,7 @@ SD_MASK_CAUSAL_IN_BLOCK, SD_MASK_BIDIR_IN_BLOCK = 0, 1
 
 EXPORTS = ["sd_last_error", "sd_version", "sd_block_attn_workspace_size", "sd_block_attn",
            "sd_accept_workspace_size", "sd_accept", "sd_kv_append", "sd_commit", "sd_verify_step_workspace_size",
-           "sd_verify_step"]
+           "sd_verify_step", "sd_policy_workspace_size", "sd_block_size_policy"]
 
 
 class SdAttnShape(ctypes.Structure):
@@ -33,6 +33,11 @@ class SdAttnShape(ctypes.Structure):
 class SdAcceptShape(ctypes.Structure):
     _fields_ = [("num_seqs", ctypes.c_int32), ("vocab", ctypes.c_int32), ("total_q", ctypes.c_int32),
                 ("max_block", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class SdPolicyShape(ctypes.Structure):
+    _fields_ = [("num_prompts", ctypes.c_int32), ("vocab", ctypes.c_int32), ("hidden", ctypes.c_int32),
+                ("radius", ctypes.c_int32), ("base_block", ctypes.c_int32), ("logits_dtype", ctypes.c_int32)]
 
 
 class SdLayerBuffers(ctypes.Structure):
@@ -77,6 +82,10 @@ def lib() -> ctypes.CDLL:
         L.sd_verify_step_workspace_size.restype = ctypes.c_int
         L.sd_verify_step_workspace_size.argtypes = [ctypes.POINTER(SdAttnShape), ctypes.POINTER(SdAcceptShape),
                                                     ctypes.c_float, ctypes.POINTER(Z)]
+        L.sd_policy_workspace_size.restype = ctypes.c_int
+        L.sd_policy_workspace_size.argtypes = [ctypes.POINTER(SdPolicyShape), ctypes.POINTER(Z)]
+        L.sd_block_size_policy.restype = ctypes.c_int
+        L.sd_block_size_policy.argtypes = [ctypes.POINTER(SdPolicyShape), P, P, P, P, P, P, P, P, P, P, Z, P]
         L.sd_verify_step.restype = ctypes.c_int
         L.sd_verify_step.argtypes = [ctypes.POINTER(SdAttnShape), I, ctypes.POINTER(SdLayerBuffers), P, P, P, I,
                                      ctypes.POINTER(SdAcceptShape), P, P, P, P, ctypes.c_float, P, P, P, Z, P]
@@ -286,6 +295,42 @@ def verify_step(layers, ctx_lens: torch.Tensor, block_lens: torch.Tensor, q_offs
                                 _ptr(next_token), _ptr(workspace), workspace.numel() * workspace.element_size(),
                                 _stream(stream)))
     return accept_len, next_token
+
+
+def policy_shape(last_logits: torch.Tensor, w1: torch.Tensor, w3: torch.Tensor, base_block: int) -> SdPolicyShape:
+    C = w3.shape[0]
+    return SdPolicyShape(last_logits.shape[0], last_logits.shape[1], w1.shape[0], (C - 1) // 2, int(base_block),
+                         _dtype_code(last_logits))
+
+
+def block_size_policy(last_logits: torch.Tensor, w1: torch.Tensor, b1: torch.Tensor, w2: torch.Tensor,
+                      b2: torch.Tensor, w3: torch.Tensor, b3: torch.Tensor, base_block: int, *,
+                      scores: Optional[torch.Tensor] = None, block_size: Optional[torch.Tensor] = None,
+                      workspace: Optional[torch.Tensor] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Block-size policy (sd_block_size_policy): last-token logits [P, V] -> (scores [P, 2k+1] fp32,
+    block sizes [P] int32).  Weights bf16 [out, in], biases fp32; 2k+1 = w3.shape[0]."""
+    dev = last_logits.device
+    _need(last_logits, "last_logits", device=dev)
+    for name, t in (("w1", w1), ("w2", w2), ("w3", w3)):
+        _need(t, name, torch.bfloat16, dev)
+    for name, t in (("b1", b1), ("b2", b2), ("b3", b3)):
+        _need(t, name, torch.float32, dev)
+    if w3.shape[0] % 2 != 1:
+        raise ValueError("w3 must have 2k+1 rows")
+    shape = policy_shape(last_logits, w1, w3, base_block)
+    n = ctypes.c_size_t(0)
+    _check(lib().sd_policy_workspace_size(ctypes.byref(shape), ctypes.byref(n)))
+    if workspace is None:
+        workspace = _default_ws.get(n.value, dev)
+    P = last_logits.shape[0]
+    if scores is None:
+        scores = torch.empty(P, w3.shape[0], dtype=torch.float32, device=dev)
+    if block_size is None:
+        block_size = torch.empty(P, dtype=torch.int32, device=dev)
+    _check(lib().sd_block_size_policy(ctypes.byref(shape), _ptr(last_logits), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2),
+                                      _ptr(w3), _ptr(b3), _ptr(scores), _ptr(block_size), _ptr(workspace),
+                                      workspace.numel() * workspace.element_size(), _stream(stream)))
+    return scores, block_size
 
 
 def version() -> str:

@@ -8,12 +8,14 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <string>
 
 #include "accept.hpp"
 #include "attn.hpp"
 #include "attn_bf16.hpp"
 #include "kvstep.hpp"
+#include "policy.hpp"
 #include "sd_block.h"
 
 namespace {
@@ -199,6 +201,61 @@ int accept_plan(const sd_accept_shape *sh, float temperature, AcceptPlan *p) {
   return ok();
 }
 
+int check_cache_shape(const sd_attn_shape *sh, const char *what) {
+  if (!sh) return fail(SD_ERR_INVALID_ARG, "%s: shape is NULL", what);
+  if (sh->num_seqs < 0) return fail(SD_ERR_INVALID_ARG, "num_seqs must be >= 0 (got %d)", sh->num_seqs);
+  if (sh->num_q_heads < 1 || sh->num_kv_heads < 1 || sh->num_q_heads % sh->num_kv_heads)
+    return fail(SD_ERR_INVALID_ARG, "head counts must be >= 1 with Hq %% Hkv == 0 (Hq=%d, Hkv=%d)",
+                sh->num_q_heads, sh->num_kv_heads);
+  if (sh->dtype != SD_BF16 && sh->dtype != SD_F32) return fail(SD_ERR_INVALID_ARG, "unknown dtype %d", sh->dtype);
+  if (sh->head_dim != 64 && sh->head_dim != 128)
+    return fail(SD_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", sh->head_dim);
+  if (sh->max_kv_len < 1) return fail(SD_ERR_INVALID_ARG, "max_kv_len must be >= 1 (got %d)", sh->max_kv_len);
+  if (sh->total_q < 0) return fail(SD_ERR_INVALID_ARG, "total_q must be >= 0 (got %d)", sh->total_q);
+  return ok();
+}
+
+struct PolicyPlan {
+  size_t off_stats, off_prob, off_h1, off_h2, total;
+};
+
+int policy_plan(const sd_policy_shape *sh, PolicyPlan *p) {
+  if (!sh) return fail(SD_ERR_INVALID_ARG, "sd_block_size_policy: shape is NULL");
+  if (sh->num_prompts < 0) return fail(SD_ERR_INVALID_ARG, "num_prompts must be >= 0 (got %d)", sh->num_prompts);
+  if (sh->vocab < 8 || sh->vocab % 8 || sh->vocab > (1 << 28))
+    return fail(SD_ERR_UNSUPPORTED, "vocab must be a multiple of 8 in [8, 2^28] (got %d)", sh->vocab);
+  if (sh->hidden < 8 || sh->hidden % 8 || sh->hidden > (1 << 20))
+    return fail(SD_ERR_UNSUPPORTED, "hidden must be a multiple of 8 in [8, 2^20] (got %d)", sh->hidden);
+  if (sh->radius < 0 || 2 * sh->radius + 1 > 64)
+    return fail(SD_ERR_INVALID_ARG, "radius must give at most 64 candidates (got %d)", sh->radius);
+  if (sh->base_block - sh->radius < 1)
+    return fail(SD_ERR_INVALID_ARG, "candidate block sizes must be >= 1 (base %d, radius %d)", sh->base_block,
+                sh->radius);
+  if (sh->logits_dtype != SD_BF16 && sh->logits_dtype != SD_F32)
+    return fail(SD_ERR_INVALID_ARG, "unknown dtype %d", sh->logits_dtype);
+  const size_t P = (size_t)sh->num_prompts;
+  size_t off = 0;
+  p->off_stats = off;
+  off = align256(off + P * sdb::kPolicyChunks * sizeof(float2));
+  p->off_prob = off;
+  off = align256(off + P * sh->vocab * sizeof(float));
+  p->off_h1 = off;
+  off = align256(off + P * sh->hidden * sizeof(float));
+  p->off_h2 = off;
+  off = align256(off + P * sh->hidden * sizeof(float));
+  p->total = off > 0 ? off : 256;
+  return ok();
+}
+
+template <bool RELU>
+void launch_dense(const sdb::DenseArgs &d, hipStream_t st) {
+  const dim3 grid((d.rows + sdb::kDenseRows - 1) / sdb::kDenseRows);
+  if (d.P <= 1) hipLaunchKernelGGL((sdb::policy_dense_kernel<1, RELU>), grid, dim3(256), 0, st, d);
+  else if (d.P <= 2) hipLaunchKernelGGL((sdb::policy_dense_kernel<2, RELU>), grid, dim3(256), 0, st, d);
+  else if (d.P <= 4) hipLaunchKernelGGL((sdb::policy_dense_kernel<4, RELU>), grid, dim3(256), 0, st, d);
+  else hipLaunchKernelGGL((sdb::policy_dense_kernel<8, RELU>), grid, dim3(256), 0, st, d);
+}
+
 }  // namespace
 
 extern "C" {
@@ -354,20 +411,6 @@ int sd_accept(const sd_accept_shape *sh, const void *target_logits, const void *
 // ---------------------------------------------------------------------------
 // the step around verification: append, commit, and the whole verify step
 // ---------------------------------------------------------------------------
-static int check_cache_shape(const sd_attn_shape *sh, const char *what) {
-  if (!sh) return fail(SD_ERR_INVALID_ARG, "%s: shape is NULL", what);
-  if (sh->num_seqs < 0) return fail(SD_ERR_INVALID_ARG, "num_seqs must be >= 0 (got %d)", sh->num_seqs);
-  if (sh->num_q_heads < 1 || sh->num_kv_heads < 1 || sh->num_q_heads % sh->num_kv_heads)
-    return fail(SD_ERR_INVALID_ARG, "head counts must be >= 1 with Hq %% Hkv == 0 (Hq=%d, Hkv=%d)",
-                sh->num_q_heads, sh->num_kv_heads);
-  if (sh->dtype != SD_BF16 && sh->dtype != SD_F32) return fail(SD_ERR_INVALID_ARG, "unknown dtype %d", sh->dtype);
-  if (sh->head_dim != 64 && sh->head_dim != 128)
-    return fail(SD_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", sh->head_dim);
-  if (sh->max_kv_len < 1) return fail(SD_ERR_INVALID_ARG, "max_kv_len must be >= 1 (got %d)", sh->max_kv_len);
-  if (sh->total_q < 0) return fail(SD_ERR_INVALID_ARG, "total_q must be >= 0 (got %d)", sh->total_q);
-  return ok();
-}
-
 int sd_kv_append(const sd_attn_shape *sh, const void *k_new, const void *v_new, void *k_cache, void *v_cache,
                  const int32_t *ctx_lens, const int32_t *q_offsets, void *stream) {
   int rc = check_cache_shape(sh, "sd_kv_append");
@@ -448,6 +491,64 @@ int sd_verify_step(const sd_attn_shape *ash, int32_t num_layers, const sd_layer_
                  accept_len, next_token, workspace, workspace_bytes, stream);
   if (rc) return rc;
   return sd_commit(csh->num_seqs, accept_len, ctx_lens, stream);
+}
+
+// ---------------------------------------------------------------------------
+// block-size policy (once per prompt)
+// ---------------------------------------------------------------------------
+int sd_policy_workspace_size(const sd_policy_shape *shape, size_t *bytes) {
+  if (!bytes) return fail(SD_ERR_INVALID_ARG, "bytes is NULL");
+  PolicyPlan p;
+  int rc = policy_plan(shape, &p);
+  if (rc) return rc;
+  *bytes = p.total;
+  return ok();
+}
+
+int sd_block_size_policy(const sd_policy_shape *sh, const void *last_logits, const void *w1, const float *b1,
+                         const void *w2, const float *b2, const void *w3, const float *b3, float *scores,
+                         int32_t *block_size, void *workspace, size_t workspace_bytes, void *stream) {
+  PolicyPlan p;
+  int rc = policy_plan(sh, &p);
+  if (rc) return rc;
+  if (sh->num_prompts == 0) return ok();
+  if (!last_logits || !w1 || !b1 || !w2 || !b2 || !w3 || !b3 || !scores || !block_size || !workspace)
+    return fail(SD_ERR_INVALID_ARG, "sd_block_size_policy: NULL pointer argument");
+  if (!aligned16(w1) || !aligned16(w2) || !aligned16(last_logits))
+    return fail(SD_ERR_INVALID_ARG, "logits and weights must be 16-byte aligned");
+  if (((uintptr_t)workspace & 255u) != 0) return fail(SD_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  if (workspace_bytes < p.total)
+    return fail(SD_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, p.total);
+  hipStream_t st = (hipStream_t)stream;
+  char *ws = (char *)workspace;
+  const int P = sh->num_prompts, V = sh->vocab, H = sh->hidden, C = 2 * sh->radius + 1;
+  sdb::PolicyArgs pa;
+  pa.logits = last_logits;
+  pa.stats = (float2 *)(ws + p.off_stats);
+  pa.prob = (float *)(ws + p.off_prob);
+  pa.P = P;
+  pa.V = V;
+  pa.logits_bf16 = sh->logits_dtype == SD_BF16;
+  const dim3 gsoft(P * sdb::kPolicyChunks);
+  if (pa.logits_bf16) {
+    hipLaunchKernelGGL(sdb::policy_stats_kernel<true>, gsoft, dim3(256), 0, st, pa);
+    hipLaunchKernelGGL(sdb::policy_prob_kernel<true>, gsoft, dim3(256), 0, st, pa);
+  } else {
+    hipLaunchKernelGGL(sdb::policy_stats_kernel<false>, gsoft, dim3(256), 0, st, pa);
+    hipLaunchKernelGGL(sdb::policy_prob_kernel<false>, gsoft, dim3(256), 0, st, pa);
+  }
+  float *h1 = (float *)(ws + p.off_h1), *h2 = (float *)(ws + p.off_h2);
+  // dense layers in groups of kPolicyMaxPrompts prompts (each group reads the weights once)
+  for (int g0 = 0; g0 < P; g0 += sdb::kPolicyMaxPrompts) {
+    const int np = std::min(sdb::kPolicyMaxPrompts, P - g0);
+    sdb::DenseArgs d1{(const uint16_t *)w1, pa.prob + (size_t)g0 * V, b1, h1 + (size_t)g0 * H, H, V, np};
+    launch_dense<true>(d1, st);
+    sdb::DenseArgs d2{(const uint16_t *)w2, h1 + (size_t)g0 * H, b2, h2 + (size_t)g0 * H, H, H, np};
+    launch_dense<true>(d2, st);
+  }
+  sdb::HeadArgs ha{(const uint16_t *)w3, h2, b3, scores, block_size, C, H, sh->base_block, sh->radius};
+  hipLaunchKernelGGL(sdb::policy_head_kernel, dim3(P), dim3(256), 0, st, ha);
+  return check_launch("sd_block_size_policy");
 }
 
 }  // extern "C"

@@ -357,3 +357,56 @@ def step_block_inputs(rs: dict, *, total_q, Hq, Hkv, D, dtype) -> dict:
     return dict(q=_to_dtype(rs["q"].standard_normal((total_q, Hq, D), dtype=np.float32), dtype),
                 k_new=_to_dtype(rs["K"].standard_normal((total_q, Hkv, D), dtype=np.float32), dtype),
                 v_new=_to_dtype(rs["V"].standard_normal((total_q, Hkv, D), dtype=np.float32), dtype))
+
+
+# --------------------------------------------------------------------------- #
+# block-size policy inputs: last-token logits and random MLP weights
+# --------------------------------------------------------------------------- #
+
+@dataclass
+class PolicyProblem:
+    """Last-token logits [P, V] and the MLP's weights (bf16, [out, in]) and biases (fp32).
+
+    The trained predictor weights are not available; the weights here are seeded random
+    draws: W1 ~ N(0, 1) (its input p sums to one), W2, W3 ~ N(0, 1/H), biases ~ N(0, 0.05^2).
+    """
+    logits: torch.Tensor
+    w1: torch.Tensor
+    b1: np.ndarray
+    w2: torch.Tensor
+    b2: np.ndarray
+    w3: torch.Tensor
+    b3: np.ndarray
+    base_block: int
+    radius: int
+    dtype: str
+    name: str = ""
+
+    @property
+    def P(self) -> int:
+        return int(self.logits.shape[0])
+
+    @property
+    def V(self) -> int:
+        return int(self.logits.shape[1])
+
+    @property
+    def H(self) -> int:
+        return int(self.w1.shape[0])
+
+    def weight_bytes(self) -> int:
+        return 2 * (self.w1.numel() + self.w2.numel() + self.w3.numel())
+
+
+def make_policy(seed: int, *, P, V, H=2048, radius=2, base_block=16, dtype="bf16", logit_sigma=3.0,
+                name="") -> PolicyProblem:
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence(seed)))
+    C = 2 * radius + 1
+    logits = _to_dtype(g.standard_normal((P, V), dtype=np.float32) * np.float32(logit_sigma), dtype)
+    w1 = torch.from_numpy(g.standard_normal((H, V), dtype=np.float32)).to(torch.bfloat16)
+    w2 = torch.from_numpy(g.standard_normal((H, H), dtype=np.float32) / np.float32(np.sqrt(H))).to(torch.bfloat16)
+    w3 = torch.from_numpy(g.standard_normal((C, H), dtype=np.float32) / np.float32(np.sqrt(H))).to(torch.bfloat16)
+    b1 = (g.standard_normal(H, dtype=np.float32) * np.float32(0.05)).astype(np.float32)
+    b2 = (g.standard_normal(H, dtype=np.float32) * np.float32(0.05)).astype(np.float32)
+    b3 = (g.standard_normal(C, dtype=np.float32) * np.float32(0.05)).astype(np.float32)
+    return PolicyProblem(logits, w1, b1, w2, b2, w3, b3, base_block, radius, dtype, name)
