@@ -215,6 +215,46 @@ def policy_run(torch, sd, prompts, reps=20, V=151936, H=2048, radius=2, base_blo
                     "argmax; random bf16 weights"}
 
 
+def paged_run(torch, sd, a, bufs, page_size, reps, shuffle=True):
+    """sd_block_attn_paged on the same keys and values as the timed step, scattered over a pool
+    of page_size-key pages in a shuffled (or in-order) page order, one pool per input copy."""
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev).manual_seed(13)
+    S, Hkv, Lmax, D = bufs[0]["k"].shape
+    mp = (Lmax + page_size - 1) // page_size
+    pools = []
+    for b in bufs:
+        perm = (torch.randperm(S * mp, device=dev, generator=g) if shuffle
+                else torch.arange(S * mp, device=dev))
+        pk = []
+        for name in ("k", "v"):
+            x = torch.nn.functional.pad(b[name], (0, 0, 0, mp * page_size - Lmax))
+            x = x.reshape(S, Hkv, mp, page_size, D).permute(0, 2, 1, 3, 4).reshape(S * mp, Hkv, page_size, D)
+            pool = torch.empty_like(x)
+            pool[perm] = x
+            pk.append(pool)
+        pools.append((pk[0], pk[1], perm.to(torch.int32).reshape(S, mp).contiguous()))
+    ctx = torch.from_numpy(a.ctx_lens).to(dev)
+    bl, off = torch.from_numpy(a.block_lens).to(dev), torch.from_numpy(a.q_offsets).to(dev)
+    out = torch.empty_like(bufs[0]["q"])
+
+    def call(i):
+        kp, vp, tab = pools[i % len(pools)]
+        sd.block_attn_paged(bufs[i % len(bufs)]["q"], kp, vp, tab, ctx, bl, off, a.mask_mode, max_ctx=a.max_ctx,
+                            max_block=a.max_block, out=out)
+
+    for i in range(10):
+        call(i)
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for i in range(reps):
+        call(i)
+    t1.record()
+    torch.cuda.synchronize()
+    return round(t0.elapsed_time(t1) / reps * 1e3, 2)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -322,6 +362,8 @@ def main():
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
                      "traffic": measured_traffic()},
     }
+    res["paged_attn_us"] = {f"page_{ps}_shuffled": paged_run(torch, sd, a, bufs, ps, K) for ps in (16, 64, 256)}
+    res["paged_attn_us"]["page_64_in_order"] = paged_run(torch, sd, a, bufs, 64, K, shuffle=False)
     if args.policy_prompts > 0:
         res["policy"] = policy_run(torch, sd, args.policy_prompts)
     if args.verify_layers > 0:

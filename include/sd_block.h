@@ -116,6 +116,22 @@ int sd_block_attn(const sd_attn_shape *shape, const void *q, const void *k_cache
                   const int32_t *ctx_lens, const int32_t *block_lens, const int32_t *q_offsets,
                   int32_t mask_mode, void *out, void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * Paged variant: the caches are pools of fixed-size pages shared by all sequences, as a
+ * serving engine keeps them.  Logical key j of sequence s lives in pool page
+ * block_table[s * max_pages + j / page_size] at row j % page_size:
+ *   k_pages, v_pages [num_pages, Hkv, page_size, D] bf16
+ *   block_table      [S, max_pages] int32 (device)
+ * Everything else, including the result, is as in sd_block_attn (same workspace size);
+ * shape->max_kv_len must equal max_pages * page_size.  page_size is a power of two in
+ * [16, 4096].  Page ids outside [0, num_pages) are clamped into the pool (the result is then
+ * meaningless, but no read leaves the pool).  bf16 only (SD_ERR_UNSUPPORTED otherwise).
+ */
+int sd_block_attn_paged(const sd_attn_shape *shape, int32_t page_size, int32_t num_pages, int32_t max_pages,
+                        const int32_t *block_table, const void *q, const void *k_pages, const void *v_pages,
+                        const int32_t *ctx_lens, const int32_t *block_lens, const int32_t *q_offsets,
+                        int32_t mask_mode, void *out, void *workspace, size_t workspace_bytes, void *stream);
+
 /* ==========================================================================
  * Speculative acceptance (Fig. 1 caption: accept the longest consistent prefix;
  * Sec. 1 and Sec. 3.1: the target's output distribution is preserved exactly).
@@ -189,6 +205,15 @@ int sd_accept(const sd_accept_shape *shape, const void *target_logits, const voi
  */
 int sd_kv_append(const sd_attn_shape *shape, const void *k_new, const void *v_new, void *k_cache, void *v_cache,
                  const int32_t *ctx_lens, const int32_t *q_offsets, void *stream);
+
+/*
+ * sd_kv_append into page pools (layout as in sd_block_attn_paged): block row i of sequence s
+ * goes to logical key ctx_s + i.  A row past max_pages * page_size, or whose page id lies
+ * outside [0, num_pages), is skipped, not written.  The shape's max_kv_len is not used.
+ */
+int sd_kv_append_paged(const sd_attn_shape *shape, int32_t page_size, int32_t num_pages, int32_t max_pages,
+                       const int32_t *block_table, const void *k_new, const void *v_new, void *k_pages, void *v_pages,
+                       const int32_t *ctx_lens, const int32_t *q_offsets, void *stream);
 
 /*
  * ctx_lens[s] += accept_len[s] + 1: the block's anchor and its accepted drafts are now part of

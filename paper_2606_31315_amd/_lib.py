@@ -20,7 +20,8 @@ SD_MASK_CAUSAL_IN_BLOCK, SD_MASK_BIDIR_IN_BLOCK = 0, 1
 
 EXPORTS = ["sd_last_error", "sd_version", "sd_block_attn_workspace_size", "sd_block_attn",
            "sd_accept_workspace_size", "sd_accept", "sd_kv_append", "sd_commit", "sd_verify_step_workspace_size",
-           "sd_verify_step", "sd_policy_workspace_size", "sd_block_size_policy"]
+           "sd_verify_step", "sd_policy_workspace_size", "sd_block_size_policy", "sd_block_attn_paged",
+           "sd_kv_append_paged"]
 
 
 class SdAttnShape(ctypes.Structure):
@@ -75,6 +76,10 @@ def lib() -> ctypes.CDLL:
         L.sd_accept_workspace_size.argtypes = [ctypes.POINTER(SdAcceptShape), ctypes.c_float, ctypes.POINTER(Z)]
         L.sd_accept.restype = ctypes.c_int
         L.sd_accept.argtypes = [ctypes.POINTER(SdAcceptShape), P, P, P, P, P, P, ctypes.c_float, P, P, P, Z, P]
+        L.sd_block_attn_paged.restype = ctypes.c_int
+        L.sd_block_attn_paged.argtypes = [ctypes.POINTER(SdAttnShape), I, I, I, P, P, P, P, P, P, P, I, P, P, Z, P]
+        L.sd_kv_append_paged.restype = ctypes.c_int
+        L.sd_kv_append_paged.argtypes = [ctypes.POINTER(SdAttnShape), I, I, I, P, P, P, P, P, P, P, P]
         L.sd_kv_append.restype = ctypes.c_int
         L.sd_kv_append.argtypes = [ctypes.POINTER(SdAttnShape), P, P, P, P, P, P, P]
         L.sd_commit.restype = ctypes.c_int
@@ -186,6 +191,54 @@ def block_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, ct
                                _ptr(block_lens), _ptr(q_offsets), int(mask_mode), _ptr(out), _ptr(workspace),
                                workspace.numel() * workspace.element_size(), _stream(stream)))
     return out
+
+
+def block_attn_paged(q: torch.Tensor, k_pages: torch.Tensor, v_pages: torch.Tensor, block_table: torch.Tensor,
+                     ctx_lens: torch.Tensor, block_lens: torch.Tensor, q_offsets: torch.Tensor, mask_mode: int, *,
+                     max_ctx: int, max_block: int, scale: float = 0.0, out: Optional[torch.Tensor] = None,
+                     workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Block attention over paged caches (sd_block_attn_paged).  k_pages, v_pages
+    [num_pages, Hkv, page_size, D] bf16; block_table [S, max_pages] int32 on the device."""
+    dev = q.device
+    _need(q, "q", torch.bfloat16, dev)
+    _need(k_pages, "k_pages", torch.bfloat16, dev)
+    _need(v_pages, "v_pages", torch.bfloat16, dev)
+    for name, t in (("block_table", block_table), ("ctx_lens", ctx_lens), ("block_lens", block_lens),
+                    ("q_offsets", q_offsets)):
+        _need(t, name, torch.int32, dev)
+    num_pages, Hkv, page_size, D = k_pages.shape
+    S, max_pages = block_table.shape
+    if out is None:
+        out = torch.empty_like(q)
+    _need(out, "out", q.dtype, dev)
+    shape = SdAttnShape(S, q.shape[1], Hkv, D, max_pages * page_size, q.shape[0], int(max_ctx), int(max_block),
+                        SD_BF16, float(scale))
+    nbytes = attn_workspace_size(shape)
+    if workspace is None:
+        workspace = _default_ws.get(nbytes, dev)
+    _check(lib().sd_block_attn_paged(ctypes.byref(shape), page_size, num_pages, max_pages, _ptr(block_table), _ptr(q),
+                                     _ptr(k_pages), _ptr(v_pages), _ptr(ctx_lens), _ptr(block_lens), _ptr(q_offsets),
+                                     int(mask_mode), _ptr(out), _ptr(workspace),
+                                     workspace.numel() * workspace.element_size(), _stream(stream)))
+    return out
+
+
+def kv_append_paged(k_new: torch.Tensor, v_new: torch.Tensor, k_pages: torch.Tensor, v_pages: torch.Tensor,
+                    block_table: torch.Tensor, ctx_lens: torch.Tensor, q_offsets: torch.Tensor, stream=None) -> None:
+    """sd_kv_append into page pools [num_pages, Hkv, page_size, D] through block_table [S, max_pages]."""
+    dev = k_new.device
+    _need(k_new, "k_new", device=dev)
+    _need(v_new, "v_new", k_new.dtype, dev)
+    _need(k_pages, "k_pages", k_new.dtype, dev)
+    _need(v_pages, "v_pages", k_new.dtype, dev)
+    for name, t in (("block_table", block_table), ("ctx_lens", ctx_lens), ("q_offsets", q_offsets)):
+        _need(t, name, torch.int32, dev)
+    num_pages, Hkv, page_size, D = k_pages.shape
+    S, max_pages = block_table.shape
+    shape = SdAttnShape(S, Hkv, Hkv, D, max_pages * page_size, k_new.shape[0], 0, 1, _dtype_code(k_new), 0.0)
+    _check(lib().sd_kv_append_paged(ctypes.byref(shape), page_size, num_pages, max_pages, _ptr(block_table),
+                                    _ptr(k_new), _ptr(v_new), _ptr(k_pages), _ptr(v_pages), _ptr(ctx_lens),
+                                    _ptr(q_offsets), _stream(stream)))
 
 
 def accept_shape(target_logits: torch.Tensor, num_seqs: int, max_block: int) -> SdAcceptShape:

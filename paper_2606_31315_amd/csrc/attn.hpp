@@ -47,6 +47,10 @@ struct AttnArgs {
   int per_xcd;        // ceil(n_work / 8)
   float scale_log2;   // softmax scale * log2(e)
   int causal;
+  // paged caches only: k, v are page pools [num_pages, Hkv, page_size, D]; logical page j of
+  // sequence s is pool page block_table[s * max_pages + j]
+  const int *block_table;
+  int page_log2, max_pages, num_pages;
 };
 
 template <bool BF16>

@@ -91,6 +91,7 @@ struct TileLoads {
   using T = Bf16Tile<D, KT, NS>;
   int row[T::LPW];
   unsigned src[T::LPW];
+  unsigned cof[T::LPW];  // swizzled chunk offset within the row
   bool isv;
   __device__ void init(int wave, int lane) {
     isv = wave * T::LPW >= T::LPI;  // uniform per wavefront
@@ -100,6 +101,37 @@ struct TileLoads {
       row[q] = li * T::RPI + lane / T::CPR;
       const int chunk = (lane % T::CPR) ^ (isv ? T::swz_v(row[q]) : T::swz_k(row[q]));
       src[q] = row[q] * T::ROWB + chunk * 16;
+      cof[q] = chunk * 16;
+    }
+  }
+  // The same tile from a page pool: key k of sequence s lives in pool page
+  // table[k >> log2] at row k & (page_size - 1).  A load instruction covers RPI consecutive
+  // keys of one page (tiles start on a multiple of 16 keys, pages hold a multiple of 16 keys,
+  // and rows past key_last re-read key_last), so its page id is uniform: fetch_pages reads it
+  // with a scalar load one tile ahead of issue_paged.  (An LDS lookup would make the compiler
+  // drain every in-flight load-to-LDS transfer before it.)  Ids are clamped into the pool.
+  __device__ void fetch_pages(const int *table, int max_pages, int num_pages, int log2, int key0, int key_last,
+                              int wave, int (&pg)[T::LPW]) const {
+#pragma unroll
+    for (int q = 0; q < T::LPW; ++q) {
+      const int li = wave * T::LPW + q - (isv ? T::LPI : 0);
+      // uniform per wavefront; readfirstlane tells the compiler, so the id comes by a scalar
+      // load (a vector load would need a vmcnt wait that drains the tile loads in flight)
+      const int key = __builtin_amdgcn_readfirstlane(min(key0 + li * T::RPI, key_last));
+      pg[q] = min(max(ld_uniform(table, min(key >> log2, max_pages - 1)), 0), num_pages - 1);
+    }
+  }
+  __device__ void issue_paged(char SDB_LDS *stage, const char *kpool, const char *vpool, int key0, int key_last,
+                              const int (&pg)[T::LPW], int log2, int Hkv, int g, int wave) const {
+    const char *pool = isv ? vpool : kpool;
+    char SDB_LDS *dst = stage + (isv ? T::TILEB : 0) + (wave * T::LPW - (isv ? T::LPI : 0)) * 1024;
+    const int mask = (1 << log2) - 1;
+#pragma unroll
+    for (int q = 0; q < T::LPW; ++q) {
+      const char *page = pool + ((((size_t)pg[q] * Hkv + g) << log2) * T::ROWB);
+      const int key = min(key0 + row[q], key_last);
+      __builtin_amdgcn_global_load_lds((const void *)(page + (unsigned)((key & mask) * T::ROWB) + cof[q]),
+                                       (SDB_LDS void *)(dst + q * 1024), 16, 0, 0);
     }
   }
   // Issue the loads of the tile starting at key0 into `stage`; rows past key_last
@@ -149,7 +181,7 @@ __device__ __forceinline__ void pv_step(const f32x4 (&p)[NSB], unsigned stage, c
   }
 }
 
-template <int D, int MT, int KT_, int NS_>
+template <int D, int MT, int KT_, int NS_, bool PAGED>
 __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   using T = Bf16Tile<D, KT_, NS_>;
   constexpr int KT = T::KT, NS = T::NS, NDT = D / 16, NST = D / 32, NSB = KT / 16;
@@ -183,8 +215,12 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   const int kgrp = lane >> 4;
   const int nmt = (M + 15) >> 4;
 
-  const char *kbase = reinterpret_cast<const char *>(a.k) + ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
-  const char *vbase = reinterpret_cast<const char *>(a.v) + ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
+  const char *kbase = reinterpret_cast<const char *>(a.k);
+  const char *vbase = reinterpret_cast<const char *>(a.v);
+  if constexpr (!PAGED) {
+    kbase += ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
+    vbase += ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
+  }
 
   // ---- query operands: element e of step st is dim st*32 + kgrp*8 + e of row m ----
   bf16x8 qop[MT][NST];
@@ -228,12 +264,24 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
 
   TileLoads<D, KT, NS> ld;
   ld.init(wave, lane);
+  // paged caches: this sequence's row of the block table
+  [[maybe_unused]] const int *table = PAGED ? a.block_table + (size_t)s * a.max_pages : nullptr;
+  [[maybe_unused]] int pgn[T::LPW];  // page ids of the next tile to issue (paged caches)
+  auto issue = [&](char SDB_LDS *stage, int key0) {
+    if constexpr (PAGED) {
+      ld.issue_paged(stage, kbase, vbase, key0, k1 - 1, pgn, a.page_log2, a.Hkv, g, wave);
+      ld.fetch_pages(table, a.max_pages, a.num_pages, a.page_log2, key0 + KT, k1 - 1, wave, pgn);
+    } else {
+      ld.issue(stage, kbase, vbase, key0, k1 - 1, wave);
+    }
+  };
 
   // ---- pipeline prologue: tiles 0 .. NS-2 in flight ----
   const int ntiles = (k1 - k0 + KT - 1) / KT;
+  if constexpr (PAGED) ld.fetch_pages(table, a.max_pages, a.num_pages, a.page_log2, k0, k1 - 1, wave, pgn);
 #pragma unroll
   for (int t = 0; t < NS - 1; ++t)
-    if (t < ntiles) ld.issue(ring + t * T::STAGEB, kbase, vbase, k0 + t * KT, k1 - 1, wave);
+    if (t < ntiles) issue(ring + t * T::STAGEB, k0 + t * KT);
   // keys every row can see: all of [k0, k1) when bidirectional, keys <= ctx when causal
   const int vis_all = a.causal ? min(k1, ctx + 1) : k1;
   const float sl2 = a.scale_log2;
@@ -246,8 +294,7 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
     else if (NS > 2 && ahead >= 1) wait_vmcnt<T::LPW>();
     else wait_vmcnt<0>();
     __syncthreads();  // tile t landed for every wavefront; stage (t-1) % NS is free again
-    if (t + NS - 1 < ntiles)
-      ld.issue(ring + ((t + NS - 1) % NS) * T::STAGEB, kbase, vbase, kt + (NS - 1) * KT, k1 - 1, wave);
+    if (t + NS - 1 < ntiles) issue(ring + ((t + NS - 1) % NS) * T::STAGEB, kt + (NS - 1) * KT);
     const unsigned stage = (unsigned)(uintptr_t)(ring + (t % NS) * T::STAGEB);
     const bool full = kt + KT <= vis_all;  // uniform: no key of this tile is masked for any row
 #pragma unroll

@@ -24,6 +24,10 @@ struct AppendArgs {
   const int *q_offsets;
   int S, Hkv, Lmax, total_q;
   int row_vecs;        // 16-byte vectors per (token, head) row: D * element bytes / 16
+  // page pools only: caches are [num_pages, Hkv, page_size, D], logical page j of sequence s is
+  // pool page block_table[s * max_pages + j]
+  const int *block_table;
+  int page_log2, max_pages, num_pages;
 };
 
 // Largest s with off[s] <= r (r < off[S]): the sequence that owns packed row r.
@@ -51,6 +55,26 @@ __global__ __launch_bounds__(256) void kv_append_kernel(AppendArgs a) {
   for (int i = threadIdx.x; i < n; i += blockDim.x) {
     const int h = i / a.row_vecs, c = i - h * a.row_vecs;
     dst[(((size_t)s * a.Hkv + h) * a.Lmax + pos) * a.row_vecs + c] = src[i];
+  }
+}
+
+// The same copy into page pools.  A row past the sequence's pages, or whose page id lies
+// outside the pool, is skipped rather than written.
+__global__ __launch_bounds__(256) void kv_append_paged_kernel(AppendArgs a) {
+  const int r = blockIdx.x;
+  const int kv = blockIdx.y;
+  const int s = row_owner(a.q_offsets, a.S, r);
+  const int pos = ld_uniform(a.ctx_lens, s) + (r - ld_uniform(a.q_offsets, s));
+  if (pos < 0 || pos >= a.Lmax) return;
+  const int pg = ld_uniform(a.block_table, (long long)s * a.max_pages + (pos >> a.page_log2));
+  if (pg < 0 || pg >= a.num_pages) return;
+  const size_t row0 = (((size_t)pg * a.Hkv) << a.page_log2) + (pos & ((1 << a.page_log2) - 1));
+  const u32x4 *src = reinterpret_cast<const u32x4 *>(kv ? a.v_new : a.k_new) + (size_t)r * a.Hkv * a.row_vecs;
+  u32x4 *dst = reinterpret_cast<u32x4 *>(kv ? a.v_cache : a.k_cache);
+  const int n = a.Hkv * a.row_vecs;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    const int h = i / a.row_vecs, c = i - h * a.row_vecs;
+    dst[(row0 + ((size_t)h << a.page_log2)) * a.row_vecs + c] = src[i];
   }
 }
 

@@ -128,13 +128,13 @@ void launch_attn(const sdb::AttnArgs &a, int grid, hipStream_t st) {
   hipLaunchKernelGGL((sdb::block_attn_kernel<BF16, D, MT>), dim3(grid), dim3(256), 0, st, a);
 }
 
-template <bool BF16, int D>
+template <bool BF16, int D, bool PAGED = false>
 void launch_attn_all(const sdb::AttnArgs &a, int grid, int MT, hipStream_t st) {
   if constexpr (BF16) {
     if (MT == 1)
-      hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 1, kBf16KT, kBf16NS>), dim3(grid), dim3(512), 0, st, a);
+      hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 1, kBf16KT, kBf16NS, PAGED>), dim3(grid), dim3(512), 0, st, a);
     else
-      hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 2, kBf16KT, kBf16NS>), dim3(grid), dim3(512), 0, st, a);
+      hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 2, kBf16KT, kBf16NS, PAGED>), dim3(grid), dim3(512), 0, st, a);
   } else {
     if (MT == 1) launch_attn<BF16, D, 1>(a, grid, st);
     else if (MT == 2) launch_attn<BF16, D, 2>(a, grid, st);
@@ -273,15 +273,13 @@ int sd_block_attn_workspace_size(const sd_attn_shape *shape, size_t *bytes) {
   return ok();
 }
 
-int sd_block_attn(const sd_attn_shape *sh, const void *q, const void *k_cache, const void *v_cache,
-                  const int32_t *ctx_lens, const int32_t *block_lens, const int32_t *q_offsets,
-                  int32_t mask_mode, void *out, void *workspace, size_t workspace_bytes, void *stream) {
-  AttnPlan p;
-  int rc = attn_plan(sh, &p);
-  if (rc) return rc;
+namespace {
+
+int attn_args(const sd_attn_shape *sh, const AttnPlan &p, const void *q, const void *k_cache, const void *v_cache,
+              const int32_t *ctx_lens, const int32_t *block_lens, const int32_t *q_offsets, int32_t mask_mode,
+              void *out, void *workspace, size_t workspace_bytes, sdb::AttnArgs *a) {
   if (mask_mode != SD_MASK_CAUSAL_IN_BLOCK && mask_mode != SD_MASK_BIDIR_IN_BLOCK)
     return fail(SD_ERR_INVALID_ARG, "unknown mask_mode %d", mask_mode);
-  if (sh->num_seqs == 0 || sh->total_q == 0) return ok();
   if (!q || !k_cache || !v_cache || !out || !ctx_lens || !block_lens || !q_offsets || !workspace)
     return fail(SD_ERR_INVALID_ARG, "sd_block_attn: NULL pointer argument");
   if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out))
@@ -289,31 +287,51 @@ int sd_block_attn(const sd_attn_shape *sh, const void *q, const void *k_cache, c
   if (((uintptr_t)workspace & 255u) != 0) return fail(SD_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
   if (workspace_bytes < p.total)
     return fail(SD_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, p.total);
-
-  sdb::AttnArgs a;
-  a.q = q;
-  a.k = k_cache;
-  a.v = v_cache;
-  a.out = out;
-  a.ctx_lens = ctx_lens;
-  a.block_lens = block_lens;
-  a.q_offsets = q_offsets;
+  a->q = q;
+  a->k = k_cache;
+  a->v = v_cache;
+  a->out = out;
+  a->ctx_lens = ctx_lens;
+  a->block_lens = block_lens;
+  a->q_offsets = q_offsets;
   char *ws = (char *)workspace;
-  a.part_ml = (float2 *)(ws + p.off_ml);
-  a.part_o = (float *)(ws + p.off_o);
-  a.S = sh->num_seqs;
-  a.Hq = sh->num_q_heads;
-  a.Hkv = sh->num_kv_heads;
-  a.G = p.G;
-  a.Lmax = sh->max_kv_len;
-  a.split_len = p.split_len;
-  a.max_splits = p.max_splits;
-  a.Mpad = p.Mpad;
-  a.n_work = p.n_work;
-  a.per_xcd = p.per_xcd;
+  a->part_ml = (float2 *)(ws + p.off_ml);
+  a->part_o = (float *)(ws + p.off_o);
+  a->S = sh->num_seqs;
+  a->Hq = sh->num_q_heads;
+  a->Hkv = sh->num_kv_heads;
+  a->G = p.G;
+  a->Lmax = sh->max_kv_len;
+  a->split_len = p.split_len;
+  a->max_splits = p.max_splits;
+  a->Mpad = p.Mpad;
+  a->n_work = p.n_work;
+  a->per_xcd = p.per_xcd;
   const float scale = sh->scale > 0.f ? sh->scale : 1.0f / sqrtf((float)sh->head_dim);
-  a.scale_log2 = scale * 1.4426950408889634f;
-  a.causal = mask_mode == SD_MASK_CAUSAL_IN_BLOCK;
+  a->scale_log2 = scale * 1.4426950408889634f;
+  a->causal = mask_mode == SD_MASK_CAUSAL_IN_BLOCK;
+  a->block_table = nullptr;
+  a->page_log2 = a->max_pages = a->num_pages = 0;
+  return ok();
+}
+
+}  // namespace
+
+int sd_block_attn(const sd_attn_shape *sh, const void *q, const void *k_cache, const void *v_cache,
+                  const int32_t *ctx_lens, const int32_t *block_lens, const int32_t *q_offsets,
+                  int32_t mask_mode, void *out, void *workspace, size_t workspace_bytes, void *stream) {
+  AttnPlan p;
+  int rc = attn_plan(sh, &p);
+  if (rc) return rc;
+  if (sh->num_seqs == 0 || sh->total_q == 0) {
+    if (mask_mode != SD_MASK_CAUSAL_IN_BLOCK && mask_mode != SD_MASK_BIDIR_IN_BLOCK)
+      return fail(SD_ERR_INVALID_ARG, "unknown mask_mode %d", mask_mode);
+    return ok();
+  }
+  sdb::AttnArgs a;
+  rc = attn_args(sh, p, q, k_cache, v_cache, ctx_lens, block_lens, q_offsets, mask_mode, out, workspace,
+                 workspace_bytes, &a);
+  if (rc) return rc;
   const int grid = p.per_xcd * sdb::kNumXcd;
   hipStream_t st = (hipStream_t)stream;
   const bool bf = sh->dtype == SD_BF16;
@@ -325,6 +343,84 @@ int sd_block_attn(const sd_attn_shape *sh, const void *q, const void *k_cache, c
     else launch_attn_all<false, 64>(a, grid, p.MT, st);
   }
   return check_launch("sd_block_attn");
+}
+
+namespace {
+
+int check_pages(const sd_attn_shape *sh, int32_t page_size, int32_t num_pages, int32_t max_pages, int *log2) {
+  if (sh && sh->dtype != SD_BF16) return fail(SD_ERR_UNSUPPORTED, "paged caches are bf16 only");
+  if (page_size < 16 || page_size > 4096 || (page_size & (page_size - 1)))
+    return fail(SD_ERR_INVALID_ARG, "page_size must be a power of two in [16, 4096] (got %d)", page_size);
+  if (num_pages < 1 || max_pages < 1) return fail(SD_ERR_INVALID_ARG, "num_pages and max_pages must be >= 1");
+  if (sh && (long long)max_pages * page_size != sh->max_kv_len)
+    return fail(SD_ERR_INVALID_ARG, "max_kv_len (%d) must equal max_pages * page_size (%d * %d)", sh->max_kv_len,
+                max_pages, page_size);
+  int l = 0;
+  while ((1 << l) < page_size) ++l;
+  *log2 = l;
+  return ok();
+}
+
+}  // namespace
+
+int sd_block_attn_paged(const sd_attn_shape *sh, int32_t page_size, int32_t num_pages, int32_t max_pages,
+                        const int32_t *block_table, const void *q, const void *k_pages, const void *v_pages,
+                        const int32_t *ctx_lens, const int32_t *block_lens, const int32_t *q_offsets,
+                        int32_t mask_mode, void *out, void *workspace, size_t workspace_bytes, void *stream) {
+  AttnPlan p;
+  int rc = attn_plan(sh, &p);
+  if (rc) return rc;
+  int log2 = 0;
+  rc = check_pages(sh, page_size, num_pages, max_pages, &log2);
+  if (rc) return rc;
+  if (sh->num_seqs == 0 || sh->total_q == 0) return ok();
+  if (!block_table) return fail(SD_ERR_INVALID_ARG, "sd_block_attn_paged: block_table is NULL");
+  sdb::AttnArgs a;
+  rc = attn_args(sh, p, q, k_pages, v_pages, ctx_lens, block_lens, q_offsets, mask_mode, out, workspace,
+                 workspace_bytes, &a);
+  if (rc) return rc;
+  a.block_table = block_table;
+  a.page_log2 = log2;
+  a.max_pages = max_pages;
+  a.num_pages = num_pages;
+  const int grid = p.per_xcd * sdb::kNumXcd;
+  hipStream_t st = (hipStream_t)stream;
+  if (sh->head_dim == 128) launch_attn_all<true, 128, true>(a, grid, p.MT, st);
+  else launch_attn_all<true, 64, true>(a, grid, p.MT, st);
+  return check_launch("sd_block_attn_paged");
+}
+
+int sd_kv_append_paged(const sd_attn_shape *sh, int32_t page_size, int32_t num_pages, int32_t max_pages,
+                       const int32_t *block_table, const void *k_new, const void *v_new, void *k_pages, void *v_pages,
+                       const int32_t *ctx_lens, const int32_t *q_offsets, void *stream) {
+  int rc = check_cache_shape(sh, "sd_kv_append_paged");
+  if (rc) return rc;
+  int log2 = 0;
+  rc = check_pages(nullptr, page_size, num_pages, max_pages, &log2);
+  if (rc) return rc;
+  if (sh->num_seqs == 0 || sh->total_q == 0) return ok();
+  if (!k_new || !v_new || !k_pages || !v_pages || !ctx_lens || !q_offsets || !block_table)
+    return fail(SD_ERR_INVALID_ARG, "sd_kv_append_paged: NULL pointer argument");
+  if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(k_pages) || !aligned16(v_pages))
+    return fail(SD_ERR_INVALID_ARG, "new rows and page pools must be 16-byte aligned");
+  sdb::AppendArgs a;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.k_cache = k_pages;
+  a.v_cache = v_pages;
+  a.ctx_lens = ctx_lens;
+  a.q_offsets = q_offsets;
+  a.S = sh->num_seqs;
+  a.Hkv = sh->num_kv_heads;
+  a.Lmax = max_pages * page_size;
+  a.total_q = sh->total_q;
+  a.row_vecs = sh->head_dim * (sh->dtype == SD_BF16 ? 2 : 4) / 16;
+  a.block_table = block_table;
+  a.page_log2 = log2;
+  a.max_pages = max_pages;
+  a.num_pages = num_pages;
+  hipLaunchKernelGGL(sdb::kv_append_paged_kernel, dim3(sh->total_q, 2), dim3(256), 0, (hipStream_t)stream, a);
+  return check_launch("sd_kv_append_paged");
 }
 
 int sd_accept_workspace_size(const sd_accept_shape *shape, float temperature, size_t *bytes) {
@@ -432,6 +528,8 @@ int sd_kv_append(const sd_attn_shape *sh, const void *k_new, const void *v_new, 
   a.Lmax = sh->max_kv_len;
   a.total_q = sh->total_q;
   a.row_vecs = sh->head_dim * (sh->dtype == SD_BF16 ? 2 : 4) / 16;
+  a.block_table = nullptr;
+  a.page_log2 = a.max_pages = a.num_pages = 0;
   hipLaunchKernelGGL(sdb::kv_append_kernel, dim3(sh->total_q, 2), dim3(256), 0, (hipStream_t)stream, a);
   return check_launch("sd_kv_append");
 }

@@ -410,3 +410,29 @@ def make_policy(seed: int, *, P, V, H=2048, radius=2, base_block=16, dtype="bf16
     b2 = (g.standard_normal(H, dtype=np.float32) * np.float32(0.05)).astype(np.float32)
     b3 = (g.standard_normal(C, dtype=np.float32) * np.float32(0.05)).astype(np.float32)
     return PolicyProblem(logits, w1, b1, w2, b2, w3, b3, base_block, radius, dtype, name)
+
+
+# --------------------------------------------------------------------------- #
+# paged caches: the same keys and values scattered over a pool of pages
+# --------------------------------------------------------------------------- #
+
+def paginate(rs: dict, k_cache: torch.Tensor, v_cache: torch.Tensor, page_size: int, spare_pages: int = 3,
+             fill=float("nan")):
+    """Scatter contiguous caches [S, Hkv, Lmax, D] (Lmax a multiple of page_size) into pools
+    [num_pages, Hkv, page_size, D] in a seeded random page order, with ``spare_pages`` unused
+    pool pages holding ``fill``.  Returns (k_pages, v_pages, block_table [S, Lmax/page_size])."""
+    S, Hkv, Lmax, D = k_cache.shape
+    if Lmax % page_size:
+        raise ValueError("Lmax must be a multiple of page_size")
+    mp = Lmax // page_size
+    num_pages = S * mp + spare_pages
+    perm = rs["ctx"].permutation(num_pages)[:S * mp].astype(np.int32)
+    table = perm.reshape(S, mp)
+    kp = torch.full((num_pages, Hkv, page_size, D), fill, dtype=k_cache.dtype)
+    vp = torch.full((num_pages, Hkv, page_size, D), fill, dtype=v_cache.dtype)
+    kv = k_cache.reshape(S, Hkv, mp, page_size, D).permute(0, 2, 1, 3, 4)  # [S, mp, Hkv, ps, D]
+    vv = v_cache.reshape(S, Hkv, mp, page_size, D).permute(0, 2, 1, 3, 4)
+    idx = torch.from_numpy(table.reshape(-1).astype(np.int64))
+    kp[idx] = kv.reshape(S * mp, Hkv, page_size, D)
+    vp[idx] = vv.reshape(S * mp, Hkv, page_size, D)
+    return kp, vp, table
