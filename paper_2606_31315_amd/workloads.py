@@ -436,3 +436,38 @@ def paginate(rs: dict, k_cache: torch.Tensor, v_cache: torch.Tensor, page_size: 
     kp[idx] = kv.reshape(S * mp, Hkv, page_size, D)
     vp[idx] = vv.reshape(S * mp, Hkv, page_size, D)
     return kp, vp, table
+
+
+# --------------------------------------------------------------------------- #
+# prefix-survival model: per-sample, per-position predictability
+# --------------------------------------------------------------------------- #
+
+@dataclass
+class SurvivalProblem:
+    gamma: np.ndarray      # [N, P] fp32 in (0, 1]: predictability gamma_j(x) of drafted position j
+    cands: np.ndarray      # [C] int32, strictly ascending candidate block sizes (<= P)
+    train_block: int       # B, the drafter's training block size
+    alpha: float           # retention sharpness
+    b_hat: np.ndarray      # [N] int32: a predicted block size per sample, drawn from the candidates
+    name: str = ""
+
+    @property
+    def N(self) -> int:
+        return int(self.gamma.shape[0])
+
+    @property
+    def P(self) -> int:
+        return int(self.gamma.shape[1])
+
+
+def make_survival(seed: int, *, N, P=32, train_block=16, radius=2, alpha=0.01, gamma_lo=0.6, gamma_hi=0.97,
+                  jitter=0.03, name="") -> SurvivalProblem:
+    """Samples whose predictability is near-constant across positions: gamma_x ~ U(lo, hi) per
+    sample, gamma_j(x) = gamma_x + N(0, jitter^2) clipped to [0.01, 1]; candidates are the local
+    interval {B - k, ..., B + k}; b_hat is uniform over the candidates."""
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence(seed)))
+    base = g.uniform(gamma_lo, gamma_hi, size=(N, 1))
+    gamma = np.clip(base + jitter * g.standard_normal((N, P)), 0.01, 1.0).astype(np.float32)
+    cands = np.arange(train_block - radius, train_block + radius + 1, dtype=np.int32)
+    b_hat = g.choice(cands, size=N).astype(np.int32)
+    return SurvivalProblem(gamma, cands, int(train_block), float(alpha), b_hat, name)
