@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--verify-steps", type=int, default=20)
     ap.add_argument("--policy-prompts", type=int, default=1,
                     help="prompts of the block-size policy timed after the main measurement (0: skip)")
+    ap.add_argument("--survival-samples", type=int, default=1 << 20,
+                    help="samples of the prefix-survival model timed after the main measurement (0: skip)")
+    ap.add_argument("--survival-trials", type=int, default=1024)
     return ap.parse_args()
 
 
@@ -215,6 +218,58 @@ def policy_run(torch, sd, prompts, reps=20, V=151936, H=2048, radius=2, base_blo
                     "argmax; random bf16 weights"}
 
 
+def survival_run(torch, sd, N, trials, reps=20):
+    """The prefix-survival model over a synthetic population: tau(b; x) for the candidates
+    {14, ..., 18} around the training size 16 (alpha = 0.001), B*(x), the regret of a uniformly drawn
+    prediction and L_tau (sd_survival_tau), then the Monte-Carlo lengths of 2^16 samples
+    (sd_survival_sample)."""
+    from paper_2606_31315_amd import workloads as W
+    dev = torch.device("cuda:0")
+    p = W.make_survival(1006, N=N, P=32, train_block=16, radius=2, alpha=0.001)
+    g = torch.from_numpy(p.gamma).to(dev)
+    bh = torch.from_numpy(p.b_hat).to(dev)
+
+    def tau_call():
+        return sd.survival_tau(g, p.cands, p.train_block, p.alpha, bh)
+
+    for _ in range(3):
+        tau_call()
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(reps):
+        out = tau_call()
+    t1.record()
+    torch.cuda.synchronize()
+    us = t0.elapsed_time(t1) / reps * 1e3
+    tau, b_star, regret, lip = out
+    C = len(p.cands)
+    nbytes = N * (p.P * 4 + 4 + C * 8 + 4 + 8 + 8)
+    bs = b_star.cpu().numpy()
+    reg = regret.cpu().numpy()
+    bound = (lip * (b_star - bh).abs().double()).cpu().numpy()
+    Nmc = min(N, 1 << 16)
+    gmc = g[:Nmc].contiguous()
+    sd.survival_sample(gmc, p.cands, p.train_block, p.alpha, 1, trials, hist=False)
+    torch.cuda.synchronize()
+    t0.record()
+    mean, _ = sd.survival_sample(gmc, p.cands, p.train_block, p.alpha, 2, trials, hist=False)
+    t1.record()
+    torch.cuda.synchronize()
+    mc_us = t0.elapsed_time(t1) * 1e3
+    gap = (mean - tau[:Nmc]).abs().mean().item()
+    return {"samples": N, "candidates": [int(b) for b in p.cands], "tau_us_per_call": round(us, 1),
+            "tau_bytes": nbytes, "tau_gbps": round(nbytes / (us * 1e-6) / 1e9, 1),
+            "b_star_hist": {int(b): int((bs == b).sum()) for b in p.cands},
+            "mean_regret_uniform_prediction": round(float(reg.mean()), 4),
+            "regret_bound_holds": bool((reg <= bound + 1e-12).all()),
+            "mc_samples": Nmc, "mc_trials": trials, "mc_us": round(mc_us, 1),
+            "mc_trials_per_s": round(Nmc * C * trials / (mc_us * 1e-6), 1),
+            "mc_mean_abs_mean_minus_tau": round(gap, 4),
+            "what": "sd_survival_tau over 2^20 synthetic samples (gamma_x ~ U(0.6, 0.97), 32 positions); "
+                    "sd_survival_sample over the first 2^16, Philox4x64-10 draws"}
+
+
 def paged_run(torch, sd, a, bufs, page_size, reps, shuffle=True):
     """sd_block_attn_paged on the same keys and values as the timed step, scattered over a pool
     of page_size-key pages in a shuffled (or in-order) page order, one pool per input copy."""
@@ -366,6 +421,8 @@ def main():
     res["paged_attn_us"]["page_64_in_order"] = paged_run(torch, sd, a, bufs, 64, K, shuffle=False)
     if args.policy_prompts > 0:
         res["policy"] = policy_run(torch, sd, args.policy_prompts)
+    if args.survival_samples > 0:
+        res["survival"] = survival_run(torch, sd, args.survival_samples, args.survival_trials)
     if args.verify_layers > 0:
         res["verify_step"] = verify_step_run(torch, sd, work, T, args.verify_layers, args.verify_steps)
     if not args.no_cpu_baseline:

@@ -287,6 +287,55 @@ int sd_block_size_policy(const sd_policy_shape *shape, const void *last_logits, 
                          const void *w2, const float *b2, const void *w3, const float *b3, float *scores,
                          int32_t *block_size, void *workspace, size_t workspace_bytes, void *stream);
 
+
+/* ==========================================================================
+ * Prefix-survival model of the accepted length (App. A).  For a sample x, block size
+ * b and drafter training block size B:
+ *   q_j(x, b)   = gamma_j(x) r(b; B),  r(b; B) = exp(-alpha (b - B)^2)       (App. A.2)
+ *   tau(b; x)   = E[L_b(x)] = sum_{i=1..b} prod_{j=1..i} q_j(x, b)          (App. A.1)
+ *   B*(x)       = argmax of tau over the candidates (smallest b on ties)     (App. A.2)
+ *   R(x)        = tau(B*(x); x) - tau(B_hat(x); x)                           (App. A.3)
+ *   L_tau(x)    = max over candidate pairs of |tau(b1) - tau(b2)| / |b1 - b2|: the smallest
+ *                 constant of the discrete Lipschitz condition, so R(x) <= L_tau |B* - B_hat|.
+ * gamma_j(x) is the intrinsic predictability of drafted position j (App. A.2).  Arithmetic
+ * is fp64.  No workspace; nothing is allocated.
+ * ========================================================================== */
+typedef struct sd_survival_shape {
+  int32_t num_samples; /* N >= 0 */
+  int32_t max_pos;     /* P: positions per sample in gamma, 1..128 */
+  int32_t num_cands;   /* C: 1..64 */
+  int32_t train_block; /* B */
+  double alpha;        /* retention sharpness, finite and >= 0 */
+  int32_t cands[64];   /* host: the C candidate block sizes, strictly ascending, each in [1, P] */
+} sd_survival_shape;
+
+/*
+ *   gamma      [N, P] fp32 device, 16-byte aligned: gamma_j(x) of sample n at column j - 1
+ *   b_hat      [N] int32 device or NULL: a predicted block size per sample
+ *   tau        [N, C] fp64 device out: tau(cands[c]; x_n)
+ *   b_star     [N] int32 device out: B*(x_n)
+ *   regret     [N] fp64 device out (given exactly when b_hat is): R(x_n); NaN where b_hat[n]
+ *              is not a candidate
+ *   lipschitz  [N] fp64 device out or NULL: L_tau(x_n)
+ * Errors: SD_ERR_INVALID_ARG, SD_ERR_HIP.  N == 0 returns SD_OK without touching the device.
+ */
+int sd_survival_tau(const sd_survival_shape *shape, const float *gamma, const int32_t *b_hat, double *tau,
+                    int32_t *b_star, double *regret, double *lipschitz, void *stream);
+
+/*
+ * Monte Carlo of L_b(x): `trials` independent verification passes per (sample, candidate).
+ * Drafted position i (1-based) of trial t, candidate index c, sample n is accepted iff
+ * u < q_i(x, b), with u the top 53 bits over 2^53 of word (i-1) mod 4 of Philox4x64-10
+ * (Salmon et al., SC'11) under key (seed, 0) at counter ((i-1) div 4, t, c, n); L is the
+ * number of leading acceptances, so L <= b.  The draws depend on those indices only, not on
+ * the launch.
+ *   mean_len  [N, C] fp64 device out: (sum of L over the trials) / trials
+ *   len_hist  [N, C, P + 1] int32 device out or NULL: trials with L = 0..P
+ * trials in [1, 2^30].  Errors: SD_ERR_INVALID_ARG, SD_ERR_HIP.
+ */
+int sd_survival_sample(const sd_survival_shape *shape, const float *gamma, uint64_t seed, int32_t trials,
+                       double *mean_len, int32_t *len_hist, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -21,7 +21,7 @@ SD_MASK_CAUSAL_IN_BLOCK, SD_MASK_BIDIR_IN_BLOCK = 0, 1
 EXPORTS = ["sd_last_error", "sd_version", "sd_block_attn_workspace_size", "sd_block_attn",
            "sd_accept_workspace_size", "sd_accept", "sd_kv_append", "sd_commit", "sd_verify_step_workspace_size",
            "sd_verify_step", "sd_policy_workspace_size", "sd_block_size_policy", "sd_block_attn_paged",
-           "sd_kv_append_paged"]
+           "sd_kv_append_paged", "sd_survival_tau", "sd_survival_sample"]
 
 
 class SdAttnShape(ctypes.Structure):
@@ -39,6 +39,11 @@ class SdAcceptShape(ctypes.Structure):
 class SdPolicyShape(ctypes.Structure):
     _fields_ = [("num_prompts", ctypes.c_int32), ("vocab", ctypes.c_int32), ("hidden", ctypes.c_int32),
                 ("radius", ctypes.c_int32), ("base_block", ctypes.c_int32), ("logits_dtype", ctypes.c_int32)]
+
+
+class SdSurvivalShape(ctypes.Structure):
+    _fields_ = [("num_samples", ctypes.c_int32), ("max_pos", ctypes.c_int32), ("num_cands", ctypes.c_int32),
+                ("train_block", ctypes.c_int32), ("alpha", ctypes.c_double), ("cands", ctypes.c_int32 * 64)]
 
 
 class SdLayerBuffers(ctypes.Structure):
@@ -94,6 +99,10 @@ def lib() -> ctypes.CDLL:
         L.sd_verify_step.restype = ctypes.c_int
         L.sd_verify_step.argtypes = [ctypes.POINTER(SdAttnShape), I, ctypes.POINTER(SdLayerBuffers), P, P, P, I,
                                      ctypes.POINTER(SdAcceptShape), P, P, P, P, ctypes.c_float, P, P, P, Z, P]
+        L.sd_survival_tau.restype = ctypes.c_int
+        L.sd_survival_tau.argtypes = [ctypes.POINTER(SdSurvivalShape), P, P, P, P, P, P, P]
+        L.sd_survival_sample.restype = ctypes.c_int
+        L.sd_survival_sample.argtypes = [ctypes.POINTER(SdSurvivalShape), P, ctypes.c_uint64, I, P, P, P]
         _lib = L
     return _lib
 
@@ -384,6 +393,50 @@ def block_size_policy(last_logits: torch.Tensor, w1: torch.Tensor, b1: torch.Ten
                                       _ptr(w3), _ptr(b3), _ptr(scores), _ptr(block_size), _ptr(workspace),
                                       workspace.numel() * workspace.element_size(), _stream(stream)))
     return scores, block_size
+
+
+def survival_shape(gamma: torch.Tensor, cands, train_block: int, alpha: float) -> SdSurvivalShape:
+    cands = [int(b) for b in cands]
+    if not 1 <= len(cands) <= 64:
+        raise ValueError("between 1 and 64 candidates")
+    sh = SdSurvivalShape(gamma.shape[0], gamma.shape[1], len(cands), int(train_block), float(alpha))
+    for i, b in enumerate(cands):
+        sh.cands[i] = b
+    return sh
+
+
+def survival_tau(gamma: torch.Tensor, cands, train_block: int, alpha: float, b_hat: Optional[torch.Tensor] = None,
+                 *, lipschitz: bool = True, stream=None):
+    """Prefix-survival model (sd_survival_tau): gamma [N, P] fp32 -> (tau [N, C] fp64, B* [N] int32,
+    regret [N] fp64 or None, L_tau [N] fp64 or None)."""
+    dev = gamma.device
+    _need(gamma, "gamma", torch.float32)
+    if b_hat is not None:
+        _need(b_hat, "b_hat", torch.int32, dev)
+    shape = survival_shape(gamma, cands, train_block, alpha)
+    N, C = gamma.shape[0], shape.num_cands
+    tau = torch.empty(N, C, dtype=torch.float64, device=dev)
+    b_star = torch.empty(N, dtype=torch.int32, device=dev)
+    regret = torch.empty(N, dtype=torch.float64, device=dev) if b_hat is not None else None
+    lip = torch.empty(N, dtype=torch.float64, device=dev) if lipschitz else None
+    _check(lib().sd_survival_tau(ctypes.byref(shape), _ptr(gamma), _ptr(b_hat), _ptr(tau), _ptr(b_star), _ptr(regret),
+                                 _ptr(lip), _stream(stream)))
+    return tau, b_star, regret, lip
+
+
+def survival_sample(gamma: torch.Tensor, cands, train_block: int, alpha: float, seed: int, trials: int, *,
+                    hist: bool = True, stream=None):
+    """Monte Carlo of the accepted length (sd_survival_sample): -> (mean [N, C] fp64,
+    histogram [N, C, P + 1] int32 or None)."""
+    dev = gamma.device
+    _need(gamma, "gamma", torch.float32)
+    shape = survival_shape(gamma, cands, train_block, alpha)
+    N, P, C = gamma.shape[0], gamma.shape[1], shape.num_cands
+    mean = torch.empty(N, C, dtype=torch.float64, device=dev)
+    h = torch.empty(N, C, P + 1, dtype=torch.int32, device=dev) if hist else None
+    _check(lib().sd_survival_sample(ctypes.byref(shape), _ptr(gamma), ctypes.c_uint64(int(seed) % 2**64),
+                                    int(trials), _ptr(mean), _ptr(h), _stream(stream)))
+    return mean, h
 
 
 def version() -> str:

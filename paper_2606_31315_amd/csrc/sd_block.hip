@@ -17,6 +17,7 @@
 #include "kvstep.hpp"
 #include "policy.hpp"
 #include "sd_block.h"
+#include "survival.hpp"
 
 namespace {
 
@@ -647,6 +648,89 @@ int sd_block_size_policy(const sd_policy_shape *sh, const void *last_logits, con
   sdb::HeadArgs ha{(const uint16_t *)w3, h2, b3, scores, block_size, C, H, sh->base_block, sh->radius};
   hipLaunchKernelGGL(sdb::policy_head_kernel, dim3(P), dim3(256), 0, st, ha);
   return check_launch("sd_block_size_policy");
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// prefix-survival model (App. A)
+// ---------------------------------------------------------------------------
+namespace {
+
+int survival_check(const sd_survival_shape *sh, const float *gamma, sdb::SurvivalArgs *a) {
+  if (!sh) return fail(SD_ERR_INVALID_ARG, "survival: shape is NULL");
+  if (sh->num_samples < 0) return fail(SD_ERR_INVALID_ARG, "num_samples must be >= 0 (got %d)", sh->num_samples);
+  if (sh->max_pos < 1 || sh->max_pos > sdb::kSurvMaxPos)
+    return fail(SD_ERR_INVALID_ARG, "max_pos must be in [1, %d] (got %d)", sdb::kSurvMaxPos, sh->max_pos);
+  if (sh->num_cands < 1 || sh->num_cands > sdb::kSurvMaxCands)
+    return fail(SD_ERR_INVALID_ARG, "num_cands must be in [1, %d] (got %d)", sdb::kSurvMaxCands, sh->num_cands);
+  for (int c = 0; c < sh->num_cands; ++c) {
+    const int b = sh->cands[c];
+    if (b < 1 || b > sh->max_pos) return fail(SD_ERR_INVALID_ARG, "candidate %d (%d) outside [1, max_pos]", c, b);
+    if (c > 0 && b <= sh->cands[c - 1]) return fail(SD_ERR_INVALID_ARG, "candidates must be strictly ascending");
+  }
+  if (!(sh->alpha >= 0.0) || isinf(sh->alpha)) return fail(SD_ERR_INVALID_ARG, "alpha must be finite and >= 0");
+  if ((long long)sh->num_samples * sh->max_pos > (1LL << 31) - 1)
+    return fail(SD_ERR_INVALID_ARG, "num_samples * max_pos exceeds 2^31 - 1");
+  if (sh->num_samples > 0 && !gamma) return fail(SD_ERR_INVALID_ARG, "gamma is NULL");
+  if (gamma && !aligned16(gamma)) return fail(SD_ERR_INVALID_ARG, "gamma must be 16-byte aligned");
+  memset(a, 0, sizeof *a);
+  a->gamma = gamma;
+  a->N = sh->num_samples;
+  a->P = sh->max_pos;
+  a->C = sh->num_cands;
+  a->train_block = sh->train_block;
+  a->alpha = sh->alpha;
+  for (int c = 0; c < sh->num_cands; ++c) a->cands[c] = sh->cands[c];
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int sd_survival_tau(const sd_survival_shape *sh, const float *gamma, const int32_t *b_hat, double *tau,
+                    int32_t *b_star, double *regret, double *lipschitz, void *stream) {
+  sdb::SurvivalArgs a;
+  int rc = survival_check(sh, gamma, &a);
+  if (rc) return rc;
+  if (!b_hat != !regret) return fail(SD_ERR_INVALID_ARG, "b_hat and regret must both be given or both be NULL");
+  if (a.N == 0) return ok();
+  if (!tau || !b_star) return fail(SD_ERR_INVALID_ARG, "sd_survival_tau: NULL output");
+  a.b_hat = b_hat;
+  a.tau = tau;
+  a.b_star = b_star;
+  a.regret = regret;
+  a.lipschitz = lipschitz;
+  // samples per workgroup: the most of 256, 128, 64 whose staged rows fit the LDS budget
+  const size_t row_bytes = (size_t)(a.P + 1) * sizeof(float), fixed = sdb::kSurvMaxCands * sizeof(double);
+  int spw = 256;
+  while (spw > 64 && fixed + spw * row_bytes > (size_t)sdb::kSurvLdsBytes) spw /= 2;
+  const size_t lds = fixed + spw * row_bytes;
+  const int grid = (a.N + spw - 1) / spw;
+  hipLaunchKernelGGL(sdb::survival_tau_kernel, dim3(grid), dim3(spw), lds, (hipStream_t)stream, a);
+  return check_launch("sd_survival_tau");
+}
+
+int sd_survival_sample(const sd_survival_shape *sh, const float *gamma, uint64_t seed, int32_t trials,
+                       double *mean_len, int32_t *len_hist, void *stream) {
+  sdb::SurvivalArgs a;
+  int rc = survival_check(sh, gamma, &a);
+  if (rc) return rc;
+  if (trials < 1 || trials > (1 << 30)) return fail(SD_ERR_INVALID_ARG, "trials must be in [1, 2^30] (got %d)", trials);
+  if (a.N == 0) return ok();
+  if (!mean_len) return fail(SD_ERR_INVALID_ARG, "sd_survival_sample: mean_len is NULL");
+  a.seed = seed;
+  a.trials = trials;
+  a.mean_len = mean_len;
+  a.len_hist = len_hist;
+  const long long pairs = (long long)a.N * a.C;
+  const long long grid = (pairs + sdb::kSurvWavesPerWg - 1) / sdb::kSurvWavesPerWg;
+  if (grid > 0x7fffffffLL) return fail(SD_ERR_INVALID_ARG, "num_samples * num_cands too large");
+  const size_t lds = (size_t)sdb::kSurvWavesPerWg * (a.P + (a.P + 2) / 2) * sizeof(double);
+  hipLaunchKernelGGL(sdb::survival_sample_kernel, dim3((unsigned)grid), dim3(64 * sdb::kSurvWavesPerWg), lds,
+                     (hipStream_t)stream, a);
+  return check_launch("sd_survival_sample");
 }
 
 }  // extern "C"

@@ -159,3 +159,56 @@ def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
     monkeypatch.setattr(L, "_lib", None)
     with pytest.raises(RuntimeError, match="missing"):
         L.lib()
+
+
+def good_survival_shape(**kw):
+    sh = L.SdSurvivalShape(num_samples=100, max_pos=32, num_cands=5, train_block=16, alpha=0.01)
+    for i, b in enumerate([14, 15, 16, 17, 18]):
+        sh.cands[i] = b
+    for k, v in kw.items():
+        setattr(sh, k, v)
+    return sh
+
+
+def call_survival_tau(sh, gamma=4096, b_hat=0, regret=0, tau=8192, b_star=16384, lip=0):
+    P = ctypes.c_void_p
+    return L.lib().sd_survival_tau(ctypes.byref(sh) if sh is not None else None, P(gamma), P(b_hat), P(tau),
+                                   P(b_star), P(regret), P(lip), None)
+
+
+def call_survival_sample(sh, gamma=4096, trials=100, mean=8192, hist=0):
+    P = ctypes.c_void_p
+    return L.lib().sd_survival_sample(ctypes.byref(sh), P(gamma), ctypes.c_uint64(1), trials, P(mean), P(hist), None)
+
+
+@pytest.mark.parametrize("field,value", [
+    ("num_samples", -1), ("max_pos", 0), ("max_pos", 129), ("num_cands", 0), ("num_cands", 65),
+    ("alpha", -0.5), ("alpha", float("inf")), ("alpha", float("nan")),
+])
+def test_survival_shape_errors(field, value):
+    sh = good_survival_shape(**{field: value})
+    assert call_survival_tau(sh) == L.SD_ERR_INVALID_ARG
+    assert call_survival_sample(sh) == L.SD_ERR_INVALID_ARG
+    assert L.lib().sd_last_error().decode()
+
+
+def test_survival_call_errors_without_device():
+    assert call_survival_tau(None) == L.SD_ERR_INVALID_ARG
+    sh = good_survival_shape()
+    sh.cands[2] = 15                                                   # not strictly ascending
+    assert call_survival_tau(sh) == L.SD_ERR_INVALID_ARG
+    sh = good_survival_shape()
+    sh.cands[4] = 33                                                   # past max_pos
+    assert call_survival_tau(sh) == L.SD_ERR_INVALID_ARG
+    sh = good_survival_shape()
+    assert call_survival_tau(sh, gamma=0) == L.SD_ERR_INVALID_ARG
+    assert call_survival_tau(sh, gamma=4100) == L.SD_ERR_INVALID_ARG   # misaligned
+    assert call_survival_tau(sh, b_hat=64) == L.SD_ERR_INVALID_ARG     # b_hat without regret
+    assert call_survival_tau(sh, regret=64) == L.SD_ERR_INVALID_ARG    # regret without b_hat
+    assert call_survival_tau(sh, tau=0) == L.SD_ERR_INVALID_ARG
+    assert call_survival_sample(sh, trials=0) == L.SD_ERR_INVALID_ARG
+    assert call_survival_sample(sh, trials=(1 << 30) + 1) == L.SD_ERR_INVALID_ARG
+    assert call_survival_sample(sh, mean=0) == L.SD_ERR_INVALID_ARG
+    # no samples: nothing to do, no device work
+    assert call_survival_tau(good_survival_shape(num_samples=0), gamma=0) == L.SD_OK
+    assert call_survival_sample(good_survival_shape(num_samples=0), gamma=0) == L.SD_OK

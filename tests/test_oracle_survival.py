@@ -147,7 +147,18 @@ def check_monte_carlo(S):
     assert (np.abs(surv - pref) <= 4 * np.sqrt(pref * (1 - pref) / trials) + 1e-9).all()
 
 
-PINS = [check_philox, check_enumeration, check_distribution_mean, check_geometric, check_certain_positions,
+def check_never_below_training_size(S):
+    """Shorter blocks than B lose both terms and retention (r <= 1 = r(B; B)), so with B among
+    the candidates B* >= B for every sample."""
+    for seed, alpha in ((24, 0.001), (25, 0.02), (26, 0.3)):
+        p = W.make_survival(seed, N=40, P=32, train_block=16, radius=4, alpha=alpha, gamma_lo=0.3, gamma_hi=1.0,
+                            jitter=0.2)
+        r = S.survival_tau(p.gamma, p.cands, p.train_block, p.alpha)
+        assert (r.b_star >= 16).all()
+        assert (r.tau[:, :4] <= r.tau[:, 4:5]).all()
+
+
+PINS = [check_never_below_training_size, check_philox, check_enumeration, check_distribution_mean, check_geometric, check_certain_positions,
         check_argmax_cases, check_regret, check_monte_carlo]
 
 
