@@ -7,8 +7,9 @@
 //   * 8 wavefronts; wavefront w owns m-tiles w, w+8 (so up to 128 query rows per
 //     m-tile slot).
 //   * K and V tiles (64 keys each) are fetched with global_load_lds_dwordx4 straight
-//     into a 4-stage LDS ring (128 KB at D = 128): three tiles stay in flight while one
-//     is consumed, and no VGPRs hold data in transit.  One barrier per tile.
+//     into an LDS ring of NS stages (3 by default, 96 KB at D = 128): NS-1 tiles stay in
+//     flight while one is consumed, and no VGPRs hold data in transit.  One barrier per
+//     tile.
 //   * Rows in LDS are XOR-swizzled at 16-byte granularity (the swizzle is applied to
 //     the global address each lane fetches, since a load-to-LDS instruction writes 1 KB
 //     contiguously): K rows by (row mod 16) so the 16 rows an MFMA A-operand read

@@ -62,15 +62,25 @@ __global__ __launch_bounds__(256) void survival_tau_kernel(SurvivalArgs a) {
   const float *src = a.gamma + n0 * P;
   const int total = rows * P;
   if ((P & 3) == 0) {
+    // batches of 8 vectors per thread, every load of a batch issued before any LDS store
     const float4 *s4 = reinterpret_cast<const float4 *>(src);
-    for (int v = tid; v < total / 4; v += spw) {
-      const float4 x = s4[v];
-      const int e = 4 * v, row = e / P, col = e % P;  // P % 4 == 0: the 4 floats share a row
-      float *d = lds + row * stride + col;
-      d[0] = x.x;
-      d[1] = x.y;
-      d[2] = x.z;
-      d[3] = x.w;
+    const int nvec = total / 4;
+    for (int v0 = tid; v0 < nvec; v0 += 8 * spw) {
+      float4 x[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) x[k] = s4[min(v0 + k * spw, nvec - 1)];  // clamped: no per-load branch
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int v = v0 + k * spw;
+        if (v < nvec) {
+          const int e = 4 * v, row = e / P, col = e % P;  // P % 4 == 0: the 4 floats share a row
+          float *d = lds + row * stride + col;
+          d[0] = x[k].x;
+          d[1] = x[k].y;
+          d[2] = x[k].z;
+          d[3] = x[k].w;
+        }
+      }
     }
   } else {
     for (int e = tid; e < total; e += spw) lds[(e / P) * stride + e % P] = src[e];
