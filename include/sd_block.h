@@ -278,7 +278,7 @@ int sd_policy_workspace_size(const sd_policy_shape *shape, size_t *bytes);
  *   b1 [H], b2 [H], b3 [2k+1]            fp32
  *   scores       [P, 2k+1]  fp32 out: o
  *   block_size   [P] int32 out
- * p and the layer activations are fp32; products accumulate in fp32.  Logits and w1, w2
+ * p and the layer activations are fp32; products accumulate in fp32.  Logits and w1, w2, w3
  * 16-byte aligned; workspace 256-byte aligned, >= sd_policy_workspace_size().
  * Errors: SD_ERR_INVALID_ARG, SD_ERR_UNSUPPORTED (vocab or hidden not a multiple of 8),
  * SD_ERR_WORKSPACE, SD_ERR_HIP.  P == 0 returns SD_OK without touching the device.

@@ -220,7 +220,7 @@ int check_cache_shape(const sd_attn_shape *sh, const char *what) {
 }
 
 struct PolicyPlan {
-  size_t off_stats, off_prob, off_h1, off_h2, total;
+  size_t off_stats, off_h1, off_h2, total;
 };
 
 int policy_plan(const sd_policy_shape *sh, PolicyPlan *p) {
@@ -241,8 +241,6 @@ int policy_plan(const sd_policy_shape *sh, PolicyPlan *p) {
   size_t off = 0;
   p->off_stats = off;
   off = align256(off + P * sdb::kPolicyChunks * sizeof(float2));
-  p->off_prob = off;
-  off = align256(off + P * sh->vocab * sizeof(float));
   p->off_h1 = off;
   off = align256(off + P * sh->hidden * sizeof(float));
   p->off_h2 = off;
@@ -251,13 +249,13 @@ int policy_plan(const sd_policy_shape *sh, PolicyPlan *p) {
   return ok();
 }
 
-template <bool RELU>
+template <bool RELU, int XM>
 void launch_dense(const sdb::DenseArgs &d, hipStream_t st) {
   const dim3 grid((d.rows + sdb::kDenseRows - 1) / sdb::kDenseRows);
-  if (d.P <= 1) hipLaunchKernelGGL((sdb::policy_dense_kernel<1, RELU>), grid, dim3(256), 0, st, d);
-  else if (d.P <= 2) hipLaunchKernelGGL((sdb::policy_dense_kernel<2, RELU>), grid, dim3(256), 0, st, d);
-  else if (d.P <= 4) hipLaunchKernelGGL((sdb::policy_dense_kernel<4, RELU>), grid, dim3(256), 0, st, d);
-  else hipLaunchKernelGGL((sdb::policy_dense_kernel<8, RELU>), grid, dim3(256), 0, st, d);
+  if (d.P <= 1) hipLaunchKernelGGL((sdb::policy_dense_kernel<1, RELU, XM>), grid, dim3(256), 0, st, d);
+  else if (d.P <= 2) hipLaunchKernelGGL((sdb::policy_dense_kernel<2, RELU, XM>), grid, dim3(256), 0, st, d);
+  else if (d.P <= 4) hipLaunchKernelGGL((sdb::policy_dense_kernel<4, RELU, XM>), grid, dim3(256), 0, st, d);
+  else hipLaunchKernelGGL((sdb::policy_dense_kernel<8, RELU, XM>), grid, dim3(256), 0, st, d);
 }
 
 }  // namespace
@@ -616,7 +614,7 @@ int sd_block_size_policy(const sd_policy_shape *sh, const void *last_logits, con
   if (sh->num_prompts == 0) return ok();
   if (!last_logits || !w1 || !b1 || !w2 || !b2 || !w3 || !b3 || !scores || !block_size || !workspace)
     return fail(SD_ERR_INVALID_ARG, "sd_block_size_policy: NULL pointer argument");
-  if (!aligned16(w1) || !aligned16(w2) || !aligned16(last_logits))
+  if (!aligned16(w1) || !aligned16(w2) || !aligned16(w3) || !aligned16(last_logits))
     return fail(SD_ERR_INVALID_ARG, "logits and weights must be 16-byte aligned");
   if (((uintptr_t)workspace & 255u) != 0) return fail(SD_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
   if (workspace_bytes < p.total)
@@ -627,26 +625,24 @@ int sd_block_size_policy(const sd_policy_shape *sh, const void *last_logits, con
   sdb::PolicyArgs pa;
   pa.logits = last_logits;
   pa.stats = (float2 *)(ws + p.off_stats);
-  pa.prob = (float *)(ws + p.off_prob);
   pa.P = P;
   pa.V = V;
   pa.logits_bf16 = sh->logits_dtype == SD_BF16;
   const dim3 gsoft(P * sdb::kPolicyChunks);
-  if (pa.logits_bf16) {
-    hipLaunchKernelGGL(sdb::policy_stats_kernel<true>, gsoft, dim3(256), 0, st, pa);
-    hipLaunchKernelGGL(sdb::policy_prob_kernel<true>, gsoft, dim3(256), 0, st, pa);
-  } else {
-    hipLaunchKernelGGL(sdb::policy_stats_kernel<false>, gsoft, dim3(256), 0, st, pa);
-    hipLaunchKernelGGL(sdb::policy_prob_kernel<false>, gsoft, dim3(256), 0, st, pa);
-  }
+  if (pa.logits_bf16) hipLaunchKernelGGL(sdb::policy_stats_kernel<true>, gsoft, dim3(256), 0, st, pa);
+  else hipLaunchKernelGGL(sdb::policy_stats_kernel<false>, gsoft, dim3(256), 0, st, pa);
   float *h1 = (float *)(ws + p.off_h1), *h2 = (float *)(ws + p.off_h2);
-  // dense layers in groups of kPolicyMaxPrompts prompts (each group reads the weights once)
+  // dense layers in groups of kPolicyMaxPrompts prompts (each group reads the weights once);
+  // the first takes the logits and makes p = softmax(z) from the chunk records on the fly
+  const size_t zb = pa.logits_bf16 ? 2 : 4;
   for (int g0 = 0; g0 < P; g0 += sdb::kPolicyMaxPrompts) {
     const int np = std::min(sdb::kPolicyMaxPrompts, P - g0);
-    sdb::DenseArgs d1{(const uint16_t *)w1, pa.prob + (size_t)g0 * V, b1, h1 + (size_t)g0 * H, H, V, np};
-    launch_dense<true>(d1, st);
-    sdb::DenseArgs d2{(const uint16_t *)w2, h1 + (size_t)g0 * H, b2, h2 + (size_t)g0 * H, H, H, np};
-    launch_dense<true>(d2, st);
+    sdb::DenseArgs d1{(const uint16_t *)w1, (const char *)last_logits + (size_t)g0 * V * zb, b1,
+                      h1 + (size_t)g0 * H, H, V, np, pa.stats + (size_t)g0 * sdb::kPolicyChunks};
+    if (pa.logits_bf16) launch_dense<true, 1>(d1, st);
+    else launch_dense<true, 2>(d1, st);
+    sdb::DenseArgs d2{(const uint16_t *)w2, h1 + (size_t)g0 * H, b2, h2 + (size_t)g0 * H, H, H, np, nullptr};
+    launch_dense<true, 0>(d2, st);
   }
   sdb::HeadArgs ha{(const uint16_t *)w3, h2, b3, scores, block_size, C, H, sh->base_block, sh->radius};
   hipLaunchKernelGGL(sdb::policy_head_kernel, dim3(P), dim3(256), 0, st, ha);
