@@ -30,31 +30,49 @@ struct AppendArgs {
   int page_log2, max_pages, num_pages;
 };
 
-// Largest s with off[s] <= r (r < off[S]): the sequence that owns packed row r.
-__device__ __forceinline__ int row_owner(const int *off, int S, int r) {
-  int lo = 0, hi = S - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (ld_uniform(off, mid) <= r) lo = mid; else hi = mid - 1;
+// The sequence s that owns packed row r (the largest s with off[s] <= r; r < off[S]) and the
+// row's cache position ctx[s] + r - off[s], in every lane of the wavefront.  Lane k loads
+// off[k] and ctx[k] together, so one round of loads (64 sequences per round) settles both;
+// offsets ascend, so the first round that has a lane past r is the last one needed.
+__device__ __forceinline__ void row_owner_pos(const int *off, const int *ctx, int S, int r, int &s_out,
+                                              int &pos_out) {
+  const int lane = threadIdx.x & 63;
+  int s = 0, pos = 0;
+  for (int k0 = 0; k0 < S; k0 += 64) {
+    const int k = min(k0 + lane, S - 1);  // clamped: no per-load branch
+    const int o = off[k], c = ctx[k];
+    const unsigned long long valid = __ballot(k0 + lane < S);
+    const unsigned long long le = __ballot(k0 + lane < S && o <= r);
+    if (le) {
+      const int last = 63 - __clzll((long long)le);
+      s = k0 + last;
+      pos = __shfl(c, last, 64) + (r - __shfl(o, last, 64));
+    }
+    if (le != valid) break;
   }
-  return lo;
+  s_out = s;
+  pos_out = pos;
 }
 
 // grid = (total_q, 2): block (r, kv) copies token row r of K (kv = 0) or V (kv = 1) for every
-// kv head; threads stride over the Hkv * row_vecs 16-byte vectors.  A destination row at or
-// past Lmax (a ctx_len beyond the cache) is skipped rather than written out of bounds.
+// kv head; threads stride over the Hkv * row_vecs 16-byte vectors.  The first vectors are
+// loaded before the owner lookup (they do not depend on it), so the copy costs one round of
+// loads.  A destination row at or past Lmax (a ctx_len beyond the cache) is skipped rather
+// than written out of bounds.
 __global__ __launch_bounds__(256) void kv_append_kernel(AppendArgs a) {
   const int r = blockIdx.x;
   const int kv = blockIdx.y;
-  const int s = row_owner(a.q_offsets, a.S, r);
-  const int pos = ld_uniform(a.ctx_lens, s) + (r - ld_uniform(a.q_offsets, s));
-  if (pos < 0 || pos >= a.Lmax) return;
-  const u32x4 *src = reinterpret_cast<const u32x4 *>(kv ? a.v_new : a.k_new) + (size_t)r * a.Hkv * a.row_vecs;
-  u32x4 *dst = reinterpret_cast<u32x4 *>(kv ? a.v_cache : a.k_cache);
   const int n = a.Hkv * a.row_vecs;
-  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+  const u32x4 *src = reinterpret_cast<const u32x4 *>(kv ? a.v_new : a.k_new) + (size_t)r * n;
+  const int i0 = threadIdx.x;
+  const u32x4 first = src[min(i0, n - 1)];
+  int s, pos;
+  row_owner_pos(a.q_offsets, a.ctx_lens, a.S, r, s, pos);
+  if (pos < 0 || pos >= a.Lmax) return;
+  u32x4 *dst = reinterpret_cast<u32x4 *>(kv ? a.v_cache : a.k_cache);
+  for (int i = i0; i < n; i += blockDim.x) {
     const int h = i / a.row_vecs, c = i - h * a.row_vecs;
-    dst[(((size_t)s * a.Hkv + h) * a.Lmax + pos) * a.row_vecs + c] = src[i];
+    dst[(((size_t)s * a.Hkv + h) * a.Lmax + pos) * a.row_vecs + c] = (i == i0) ? first : src[i];
   }
 }
 
@@ -63,18 +81,20 @@ __global__ __launch_bounds__(256) void kv_append_kernel(AppendArgs a) {
 __global__ __launch_bounds__(256) void kv_append_paged_kernel(AppendArgs a) {
   const int r = blockIdx.x;
   const int kv = blockIdx.y;
-  const int s = row_owner(a.q_offsets, a.S, r);
-  const int pos = ld_uniform(a.ctx_lens, s) + (r - ld_uniform(a.q_offsets, s));
+  const int n = a.Hkv * a.row_vecs;
+  const u32x4 *src = reinterpret_cast<const u32x4 *>(kv ? a.v_new : a.k_new) + (size_t)r * n;
+  const int i0 = threadIdx.x;
+  const u32x4 first = src[min(i0, n - 1)];
+  int s, pos;
+  row_owner_pos(a.q_offsets, a.ctx_lens, a.S, r, s, pos);
   if (pos < 0 || pos >= a.Lmax) return;
   const int pg = ld_uniform(a.block_table, (long long)s * a.max_pages + (pos >> a.page_log2));
   if (pg < 0 || pg >= a.num_pages) return;
   const size_t row0 = (((size_t)pg * a.Hkv) << a.page_log2) + (pos & ((1 << a.page_log2) - 1));
-  const u32x4 *src = reinterpret_cast<const u32x4 *>(kv ? a.v_new : a.k_new) + (size_t)r * a.Hkv * a.row_vecs;
   u32x4 *dst = reinterpret_cast<u32x4 *>(kv ? a.v_cache : a.k_cache);
-  const int n = a.Hkv * a.row_vecs;
-  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+  for (int i = i0; i < n; i += blockDim.x) {
     const int h = i / a.row_vecs, c = i - h * a.row_vecs;
-    dst[(row0 + ((size_t)h << a.page_log2)) * a.row_vecs + c] = src[i];
+    dst[(row0 + ((size_t)h << a.page_log2)) * a.row_vecs + c] = (i == i0) ? first : src[i];
   }
 }
 
