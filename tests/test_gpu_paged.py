@@ -70,3 +70,25 @@ def test_kv_append_paged_bit_exact(page_size):
     rk, rv = OPG.kv_append_paged(kp, vp, table, blk["k_new"], blk["v_new"], ctx, off)
     assert np.array_equal(dkp.float().cpu().numpy(), rk, equal_nan=True)
     assert np.array_equal(dvp.float().cpu().numpy(), rv, equal_nan=True)
+
+
+def test_kv_append_paged_many_sequences():
+    """70 sequences: the owner lookup crosses a 64-sequence round, with empty blocks at its edge."""
+    rs = W._streams(5402)
+    S, Lmax = 70, 48
+    ctx = rs["ctx"].integers(0, 40, S).astype(np.int32)
+    B = rs["B"].integers(0, 6, S).astype(np.int32)
+    B[[62, 63, 64, 69]] = [0, 0, 3, 0]
+    off = W.offsets_from_lens(B)
+    k, v = W.step_caches(rs, S=S, Hkv=8, D=128, Lmax=Lmax, ctx_lens=ctx, dtype="bf16")
+    kp, vp, table = W.paginate(rs, k, v, 16)
+    blk = W.step_block_inputs(rs, total_q=int(off[-1]), Hq=8, Hkv=8, D=128, dtype="bf16")
+    dev = G.dev()
+    dkp, dvp = kp.to(dev), vp.to(dev)
+    G.log(f"sd_kv_append_paged S={S} page=16")
+    sd.kv_append_paged(blk["k_new"].to(dev), blk["v_new"].to(dev), dkp, dvp, torch.from_numpy(table).to(dev),
+                       torch.from_numpy(ctx).to(dev), torch.from_numpy(off).to(dev))
+    torch.cuda.synchronize()
+    rk, rv = OPG.kv_append_paged(kp, vp, table, blk["k_new"], blk["v_new"], ctx, off)
+    assert np.array_equal(dkp.float().cpu().numpy(), rk, equal_nan=True)
+    assert np.array_equal(dvp.float().cpu().numpy(), rv, equal_nan=True)

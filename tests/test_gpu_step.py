@@ -39,6 +39,28 @@ def test_kv_append_bit_exact(dtype, D):
     assert _same(dv, rv)
 
 
+def test_kv_append_many_sequences_and_wide_rows():
+    """150 sequences (the owner lookup takes 64 sequences per round), empty blocks on both
+    sides of each round's edge, and rows of 32 heads x 128 fp32 (more 16-byte vectors per
+    row than threads in the copying workgroup)."""
+    rs = W._streams(4103)
+    S, Hkv, D, Lmax = 150, 32, 128, 48
+    ctx = rs["ctx"].integers(0, 40, S).astype(np.int32)
+    B = rs["B"].integers(0, 6, S).astype(np.int32)
+    B[[0, 62, 63, 64, 65, 127, 128, 149]] = [3, 0, 0, 0, 2, 0, 4, 0]
+    off = W.offsets_from_lens(B)
+    k, v = W.step_caches(rs, S=S, Hkv=Hkv, D=D, Lmax=Lmax, ctx_lens=ctx, dtype="f32")
+    blk = W.step_block_inputs(rs, total_q=int(off[-1]), Hq=Hkv, Hkv=Hkv, D=D, dtype="f32")
+    dk, dv = k.to(G.dev()), v.to(G.dev())
+    G.log(f"sd_kv_append S={S} Hkv={Hkv} D={D} f32 total_q={int(off[-1])}")
+    sd.kv_append(blk["k_new"].to(G.dev()), blk["v_new"].to(G.dev()), dk, dv, torch.from_numpy(ctx).to(G.dev()),
+                 torch.from_numpy(off).to(G.dev()))
+    torch.cuda.synchronize()
+    rk, rv = OS.kv_append(k, v, blk["k_new"], blk["v_new"], ctx, off)
+    assert _same(dk, rk)
+    assert _same(dv, rv)
+
+
 def test_kv_append_skips_rows_past_capacity():
     rs = W._streams(4102)
     ctx = np.array([30, 31], np.int32)
