@@ -47,6 +47,8 @@ def parse():
     ap.add_argument("--survival-samples", type=int, default=1 << 20,
                     help="samples of the prefix-survival model timed after the main measurement (0: skip)")
     ap.add_argument("--survival-trials", type=int, default=1024)
+    ap.add_argument("--no-other-configs", dest="other_configs", action="store_false",
+                    help="skip the drafter and long-context timings after the main measurement")
     return ap.parse_args()
 
 
@@ -270,6 +272,71 @@ def survival_run(torch, sd, N, trials, reps=20):
                     "sd_survival_sample over the first 2^16, Philox4x64-10 draws"}
 
 
+def other_configs_run(torch, sd, reps=20):
+    """The drafter pass (16 sequences, ctx U{1024..8192}, B U{8..32}, bidirectional) and the
+    long-context serving step (32 sequences, ctx U{8192..32768}, B U{4..32}, causal attention,
+    then acceptance at T = 1 over V = 151936), with the seeded lengths of those workloads and
+    random bf16 values generated on the device.  Per-call times and algorithmic GB/s."""
+    from paper_2606_31315_amd import workloads as W
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev).manual_seed(17)
+    Hq, Hkv, D, V = 32, 8, 128, 151936
+    out = {}
+
+    def timed(fn, n):
+        fn()
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for i in range(n):
+            fn(i)
+        t1.record()
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / n * 1e3
+
+    for name, (ctx, B), mask, Lmax, copies in (
+            ("drafter_bidir_S16_ctx1k-8k_B8-32", W.c4_lens(), 1, 8192 + 32, 3),
+            ("qwen3_8b_long_S32_ctx8k-32k_B4-32", W.c5_lens(), 0, 32768 + 32, 1)):
+        S = len(ctx)
+        off = np.concatenate([[0], np.cumsum(B)]).astype(np.int32)
+        tq = int(off[-1])
+        bufs = [dict(q=torch.randn(tq, Hq, D, device=dev, generator=g).to(torch.bfloat16),
+                     k=torch.randn(S, Hkv, Lmax, D, device=dev, generator=g).to(torch.bfloat16),
+                     v=torch.randn(S, Hkv, Lmax, D, device=dev, generator=g).to(torch.bfloat16)) for _ in range(copies)]
+        o = torch.empty_like(bufs[0]["q"])
+        dc, db, do = (torch.from_numpy(x).to(dev) for x in (ctx, B, off))
+        mc, mb = int(ctx.max()), int(B.max())
+
+        def attn(i=0):
+            b = bufs[i % copies]
+            sd.block_attn(b["q"], b["k"], b["v"], dc, db, do, mask, max_ctx=mc, max_block=mb, out=o)
+
+        us = timed(attn, reps)
+        nbytes = int(((ctx + B).astype(np.int64) * Hkv * D * 2 * 2).sum() + 2 * tq * Hq * D * 2)
+        rec = {"num_seqs": S, "mask": "bidirectional_in_block" if mask else "causal_in_block",
+               "attn_us": round(us, 1), "attn_bytes": nbytes, "attn_gbps": round(nbytes / (us * 1e-6) / 1e9, 1)}
+        del bufs
+        if mask == 0:
+            t_ = (torch.randn(tq, V, device=dev, generator=g) * 3).to(torch.bfloat16)
+            d_ = (t_[:tq - S].float() + torch.randn(tq - S, V, device=dev, generator=g)).to(torch.bfloat16)
+            tok = torch.randint(0, V, (tq - S,), device=dev, generator=g, dtype=torch.int32)
+            u = torch.rand(tq, device=dev, generator=g)
+            al = torch.empty(S, dtype=torch.int32, device=dev)
+            nt = torch.empty(S, dtype=torch.int32, device=dev)
+
+            def acc(i=0):
+                sd.accept(t_, d_, tok, u, db, do, 1.0, max_block=mb, accept_len=al, next_token=nt)
+
+            aus = timed(acc, reps)
+            abytes = (2 * tq - S) * V * 2
+            rec.update({"accept_us": round(aus, 1), "accept_bytes": abytes,
+                        "accept_gbps": round(abytes / (aus * 1e-6) / 1e9, 1)})
+            del t_, d_
+        out[name] = rec
+        torch.cuda.empty_cache()
+    return out
+
+
 def paged_run(torch, sd, a, bufs, page_size, reps, shuffle=True):
     """sd_block_attn_paged on the same keys and values as the timed step, scattered over a pool
     of page_size-key pages in a shuffled (or in-order) page order, one pool per input copy."""
@@ -421,6 +488,8 @@ def main():
     res["paged_attn_us"]["page_64_in_order"] = paged_run(torch, sd, a, bufs, 64, K, shuffle=False)
     if args.policy_prompts > 0:
         res["policy"] = policy_run(torch, sd, args.policy_prompts)
+    if args.other_configs:
+        res["other_configs"] = other_configs_run(torch, sd)
     if args.survival_samples > 0:
         res["survival"] = survival_run(torch, sd, args.survival_samples, args.survival_trials)
     if args.verify_layers > 0:

@@ -40,11 +40,13 @@ struct AttnArgs {
   float *part_o;      // [n_work, Mpad, D] unnormalised partial outputs
   float2 *part_ml;    // [n_work, Mpad]    (row max in log2 units, row sum)
   int S, Hq, Hkv, G, Lmax;
-  int split_len;      // keys per split, multiple of the key tile
+  int split_len;      // longest split (keys), a multiple of gran
+  int gran;           // split lengths are multiples of gran keys
   int max_splits;     // splits per (sequence, kv head) at the host-known maximum length
   int Mpad;           // rows reserved per work item in the partial buffers
   int n_work;         // S * Hkv * max_splits
-  int per_xcd;        // ceil(n_work / 8)
+  int per_xcd;        // ceil(n_work / 8): the XCD-grouped deal of a one-wave grid
+  int dense;          // more than one wave: work items numbered densely on the device
   float scale_log2;   // softmax scale * log2(e)
   int causal;
   // paged caches only: k, v are page pools [num_pages, Hkv, page_size, D]; logical page j of
@@ -52,6 +54,100 @@ struct AttnArgs {
   const int *block_table;
   int page_log2, max_pages, num_pages;
 };
+
+// ---- work items ----------------------------------------------------------------
+// Each (sequence, kv head) pair of L keys is cut into nsplit = ceil(L / split_len) splits of
+// even length (ceil(L / nsplit) rounded up to gran keys, never more than split_len, so every
+// split is non-empty).  One work item per split.
+//   One-wave grid (n_work <= one workgroup per CU): workgroup w owns slot w = pair *
+//     max_splits + split, dealt so that a pair's splits share an XCD; slots past a pair's
+//     nsplit have no work.
+//   Larger grids: the items that exist are numbered densely on the device, sequence by
+//     sequence, pair by pair, split by split (a prefix sum of Hkv * nsplit over the
+//     sequences, 64 per round), and workgroup i takes item i; round-robin dispatch over the
+//     XCDs then spreads every long sequence over all of them, and no workgroup is spent on an
+//     empty slot.
+// Partial slots are the workgroup's slot (one wave) or item index (dense).
+struct AttnItem {
+  int s, g, split, nsplit, k0, k1, slot, ctx, B, qoff;
+};
+
+__device__ __forceinline__ bool attn_item(const AttnArgs &a, int b, AttnItem &it) {
+  if (!a.dense) {
+    const int w = xcd_logical_id(b, a.per_xcd);
+    if (w >= a.n_work) return false;
+    it.split = w % a.max_splits;
+    const int sg = w / a.max_splits;
+    it.g = sg % a.Hkv;
+    it.s = sg / a.Hkv;
+    it.ctx = a.ctx_lens[it.s];
+    it.B = a.block_lens[it.s];
+    it.qoff = a.q_offsets[it.s];
+    if (it.B <= 0) return false;
+    it.nsplit = (it.ctx + it.B + a.split_len - 1) / a.split_len;
+    if (it.split >= it.nsplit) return false;
+    it.slot = w;
+  } else {
+    const int lane = threadIdx.x & 63;
+    int before = 0;
+    bool found = false;
+    for (int c0 = 0; c0 < a.S && !found; c0 += 64) {
+      const int k = min(c0 + lane, a.S - 1);  // clamped: no per-load branch
+      const int ctx = a.ctx_lens[k], B = a.block_lens[k], off = a.q_offsets[k];
+      const int n = (c0 + lane < a.S && B > 0) ? (ctx + B + a.split_len - 1) / a.split_len : 0;
+      const int items = n * a.Hkv;
+      const int incl = before + wave_scan_i(items);
+      const unsigned long long hit = __ballot(incl > b && incl - items <= b);
+      if (hit) {
+        const int l = __ffsll((long long)hit) - 1;  // wave-uniform
+        it.s = c0 + l;
+        it.ctx = __builtin_amdgcn_readlane(ctx, l);
+        it.B = __builtin_amdgcn_readlane(B, l);
+        it.qoff = __builtin_amdgcn_readlane(off, l);
+        it.nsplit = __builtin_amdgcn_readlane(n, l);
+        const int r = b - __builtin_amdgcn_readlane(incl - items, l);
+        it.g = r / it.nsplit;
+        it.split = r - it.g * it.nsplit;
+        it.slot = b;
+        found = true;
+      }
+      before = __builtin_amdgcn_readlane(incl, 63);
+    }
+    if (!found) return false;  // past the last item
+  }
+  const int L = it.ctx + it.B;
+  const int slen = (((L + it.nsplit - 1) / it.nsplit + a.gran - 1) / a.gran) * a.gran;
+  it.k0 = it.split * slen;
+  it.k1 = min(it.k0 + slen, L);
+  return true;
+}
+
+// Partial slot of split 0 of pair (s, g) and the pair's split count (0: no block).
+__device__ __forceinline__ int2 attn_pair_slots(const AttnArgs &a, int s, int g, int &B) {
+  if (!a.dense) {
+    B = a.block_lens[s];
+    if (B <= 0) return int2{0, 0};
+    return int2{(s * a.Hkv + g) * a.max_splits, (a.ctx_lens[s] + B + a.split_len - 1) / a.split_len};
+  }
+  const int lane = threadIdx.x & 63;
+  int before = 0;
+  for (int c0 = 0; c0 <= s; c0 += 64) {
+    const int k = min(c0 + lane, a.S - 1);  // clamped: no per-load branch
+    const int ctx = a.ctx_lens[k], Bk = a.block_lens[k];
+    const int n = (c0 + lane < a.S && Bk > 0) ? (ctx + Bk + a.split_len - 1) / a.split_len : 0;
+    const int incl = before + wave_scan_i(n * a.Hkv);
+    if (s < c0 + 64) {
+      const int l = s - c0;
+      B = __builtin_amdgcn_readlane(Bk, l);
+      const int ns = __builtin_amdgcn_readlane(n, l);
+      if (B <= 0) return int2{0, 0};
+      return int2{__builtin_amdgcn_readlane(incl, l) - ns * a.Hkv + g * ns, ns};
+    }
+    before = __builtin_amdgcn_readlane(incl, 63);
+  }
+  B = 0;
+  return int2{0, 0};
+}
 
 template <bool BF16>
 struct AttnCfg {
@@ -170,22 +266,11 @@ __global__ __launch_bounds__(256) void block_attn_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) char ks[KT * KPITCH];
   __shared__ __attribute__((aligned(16))) char vts[D * VPITCH];
 
-  const int w = xcd_logical_id(blockIdx.x, a.per_xcd);
-  if (w >= a.n_work) return;
-  const int split = w % a.max_splits;
-  const int sg = w / a.max_splits;
-  const int g = sg % a.Hkv;
-  const int s = sg / a.Hkv;
-  const int ctx = a.ctx_lens[s];
-  const int B = a.block_lens[s];
-  if (B <= 0) return;
-  const int L = ctx + B;
-  const int nsplit = (L + a.split_len - 1) / a.split_len;
-  if (split >= nsplit) return;
-  const int k0 = split * a.split_len;
-  const int k1 = min(k0 + a.split_len, L);
+  AttnItem it;
+  if (!attn_item(a, blockIdx.x, it)) return;
+  const int s = it.s, g = it.g, k0 = it.k0, k1 = it.k1, nsplit = it.nsplit;
+  const int ctx = it.ctx, B = it.B, qoff = it.qoff;
   const int M = a.G * B;
-  const int qoff = a.q_offsets[s];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -384,7 +469,7 @@ __global__ __launch_bounds__(256) void block_attn_kernel(AttnArgs a) {
   }
 
   // ---- several splits: write this split's partials for the merge launch ----
-  const size_t wrow = (size_t)w * a.Mpad;
+  const size_t wrow = (size_t)it.slot * a.Mpad;
 #pragma unroll
   for (int j = 0; j < MT; ++j) {
     const int mt = wave + 4 * j;
@@ -409,16 +494,15 @@ __global__ __launch_bounds__(256) void block_attn_merge_kernel(AttnArgs a) {
   const int rb = blockIdx.x % nrb;
   const int sg = blockIdx.x / nrb;
   const int s = sg / a.Hkv, g = sg % a.Hkv;
-  const int ctx = a.ctx_lens[s];
-  const int B = a.block_lens[s];
-  if (B <= 0) return;
-  const int nsplit = (ctx + B + a.split_len - 1) / a.split_len;
-  if (nsplit <= 1) return;  // written directly by the split kernel
+  int B;
+  const int2 ps = attn_pair_slots(a, s, g, B);
+  const int nsplit = ps.y;
+  if (nsplit <= 1) return;  // no block, or written directly by the split kernel
   const int M = a.G * B;
   const int m = rb * RB + threadIdx.x / TPR;
   if (m >= M) return;
   const int d = (threadIdx.x % TPR) * 4;
-  const size_t wbase = (size_t)sg * a.max_splits * a.Mpad + m;  // row m of split 0
+  const size_t wbase = (size_t)ps.x * a.Mpad + m;  // row m of split 0
   // online merge over batches of SB splits whose loads are issued together (clamped, no
   // per-load branch): one memory round trip per batch instead of one per split
   constexpr int SB = 4;

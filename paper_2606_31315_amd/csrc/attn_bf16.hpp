@@ -192,22 +192,11 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) char ring_raw[NS * T::STAGEB];
   char SDB_LDS *ring = (char SDB_LDS *)(SDB_LDS void *)ring_raw;
 
-  const int w = xcd_logical_id(blockIdx.x, a.per_xcd);
-  if (w >= a.n_work) return;
-  const int split = w % a.max_splits;
-  const int sg = w / a.max_splits;
-  const int g = sg % a.Hkv;
-  const int s = sg / a.Hkv;
-  const int ctx = a.ctx_lens[s];
-  const int B = a.block_lens[s];
-  if (B <= 0) return;
-  const int L = ctx + B;
-  const int nsplit = (L + a.split_len - 1) / a.split_len;
-  if (split >= nsplit) return;
-  const int k0 = split * a.split_len;
-  const int k1 = min(k0 + a.split_len, L);
+  AttnItem it;
+  if (!attn_item(a, blockIdx.x, it)) return;
+  const int s = it.s, g = it.g, k0 = it.k0, k1 = it.k1, nsplit = it.nsplit;
+  const int ctx = it.ctx, B = it.B, qoff = it.qoff;
   const int M = a.G * B;
-  const int qoff = a.q_offsets[s];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -379,7 +368,7 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
     }
     return;
   }
-  const size_t wrow = (size_t)w * a.Mpad;
+  const size_t wrow = (size_t)it.slot * a.Mpad;
 #pragma unroll
   for (int j = 0; j < MT; ++j) {
     const int m = (wave + T::NW * j) * 16 + l16;

@@ -117,6 +117,17 @@ __device__ __forceinline__ double wave_scan_d(double x, double *excl) {
   return x;
 }
 
+// Inclusive prefix sum of an int over the 64 lanes (DPP lane moves).
+__device__ __forceinline__ int wave_scan_i(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15 into rows 1, 3
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31 into rows 2, 3
+  return x;
+}
+
 // Largest value over the 64 lanes (fmaxf: NaN lanes are ignored), in every lane.
 __device__ __forceinline__ float wave_max_f(float x) {
   x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0x7fc00000, __float_as_int(x), 0x128, 0xf, 0xf, false)));

@@ -62,7 +62,7 @@ constexpr int kBf16KT = SDB_BF16_KT, kBf16NS = SDB_BF16_NS;
 // attention planning
 // ---------------------------------------------------------------------------
 struct AttnPlan {
-  int G, KT, split_len, max_splits, Mpad, n_work, per_xcd, MT;
+  int G, KT, split_len, max_splits, Mpad, n_work, per_xcd, grid, dense, MT;
   size_t off_ml, off_o, total;
 };
 
@@ -114,7 +114,14 @@ int attn_plan(const sd_attn_shape *sh, AttnPlan *p) {
   const long long nw = pairs * p->max_splits;
   if (nw > (1LL << 30)) return fail(SD_ERR_INVALID_ARG, "problem too large");
   p->n_work = (int)nw;
+  // One wave: one workgroup per slot, the splits of a pair dealt to one XCD (measured slightly
+  // faster on the ragged Qwen3-4B batch than round-robin).  More than one wave: the device
+  // numbers the existing splits densely (attn_item), so no workgroup is spent on an empty slot
+  // and round-robin dispatch spreads long sequences over every XCD (long-context batch, 32
+  // sequences with contexts 8k-32k: 677-714 us with one workgroup per slot, about 600 dense).
+  p->dense = nw > target_wgs;
   p->per_xcd = (int)((nw + sdb::kNumXcd - 1) / sdb::kNumXcd);
+  p->grid = p->dense ? (int)nw : p->per_xcd * sdb::kNumXcd;
   const int nmt = p->Mpad / 16;
   if (sh->dtype == SD_BF16) p->MT = nmt <= 8 ? 1 : 2;  // 8 wavefronts, 1 or 2 m-tiles each
   else p->MT = nmt <= 4 ? 1 : nmt <= 8 ? 2 : 4;      // 4 wavefronts
@@ -305,10 +312,12 @@ int attn_args(const sd_attn_shape *sh, const AttnPlan &p, const void *q, const v
   a->G = p.G;
   a->Lmax = sh->max_kv_len;
   a->split_len = p.split_len;
+  a->gran = sh->dtype == SD_BF16 ? 16 : p.KT;
   a->max_splits = p.max_splits;
   a->Mpad = p.Mpad;
   a->n_work = p.n_work;
   a->per_xcd = p.per_xcd;
+  a->dense = p.dense;
   const float scale = sh->scale > 0.f ? sh->scale : 1.0f / sqrtf((float)sh->head_dim);
   a->scale_log2 = scale * 1.4426950408889634f;
   a->causal = mask_mode == SD_MASK_CAUSAL_IN_BLOCK;
@@ -334,7 +343,7 @@ int sd_block_attn(const sd_attn_shape *sh, const void *q, const void *k_cache, c
   rc = attn_args(sh, p, q, k_cache, v_cache, ctx_lens, block_lens, q_offsets, mask_mode, out, workspace,
                  workspace_bytes, &a);
   if (rc) return rc;
-  const int grid = p.per_xcd * sdb::kNumXcd;
+  const int grid = p.grid;
   hipStream_t st = (hipStream_t)stream;
   const bool bf = sh->dtype == SD_BF16;
   if (sh->head_dim == 128) {
@@ -385,7 +394,7 @@ int sd_block_attn_paged(const sd_attn_shape *sh, int32_t page_size, int32_t num_
   a.page_log2 = log2;
   a.max_pages = max_pages;
   a.num_pages = num_pages;
-  const int grid = p.per_xcd * sdb::kNumXcd;
+  const int grid = p.grid;
   hipStream_t st = (hipStream_t)stream;
   if (sh->head_dim == 128) launch_attn_all<true, 128, true>(a, grid, p.MT, st);
   else launch_attn_all<true, 64, true>(a, grid, p.MT, st);

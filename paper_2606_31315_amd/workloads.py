@@ -327,6 +327,13 @@ def c5_long_context(temperatures=(1.0,), seed=1005, dtype="bf16", S=32, with_att
     return out
 
 
+def c4_lens(seed=1004, S=16):
+    rs = _streams(seed)
+    ctx = rs["ctx"].integers(1024, 8192, endpoint=True, size=S).astype(np.int32)
+    B = rs["B"].integers(8, 32, endpoint=True, size=S).astype(np.int32)
+    return ctx, B
+
+
 def c5_lens(seed=1005, S=32):
     rs = _streams(seed)
     ctx = rs["ctx"].integers(8192, 32768, endpoint=True, size=S).astype(np.int32)
