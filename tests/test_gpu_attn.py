@@ -136,3 +136,23 @@ def test_alternating_calls_arbitrary_workspace():
             assert torch.equal(first[p.name], o), (it, p.name)
         else:
             first[p.name] = o
+
+
+def _many_sequences(seed, S, mode, name):
+    """S sequences with ragged contexts (one empty context, some empty blocks)."""
+    rs = W._streams(seed)
+    ctx = rs["ctx"].integers(2000, 5000, endpoint=True, size=S).astype(np.int32)
+    B = rs["B"].integers(0, 24, endpoint=True, size=S).astype(np.int32)
+    ctx[3] = 0
+    B[[0, 63, 64, 65]] = [0, 0, 7, 0]
+    B[3] = max(int(B[3]), 1)
+    return W.make_attn(rs, S=S, Hq=8, Hkv=2, D=128, ctx_lens=ctx, block_lens=B, dtype="bf16", mask_mode=mode,
+                       name=name)
+
+
+@pytest.mark.parametrize("mode", [CAUSAL, BIDIR])
+def test_dense_plan_many_sequences(mode):
+    """100 sequences x 2 kv heads with contexts 2k-5k: the grid is more than one wave, so the
+    device numbers the existing splits densely (a prefix sum over 64 sequences per round, two
+    rounds here), with empty blocks at the round's edge; every output row compared."""
+    G.check_attn(_many_sequences(7301, 100, mode, "dense_many_seqs"))

@@ -92,3 +92,18 @@ def test_kv_append_paged_many_sequences():
     rk, rv = OPG.kv_append_paged(kp, vp, table, blk["k_new"], blk["v_new"], ctx, off)
     assert np.array_equal(dkp.float().cpu().numpy(), rk, equal_nan=True)
     assert np.array_equal(dvp.float().cpu().numpy(), rv, equal_nan=True)
+
+
+def test_paged_dense_plan_many_sequences():
+    """The dense split numbering (more than one wave of splits) through page pools: bit-identical
+    to the contiguous kernel on the same keys."""
+    from test_gpu_attn import _many_sequences
+    p = _many_sequences(7302, 100, CAUSAL, "paged_dense_many_seqs")
+    rs = W._streams(7303)
+    Lp = ((p.Lmax + 31) // 32) * 32
+    k = torch.nn.functional.pad(p.k_cache, (0, 0, 0, Lp - p.Lmax), value=float("nan"))
+    v = torch.nn.functional.pad(p.v_cache, (0, 0, 0, Lp - p.Lmax), value=float("nan"))
+    kp, vp, table = W.paginate(rs, k, v, 32)
+    got = _paged_run(p, kp, vp, table).cpu()
+    ref = G.run_attn(p).cpu()
+    assert torch.equal(got, ref)
