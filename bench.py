@@ -484,6 +484,25 @@ def main():
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
                      "traffic": measured_traffic()},
     }
+    res["attn_frac_of_copy_rate"] = round(attn_gbps / copy_cal["gbps_read_plus_write"], 4)
+    # the same step with greedy acceptance (T = 0): same target logits, drafts = the drafter's argmax
+    acc0 = W.c3_ragged(temperatures=(0.0,), with_attn=False, dtype="bf16").accept[0.0]
+    tok0 = torch.from_numpy(acc0.draft_tokens).to(dev)
+    al0 = torch.empty_like(al)
+    nt0 = torch.empty_like(nt)
+
+    def step0(i):
+        attn_call(i)
+        sd.accept(bufs[i % copies]["t"], None, tok0, None, small["bl"], small["off"], 0.0, max_block=a.max_block,
+                  accept_len=al0, next_token=nt0, workspace=ws_acc)
+
+    for i in range(args.warmup):
+        step0(i)
+    ms0 = timed(step0, K)
+    acc0_bytes = acc0.logit_bytes()
+    res["t0"] = {"ms_per_step": round(ms0, 6), "verified_draft_tokens_per_s": round(ntok / (ms0 * 1e-3), 1),
+                 "accept_bytes": acc0_bytes, "step_gbps": round((attn_bytes + acc0_bytes) / (ms0 * 1e-3) / 1e9, 1),
+                 "what": "the same step with greedy acceptance (T = 0): every target row read once"}
     res["paged_attn_us"] = {f"page_{ps}_shuffled": paged_run(torch, sd, a, bufs, ps, K) for ps in (16, 64, 256)}
     res["paged_attn_us"]["page_64_in_order"] = paged_run(torch, sd, a, bufs, 64, K, shuffle=False)
     if args.policy_prompts > 0:
