@@ -132,6 +132,22 @@ int sd_block_attn_paged(const sd_attn_shape *shape, int32_t page_size, int32_t n
                         const int32_t *ctx_lens, const int32_t *block_lens, const int32_t *q_offsets,
                         int32_t mask_mode, void *out, void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * sd_block_attn with the block's keys and values taken from the new rows rather than the
+ * cache, and written into the cache by the same launch (the append before verification,
+ * Sec. 2.1, fused into it):
+ *   k_new, v_new    [total_q, Hkv, D] bf16: row q_offsets[s] + i is block position i of s
+ *   k_cache,v_cache [S, Hkv, Lmax, D] bf16: rows [0, ctx_s) are read; rows [ctx_s, ctx_s + B_s)
+ *                                     are written with the new rows (their old contents are
+ *                                     never read)
+ * The result equals sd_kv_append followed by sd_block_attn, bit for bit.  Everything else is
+ * as in sd_block_attn (same workspace size).  bf16 only (SD_ERR_UNSUPPORTED otherwise).
+ */
+int sd_block_attn_append(const sd_attn_shape *shape, const void *q, const void *k_new, const void *v_new,
+                         void *k_cache, void *v_cache, const int32_t *ctx_lens, const int32_t *block_lens,
+                         const int32_t *q_offsets, int32_t mask_mode, void *out, void *workspace,
+                         size_t workspace_bytes, void *stream);
+
 /* ==========================================================================
  * Speculative acceptance (Fig. 1 caption: accept the longest consistent prefix;
  * Sec. 1 and Sec. 3.1: the target's output distribution is preserved exactly).
@@ -239,7 +255,8 @@ int sd_verify_step_workspace_size(const sd_attn_shape *attn_shape, const sd_acce
 
 /*
  * One verify step, enqueued on `stream` with no host synchronisation: for every layer l,
- * sd_kv_append then sd_block_attn (layers[l]); then sd_accept on the given logits; then
+ * sd_kv_append then sd_block_attn (layers[l]; for bf16 both in one sd_block_attn_append
+ * launch); then sd_accept on the given logits; then
  * sd_commit (ctx_lens advances by accept_len + 1).  The logits are the caller's (the model's
  * head after the last layer); every other argument has the meaning given above.  The two
  * shapes must agree on num_seqs, total_q and max_block; attn_shape->max_ctx bounds ctx_lens

@@ -8,7 +8,8 @@ include/sd_block.h:
   accept      vocabulary-wide speculative acceptance (greedy at T=0, lossless
               rejection sampling at T>0) returning accept_len and the next token.
 
-and the step around them: kv_append (the block's keys and values into the cache),
+and the step around them: kv_append (the block's keys and values into the cache;
+block_attn_append fuses it into the attention launch),
 commit (ctx += accept_len + 1) and verify_step (append + attention per layer,
 acceptance, commit, in one native call); block_attn_paged and kv_append_paged over
 page pools with a block table; and the once-per-prompt block-size policy
@@ -18,10 +19,10 @@ survival_tau and survival_sample: the prefix-survival model of the accepted leng
 """
 from ._lib import (SD_BF16, SD_F32, SD_MASK_BIDIR_IN_BLOCK, SD_MASK_CAUSAL_IN_BLOCK, SdError, Workspace,
                    accept, accept_shape, accept_workspace_size, attn_shape, attn_workspace_size, block_attn,
-                   block_attn_paged, block_size_policy, commit, kv_append_paged,
+                   block_attn_append, block_attn_paged, block_size_policy, commit, kv_append_paged,
                    kv_append, lib, survival_sample, survival_tau, verify_step, version)
 
-__all__ = ["block_attn", "block_attn_paged", "kv_append_paged", "accept", "kv_append", "commit", "verify_step", "block_size_policy", "survival_tau", "survival_sample", "attn_shape", "accept_shape",
+__all__ = ["block_attn", "block_attn_append", "block_attn_paged", "kv_append_paged", "accept", "kv_append", "commit", "verify_step", "block_size_policy", "survival_tau", "survival_sample", "attn_shape", "accept_shape",
            "attn_workspace_size", "accept_workspace_size",
            "Workspace", "SdError", "lib", "version", "SD_BF16", "SD_F32", "SD_MASK_CAUSAL_IN_BLOCK",
            "SD_MASK_BIDIR_IN_BLOCK"]

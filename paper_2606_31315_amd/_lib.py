@@ -21,7 +21,7 @@ SD_MASK_CAUSAL_IN_BLOCK, SD_MASK_BIDIR_IN_BLOCK = 0, 1
 EXPORTS = ["sd_last_error", "sd_version", "sd_block_attn_workspace_size", "sd_block_attn",
            "sd_accept_workspace_size", "sd_accept", "sd_kv_append", "sd_commit", "sd_verify_step_workspace_size",
            "sd_verify_step", "sd_policy_workspace_size", "sd_block_size_policy", "sd_block_attn_paged",
-           "sd_kv_append_paged", "sd_survival_tau", "sd_survival_sample"]
+           "sd_kv_append_paged", "sd_survival_tau", "sd_survival_sample", "sd_block_attn_append"]
 
 
 class SdAttnShape(ctypes.Structure):
@@ -83,6 +83,8 @@ def lib() -> ctypes.CDLL:
         L.sd_accept.argtypes = [ctypes.POINTER(SdAcceptShape), P, P, P, P, P, P, ctypes.c_float, P, P, P, Z, P]
         L.sd_block_attn_paged.restype = ctypes.c_int
         L.sd_block_attn_paged.argtypes = [ctypes.POINTER(SdAttnShape), I, I, I, P, P, P, P, P, P, P, I, P, P, Z, P]
+        L.sd_block_attn_append.restype = ctypes.c_int
+        L.sd_block_attn_append.argtypes = [ctypes.POINTER(SdAttnShape), P, P, P, P, P, P, P, P, I, P, P, Z, P]
         L.sd_kv_append_paged.restype = ctypes.c_int
         L.sd_kv_append_paged.argtypes = [ctypes.POINTER(SdAttnShape), I, I, I, P, P, P, P, P, P, P, P]
         L.sd_kv_append.restype = ctypes.c_int
@@ -199,6 +201,33 @@ def block_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, ct
     _check(lib().sd_block_attn(ctypes.byref(shape), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(ctx_lens),
                                _ptr(block_lens), _ptr(q_offsets), int(mask_mode), _ptr(out), _ptr(workspace),
                                workspace.numel() * workspace.element_size(), _stream(stream)))
+    return out
+
+
+def block_attn_append(q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor, k_cache: torch.Tensor,
+                      v_cache: torch.Tensor, ctx_lens: torch.Tensor, block_lens: torch.Tensor, q_offsets: torch.Tensor,
+                      mask_mode: int, *, max_ctx: int, max_block: int, scale: float = 0.0,
+                      out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                      stream=None) -> torch.Tensor:
+    """Block attention with the block's keys/values read from k_new, v_new [total_q, Hkv, D] and
+    written into the caches by the same launch (sd_block_attn_append); bf16."""
+    dev = q.device
+    _need(q, "q", torch.bfloat16, dev)
+    for name, t in (("k_new", k_new), ("v_new", v_new), ("k_cache", k_cache), ("v_cache", v_cache)):
+        _need(t, name, torch.bfloat16, dev)
+    for name, t in (("ctx_lens", ctx_lens), ("block_lens", block_lens), ("q_offsets", q_offsets)):
+        _need(t, name, torch.int32, dev)
+    if out is None:
+        out = torch.empty_like(q)
+    _need(out, "out", q.dtype, dev)
+    shape = attn_shape(q, k_cache, max_ctx, max_block, scale)
+    nbytes = attn_workspace_size(shape)
+    if workspace is None:
+        workspace = _default_ws.get(nbytes, dev)
+    _check(lib().sd_block_attn_append(ctypes.byref(shape), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache),
+                                      _ptr(v_cache), _ptr(ctx_lens), _ptr(block_lens), _ptr(q_offsets),
+                                      int(mask_mode), _ptr(out), _ptr(workspace),
+                                      workspace.numel() * workspace.element_size(), _stream(stream)))
     return out
 
 

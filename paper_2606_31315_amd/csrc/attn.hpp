@@ -53,6 +53,9 @@ struct AttnArgs {
   // sequence s is pool page block_table[s * max_pages + j]
   const int *block_table;
   int page_log2, max_pages, num_pages;
+  // fused append only: the block's new keys and values [total_q, Hkv, D]
+  const void *k_new;
+  const void *v_new;
 };
 
 // ---- work items ----------------------------------------------------------------

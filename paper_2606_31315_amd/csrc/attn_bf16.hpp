@@ -67,6 +67,11 @@ __device__ __forceinline__ void wait_lds_tr(s16x4 (&v)[NDT][2]) {
   }
 }
 
+// 16-byte vector of new block rows (K or V) that a thread carries into the cache in an APPEND
+// launch.  A vector type, not the u32x4 struct: a struct array held across the tile loop is
+// copied through private memory.
+typedef unsigned AppendVec __attribute__((ext_vector_type(4)));
+
 template <int D, int KT_, int NS_>
 struct Bf16Tile {
   static constexpr int KT = KT_;                // keys per tile
@@ -135,6 +140,21 @@ struct TileLoads {
                                        (SDB_LDS void *)(dst + q * 1024), 16, 0, 0);
     }
   }
+  // The tile starting at key0 when the block's own keys are not in the cache yet: key
+  // k >= ctx is block row k - ctx, read from the new rows (nbase: the kv head's row of block
+  // position 0; rows nstride bytes apart).  Rows past key_last re-read key_last.
+  __device__ void issue_append(char SDB_LDS *stage, const char *kbase, const char *vbase, const char *knew,
+                               const char *vnew, size_t nstride, int key0, int key_last, int ctx, int wave) const {
+    const char *base = isv ? vbase : kbase;
+    const char *nbase = isv ? vnew : knew;
+    char SDB_LDS *dst = stage + (isv ? T::TILEB : 0) + (wave * T::LPW - (isv ? T::LPI : 0)) * 1024;
+#pragma unroll
+    for (int q = 0; q < T::LPW; ++q) {
+      const int key = min(key0 + row[q], key_last);
+      const char *src = key < ctx ? base + (size_t)key * T::ROWB + cof[q] : nbase + (size_t)(key - ctx) * nstride + cof[q];
+      __builtin_amdgcn_global_load_lds((const void *)src, (SDB_LDS void *)(dst + q * 1024), 16, 0, 0);
+    }
+  }
   // Issue the loads of the tile starting at key0 into `stage`; rows past key_last
   // re-read key_last (only the split's last tile can need that).
   __device__ void issue(char SDB_LDS *stage, const char *kbase, const char *vbase, int key0, int key_last,
@@ -182,7 +202,9 @@ __device__ __forceinline__ void pv_step(const f32x4 (&p)[NSB], unsigned stage, c
   }
 }
 
-template <int D, int MT, int KT_, int NS_, bool PAGED>
+// APPEND: the block's keys and values are read from a.k_new / a.v_new rather than the cache,
+// and the split that covers them also writes them into the cache (sd_block_attn_append).
+template <int D, int MT, int KT_, int NS_, bool PAGED, bool APPEND = false>
 __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   using T = Bf16Tile<D, KT_, NS_>;
   constexpr int KT = T::KT, NS = T::NS, NDT = D / 16, NST = D / 32, NSB = KT / 16;
@@ -257,10 +279,36 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   // paged caches: this sequence's row of the block table
   [[maybe_unused]] const int *table = PAGED ? a.block_table + (size_t)s * a.max_pages : nullptr;
   [[maybe_unused]] int pgn[T::LPW];  // page ids of the next tile to issue (paged caches)
+  // APPEND: the block rows of this kv head in the new-row arrays, and this split's share of
+  // them ([ab0, k1) of the keys) copied into the cache through registers: loaded now, stored
+  // once the first tile has landed (the loads are older than the tile's, so they are done).
+  [[maybe_unused]] const size_t nstride = (size_t)a.Hkv * D * EB;
+  [[maybe_unused]] const char *knew = nullptr, *vnew = nullptr;
+  [[maybe_unused]] int ab0 = k1;
+  constexpr int NAV = D / 32;  // 64 rows x 2 x D*2/16 vectors over 512 threads
+  [[maybe_unused]] AppendVec cpv[NAV];
+  if constexpr (APPEND) {
+    knew = reinterpret_cast<const char *>(a.k_new) + ((size_t)qoff * a.Hkv + g) * D * EB;
+    vnew = reinterpret_cast<const char *>(a.v_new) + ((size_t)qoff * a.Hkv + g) * D * EB;
+    ab0 = max(k0, ctx);
+    if (ab0 < k1) {  // uniform: this split covers block rows ab0 - ctx .. k1 - 1 - ctx
+      constexpr int RV = D * EB / 16;  // 16-byte vectors per row
+      const int half = (k1 - ab0) * RV;  // K vectors, then as many V vectors
+#pragma unroll
+      for (int c = 0; c < NAV; ++c) {
+        const int v = min(tid + 512 * c, 2 * half - 1);  // clamped: no per-load branch
+        const int kv = v >= half, w = v - kv * half, r = w / RV, ch = w % RV;
+        cpv[c] = *reinterpret_cast<const AppendVec *>((kv ? vnew : knew) + (size_t)(ab0 - ctx + r) * nstride + ch * 16);
+      }
+    }
+  }
   auto issue = [&](char SDB_LDS *stage, int key0) {
     if constexpr (PAGED) {
       ld.issue_paged(stage, kbase, vbase, key0, k1 - 1, pgn, a.page_log2, a.Hkv, g, wave);
       ld.fetch_pages(table, a.max_pages, a.num_pages, a.page_log2, key0 + KT, k1 - 1, wave, pgn);
+    } else if constexpr (APPEND) {
+      if (key0 + KT > ctx) ld.issue_append(stage, kbase, vbase, knew, vnew, nstride, key0, k1 - 1, ctx, wave);
+      else ld.issue(stage, kbase, vbase, key0, k1 - 1, wave);
     } else {
       ld.issue(stage, kbase, vbase, key0, k1 - 1, wave);
     }
@@ -284,6 +332,22 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
     else if (NS > 2 && ahead >= 1) wait_vmcnt<T::LPW>();
     else wait_vmcnt<0>();
     __syncthreads();  // tile t landed for every wavefront; stage (t-1) % NS is free again
+    if constexpr (APPEND) {
+      if (t == 0 && ab0 < k1) {  // the block rows this split covers, into the cache
+        constexpr int RV = D * EB / 16;
+        const int half = (k1 - ab0) * RV;
+        char *kc = reinterpret_cast<char *>(const_cast<void *>(a.k)) + ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
+        char *vc = reinterpret_cast<char *>(const_cast<void *>(a.v)) + ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
+#pragma unroll
+        for (int c = 0; c < NAV; ++c) {
+          const int v = tid + 512 * c;
+          if (v < 2 * half) {
+            const int kv = v >= half, w = v - kv * half, r = w / RV, ch = w % RV;
+            *reinterpret_cast<AppendVec *>((kv ? vc : kc) + (size_t)(ab0 + r) * T::ROWB + ch * 16) = cpv[c];
+          }
+        }
+      }
+    }
     if (t + NS - 1 < ntiles) issue(ring + ((t + NS - 1) % NS) * T::STAGEB, kt + (NS - 1) * KT);
     const unsigned stage = (unsigned)(uintptr_t)(ring + (t % NS) * T::STAGEB);
     const bool full = kt + KT <= vis_all;  // uniform: no key of this tile is masked for any row

@@ -139,13 +139,15 @@ void launch_attn(const sdb::AttnArgs &a, int grid, hipStream_t st) {
   hipLaunchKernelGGL((sdb::block_attn_kernel<BF16, D, MT>), dim3(grid), dim3(256), 0, st, a);
 }
 
-template <bool BF16, int D, bool PAGED = false>
+template <bool BF16, int D, bool PAGED = false, bool APPEND = false>
 void launch_attn_all(const sdb::AttnArgs &a, int grid, int MT, hipStream_t st) {
   if constexpr (BF16) {
     if (MT == 1)
-      hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 1, kBf16KT, kBf16NS, PAGED>), dim3(grid), dim3(512), 0, st, a);
+      hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 1, kBf16KT, kBf16NS, PAGED, APPEND>), dim3(grid), dim3(512), 0,
+                         st, a);
     else
-      hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 2, kBf16KT, kBf16NS, PAGED>), dim3(grid), dim3(512), 0, st, a);
+      hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 2, kBf16KT, kBf16NS, PAGED, APPEND>), dim3(grid), dim3(512), 0,
+                         st, a);
   } else {
     if (MT == 1) launch_attn<BF16, D, 1>(a, grid, st);
     else if (MT == 2) launch_attn<BF16, D, 2>(a, grid, st);
@@ -323,6 +325,7 @@ int attn_args(const sd_attn_shape *sh, const AttnPlan &p, const void *q, const v
   a->causal = mask_mode == SD_MASK_CAUSAL_IN_BLOCK;
   a->block_table = nullptr;
   a->page_log2 = a->max_pages = a->num_pages = 0;
+  a->k_new = a->v_new = nullptr;
   return ok();
 }
 
@@ -354,6 +357,32 @@ int sd_block_attn(const sd_attn_shape *sh, const void *q, const void *k_cache, c
     else launch_attn_all<false, 64>(a, grid, p.MT, st);
   }
   return check_launch("sd_block_attn");
+}
+
+int sd_block_attn_append(const sd_attn_shape *sh, const void *q, const void *k_new, const void *v_new, void *k_cache,
+                         void *v_cache, const int32_t *ctx_lens, const int32_t *block_lens, const int32_t *q_offsets,
+                         int32_t mask_mode, void *out, void *workspace, size_t workspace_bytes, void *stream) {
+  AttnPlan p;
+  int rc = attn_plan(sh, &p);
+  if (rc) return rc;
+  if (sh->dtype != SD_BF16) return fail(SD_ERR_UNSUPPORTED, "sd_block_attn_append: bf16 only");
+  if (sh->num_seqs == 0 || sh->total_q == 0) {
+    if (mask_mode != SD_MASK_CAUSAL_IN_BLOCK && mask_mode != SD_MASK_BIDIR_IN_BLOCK)
+      return fail(SD_ERR_INVALID_ARG, "unknown mask_mode %d", mask_mode);
+    return ok();
+  }
+  if (!k_new || !v_new) return fail(SD_ERR_INVALID_ARG, "sd_block_attn_append: NULL pointer argument");
+  if (!aligned16(k_new) || !aligned16(v_new)) return fail(SD_ERR_INVALID_ARG, "new rows must be 16-byte aligned");
+  sdb::AttnArgs a;
+  rc = attn_args(sh, p, q, k_cache, v_cache, ctx_lens, block_lens, q_offsets, mask_mode, out, workspace,
+                 workspace_bytes, &a);
+  if (rc) return rc;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  hipStream_t st = (hipStream_t)stream;
+  if (sh->head_dim == 128) launch_attn_all<true, 128, false, true>(a, p.grid, p.MT, st);
+  else launch_attn_all<true, 64, false, true>(a, p.grid, p.MT, st);
+  return check_launch("sd_block_attn_append");
 }
 
 namespace {
@@ -590,11 +619,17 @@ int sd_verify_step(const sd_attn_shape *ash, int32_t num_layers, const sd_layer_
   if (workspace_bytes < need) return fail(SD_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
   for (int l = 0; l < num_layers; ++l) {
     const sd_layer_buffers &L = layers[l];
-    rc = sd_kv_append(ash, L.k_new, L.v_new, L.k_cache, L.v_cache, ctx_lens, q_offsets, stream);
-    if (rc) return rc;
-    rc = sd_block_attn(ash, L.q, L.k_cache, L.v_cache, ctx_lens, block_lens, q_offsets, mask_mode, L.out, workspace,
-                       workspace_bytes, stream);
-    if (rc) return rc;
+    if (ash->dtype == SD_BF16) {  // append fused into the attention launch
+      rc = sd_block_attn_append(ash, L.q, L.k_new, L.v_new, L.k_cache, L.v_cache, ctx_lens, block_lens, q_offsets,
+                                mask_mode, L.out, workspace, workspace_bytes, stream);
+      if (rc) return rc;
+    } else {
+      rc = sd_kv_append(ash, L.k_new, L.v_new, L.k_cache, L.v_cache, ctx_lens, q_offsets, stream);
+      if (rc) return rc;
+      rc = sd_block_attn(ash, L.q, L.k_cache, L.v_cache, ctx_lens, block_lens, q_offsets, mask_mode, L.out, workspace,
+                         workspace_bytes, stream);
+      if (rc) return rc;
+    }
   }
   rc = sd_accept(csh, target_logits, draft_logits, draft_tokens, uniforms, block_lens, q_offsets, temperature,
                  accept_len, next_token, workspace, workspace_bytes, stream);

@@ -97,6 +97,28 @@ def test_attn_call_errors_without_device():
     assert call_attn(good_attn_shape(total_q=0)) == L.SD_OK
 
 
+def call_attn_append(sh, ptrs=None, mask=0):
+    P = ctypes.c_void_p
+    p = dict(q=4096, kn=20480, vn=24576, k=8192, v=12288, ctx=16, bl=32, off=48, out=16384)
+    if ptrs:
+        p.update(ptrs)
+    return L.lib().sd_block_attn_append(ctypes.byref(sh), P(p["q"]), P(p["kn"]), P(p["vn"]), P(p["k"]), P(p["v"]),
+                                        P(p["ctx"]), P(p["bl"]), P(p["off"]), mask, P(p["out"]), P(256),
+                                        attn_ws(sh)[1], None)
+
+
+def test_attn_append_call_errors_without_device():
+    sh = good_attn_shape()
+    assert call_attn_append(good_attn_shape(dtype=L.SD_F32)) == L.SD_ERR_UNSUPPORTED
+    assert call_attn_append(sh, ptrs=dict(kn=0)) == L.SD_ERR_INVALID_ARG
+    assert call_attn_append(sh, ptrs=dict(vn=0)) == L.SD_ERR_INVALID_ARG
+    assert call_attn_append(sh, ptrs=dict(kn=20488)) == L.SD_ERR_INVALID_ARG     # misaligned new rows
+    assert call_attn_append(sh, ptrs=dict(q=0)) == L.SD_ERR_INVALID_ARG
+    assert call_attn_append(sh, mask=2) == L.SD_ERR_INVALID_ARG
+    assert call_attn_append(good_attn_shape(total_q=0), mask=2) == L.SD_ERR_INVALID_ARG
+    assert call_attn_append(good_attn_shape(total_q=0)) == L.SD_OK
+
+
 def good_accept_shape(**kw):
     sh = L.SdAcceptShape(num_seqs=8, vocab=151936, total_q=124, max_block=24, dtype=L.SD_BF16)
     for k, v in kw.items():
