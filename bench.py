@@ -135,9 +135,9 @@ def copy_calibration(torch, dev, nbytes=1 << 29, reps=3):
 
 
 def verify_step_run(torch, sd, work, T, layers, steps, warmup=3):
-    """The whole verify step through sd_verify_step: for every layer the block's keys and values
-    are appended to that layer's cache and the block attends over it; then acceptance and the
-    commit.  Consecutive decode steps: ctx starts at the workload's 4096 and advances by
+    """The whole verify step through sd_verify_step: for every layer the block attends over that
+    layer's cache and its own keys and values, which the same launch writes into the cache; then
+    acceptance and the commit.  Consecutive decode steps: ctx starts at the workload's 4096 and advances by
     accept_len + 1 each step.  Caches and block inputs are random bf16 on the device."""
     a, acc = work.attn, work.accept[T]
     dev = torch.device("cuda:0")
@@ -184,8 +184,9 @@ def verify_step_run(torch, sd, work, T, layers, steps, warmup=3):
     return {"layers": layers, "steps": steps, "us_per_step": round(us, 1),
             "verified_draft_tokens_per_s": round(work.verified_draft_tokens() / (us * 1e-6), 1),
             "ctx_start": ctx0, "ctx_end": int(ctx.max().item()),
-            "what": "sd_verify_step: per layer sd_kv_append + sd_block_attn, then sd_accept (T=%g) and sd_commit; "
-                    "consecutive decode steps" % T}
+            "what": "sd_verify_step: per layer sd_block_attn_append (the block's keys and values written into "
+                    "the cache by the attention launch), then sd_accept (T=%g) and sd_commit; consecutive decode "
+                    "steps" % T}
 
 
 def policy_run(torch, sd, prompts, reps=20, V=151936, H=2048, radius=2, base_block=16):

@@ -281,7 +281,8 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   [[maybe_unused]] int pgn[T::LPW];  // page ids of the next tile to issue (paged caches)
   // APPEND: the block rows of this kv head in the new-row arrays, and this split's share of
   // them ([ab0, k1) of the keys) copied into the cache through registers: loaded now, stored
-  // once the first tile has landed (the loads are older than the tile's, so they are done).
+  // after the last tile.  (Stores count in vmcnt: issued earlier, they would hold up the next
+  // tile wait until they were acknowledged.)
   [[maybe_unused]] const size_t nstride = (size_t)a.Hkv * D * EB;
   [[maybe_unused]] const char *knew = nullptr, *vnew = nullptr;
   [[maybe_unused]] int ab0 = k1;
@@ -332,22 +333,6 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
     else if (NS > 2 && ahead >= 1) wait_vmcnt<T::LPW>();
     else wait_vmcnt<0>();
     __syncthreads();  // tile t landed for every wavefront; stage (t-1) % NS is free again
-    if constexpr (APPEND) {
-      if (t == 0 && ab0 < k1) {  // the block rows this split covers, into the cache
-        constexpr int RV = D * EB / 16;
-        const int half = (k1 - ab0) * RV;
-        char *kc = reinterpret_cast<char *>(const_cast<void *>(a.k)) + ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
-        char *vc = reinterpret_cast<char *>(const_cast<void *>(a.v)) + ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
-#pragma unroll
-        for (int c = 0; c < NAV; ++c) {
-          const int v = tid + 512 * c;
-          if (v < 2 * half) {
-            const int kv = v >= half, w = v - kv * half, r = w / RV, ch = w % RV;
-            *reinterpret_cast<AppendVec *>((kv ? vc : kc) + (size_t)(ab0 + r) * T::ROWB + ch * 16) = cpv[c];
-          }
-        }
-      }
-    }
     if (t + NS - 1 < ntiles) issue(ring + ((t + NS - 1) % NS) * T::STAGEB, kt + (NS - 1) * KT);
     const unsigned stage = (unsigned)(uintptr_t)(ring + (t % NS) * T::STAGEB);
     const bool full = kt + KT <= vis_all;  // uniform: no key of this tile is masked for any row
@@ -407,6 +392,23 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
       if constexpr (NSB > 4) {
         pv_step<2, NDT, NSB>(sacc, stage, voff, oacc[j]);
         pv_step<3, NDT, NSB>(sacc, stage, voff, oacc[j]);
+      }
+    }
+  }
+
+  if constexpr (APPEND) {
+    if (ab0 < k1) {  // the block rows this split covers, into the cache
+      constexpr int RV = D * EB / 16;
+      const int half = (k1 - ab0) * RV;
+      char *kc = reinterpret_cast<char *>(const_cast<void *>(a.k)) + ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
+      char *vc = reinterpret_cast<char *>(const_cast<void *>(a.v)) + ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
+#pragma unroll
+      for (int c = 0; c < NAV; ++c) {
+        const int v = tid + 512 * c;
+        if (v < 2 * half) {
+          const int kv = v >= half, w = v - kv * half, r = w / RV, ch = w % RV;
+          *reinterpret_cast<AppendVec *>((kv ? vc : kc) + (size_t)(ab0 + r) * T::ROWB + ch * 16) = cpv[c];
+        }
       }
     }
   }
