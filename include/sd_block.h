@@ -28,7 +28,7 @@
  *     returns a status code; it never aborts or prints.  Per-sequence values that
  *     live in device memory (ctx_lens, block_lens, q_offsets, tokens) cannot be
  *     checked on the host: values outside the documented ranges are undefined
- *     behaviour.
+ *     behaviour (sd_check_attn_inputs and sd_check_accept_inputs test them on the device).
  *   - Workspace: each operation needs device scratch memory of the size its
  *     *_workspace_size() reports (partial results between the kernels of one
  *     call).  Its contents on entry do not matter.  Calls that share a workspace
@@ -198,6 +198,43 @@ int sd_accept(const sd_accept_shape *shape, const void *target_logits, const voi
               const int32_t *draft_tokens, const float *uniforms, const int32_t *block_lens,
               const int32_t *q_offsets, float temperature, int32_t *accept_len, int32_t *next_token,
               void *workspace, size_t workspace_bytes, void *stream);
+
+/* ==========================================================================
+ * Checks of the per-sequence values the calls above read from device memory and take on
+ * trust.  For tests and debugging, not for the hot path: one small launch files an error
+ * word; nothing else is touched.  An element is read only where the values checked before
+ * it keep the index inside its documented array.
+ * ========================================================================== */
+enum {
+  SD_CHECK_CTX = 1,      /* ctx_s outside [0, max_ctx] */
+  SD_CHECK_BLOCK = 2,    /* B_s outside [0, max_block] (attention) or [1, max_block] (acceptance) */
+  SD_CHECK_OFFSETS = 4,  /* q_offsets[0] != 0, q_offsets[s+1] - q_offsets[s] != B_s, q_offsets[S] !=
+                            total_q, or an offset outside [0, total_q] */
+  SD_CHECK_TOKEN = 8,    /* a drafted token outside [0, V) */
+  SD_CHECK_UNIFORM = 16  /* a uniform outside [0, 1), NaN included */
+};
+
+/*
+ * status [3] int32 device out: status[0] = OR of the SD_CHECK_* bits found over all
+ * sequences (0: the values meet sd_block_attn's documented ranges for this shape);
+ * status[1] = the smallest offending sequence, or -1; status[2] = the number of offending
+ * sequences.  ctx_lens, block_lens [S] and q_offsets [S + 1] as in sd_block_attn (may be
+ * NULL when S == 0; status is still written).  Only num_seqs, total_q, max_ctx and max_block
+ * of the shape are used.
+ * Errors: SD_ERR_INVALID_ARG, SD_ERR_HIP.
+ */
+int sd_check_attn_inputs(const sd_attn_shape *shape, const int32_t *ctx_lens, const int32_t *block_lens,
+                         const int32_t *q_offsets, int32_t *status, void *stream);
+
+/*
+ * The same for sd_accept: block_lens, q_offsets, draft_tokens [total_q - S] and, when
+ * temperature > 0, uniforms [total_q] (unused and may be NULL at temperature 0).  Only
+ * num_seqs, vocab, total_q and max_block of the shape are used.
+ * Errors: SD_ERR_INVALID_ARG, SD_ERR_HIP.
+ */
+int sd_check_accept_inputs(const sd_accept_shape *shape, const int32_t *draft_tokens, const float *uniforms,
+                           const int32_t *block_lens, const int32_t *q_offsets, float temperature,
+                           int32_t *status, void *stream);
 
 /* ==========================================================================
  * The step around verification.  One speculative step writes the block's keys and

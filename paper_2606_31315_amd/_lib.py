@@ -21,7 +21,10 @@ SD_MASK_CAUSAL_IN_BLOCK, SD_MASK_BIDIR_IN_BLOCK = 0, 1
 EXPORTS = ["sd_last_error", "sd_version", "sd_block_attn_workspace_size", "sd_block_attn",
            "sd_accept_workspace_size", "sd_accept", "sd_kv_append", "sd_commit", "sd_verify_step_workspace_size",
            "sd_verify_step", "sd_policy_workspace_size", "sd_block_size_policy", "sd_block_attn_paged",
-           "sd_kv_append_paged", "sd_survival_tau", "sd_survival_sample", "sd_block_attn_append"]
+           "sd_kv_append_paged", "sd_survival_tau", "sd_survival_sample", "sd_block_attn_append",
+           "sd_check_attn_inputs", "sd_check_accept_inputs"]
+
+SD_CHECK_CTX, SD_CHECK_BLOCK, SD_CHECK_OFFSETS, SD_CHECK_TOKEN, SD_CHECK_UNIFORM = 1, 2, 4, 8, 16
 
 
 class SdAttnShape(ctypes.Structure):
@@ -105,6 +108,10 @@ def lib() -> ctypes.CDLL:
         L.sd_survival_tau.argtypes = [ctypes.POINTER(SdSurvivalShape), P, P, P, P, P, P, P]
         L.sd_survival_sample.restype = ctypes.c_int
         L.sd_survival_sample.argtypes = [ctypes.POINTER(SdSurvivalShape), P, ctypes.c_uint64, I, P, P, P]
+        L.sd_check_attn_inputs.restype = ctypes.c_int
+        L.sd_check_attn_inputs.argtypes = [ctypes.POINTER(SdAttnShape), P, P, P, P, P]
+        L.sd_check_accept_inputs.restype = ctypes.c_int
+        L.sd_check_accept_inputs.argtypes = [ctypes.POINTER(SdAcceptShape), P, P, P, P, ctypes.c_float, P, P]
         _lib = L
     return _lib
 
@@ -317,6 +324,45 @@ def accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor], dr
                            float(temperature), _ptr(accept_len), _ptr(next_token), _ptr(workspace),
                            workspace.numel() * workspace.element_size(), _stream(stream)))
     return accept_len, next_token
+
+
+def check_attn_inputs(ctx_lens: torch.Tensor, block_lens: torch.Tensor, q_offsets: torch.Tensor, *, total_q: int,
+                      max_ctx: int, max_block: int, status: Optional[torch.Tensor] = None,
+                      stream=None) -> torch.Tensor:
+    """sd_check_attn_inputs: device int32 [3] = (OR of SD_CHECK_* bits, first offending
+    sequence or -1, number of offending sequences)."""
+    dev = block_lens.device
+    for name, t in (("ctx_lens", ctx_lens), ("block_lens", block_lens), ("q_offsets", q_offsets)):
+        _need(t, name, torch.int32, dev)
+    if status is None:
+        status = torch.empty(3, dtype=torch.int32, device=dev)
+    _need(status, "status", torch.int32, dev)
+    shape = SdAttnShape(num_seqs=block_lens.shape[0], num_q_heads=1, num_kv_heads=1, head_dim=128,
+                        max_kv_len=max_ctx + max_block, total_q=total_q, max_ctx=max_ctx, max_block=max_block,
+                        dtype=SD_BF16, scale=0.0)
+    _check(lib().sd_check_attn_inputs(ctypes.byref(shape), _ptr(ctx_lens), _ptr(block_lens), _ptr(q_offsets),
+                                      _ptr(status), _stream(stream)))
+    return status
+
+
+def check_accept_inputs(draft_tokens: torch.Tensor, uniforms: Optional[torch.Tensor], block_lens: torch.Tensor,
+                        q_offsets: torch.Tensor, temperature: float, *, vocab: int, total_q: int, max_block: int,
+                        status: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """sd_check_accept_inputs: device int32 [3], as check_attn_inputs."""
+    dev = block_lens.device
+    for name, t in (("draft_tokens", draft_tokens), ("block_lens", block_lens), ("q_offsets", q_offsets)):
+        _need(t, name, torch.int32, dev)
+    if temperature > 0:
+        _need(uniforms, "uniforms", torch.float32, dev)
+    if status is None:
+        status = torch.empty(3, dtype=torch.int32, device=dev)
+    _need(status, "status", torch.int32, dev)
+    shape = SdAcceptShape(num_seqs=block_lens.shape[0], vocab=vocab, total_q=total_q, max_block=max_block,
+                          dtype=SD_BF16)
+    _check(lib().sd_check_accept_inputs(ctypes.byref(shape), _ptr(draft_tokens),
+                                        _ptr(uniforms if temperature > 0 else None), _ptr(block_lens),
+                                        _ptr(q_offsets), float(temperature), _ptr(status), _stream(stream)))
+    return status
 
 
 def kv_append(k_new: torch.Tensor, v_new: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,

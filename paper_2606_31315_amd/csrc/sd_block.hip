@@ -14,6 +14,7 @@
 #include "accept.hpp"
 #include "attn.hpp"
 #include "attn_bf16.hpp"
+#include "check.hpp"
 #include "kvstep.hpp"
 #include "policy.hpp"
 #include "sd_block.h"
@@ -547,6 +548,57 @@ int sd_accept(const sd_accept_shape *sh, const void *target_logits, const void *
 // ---------------------------------------------------------------------------
 // the step around verification: append, commit, and the whole verify step
 // ---------------------------------------------------------------------------
+static_assert(SD_CHECK_CTX == sdb::kCheckCtx && SD_CHECK_BLOCK == sdb::kCheckBlock &&
+                  SD_CHECK_OFFSETS == sdb::kCheckOffsets && SD_CHECK_TOKEN == sdb::kCheckToken &&
+                  SD_CHECK_UNIFORM == sdb::kCheckUniform,
+              "check bits of the header and the kernel agree");
+
+int sd_check_attn_inputs(const sd_attn_shape *sh, const int32_t *ctx_lens, const int32_t *block_lens,
+                         const int32_t *q_offsets, int32_t *status, void *stream) {
+  if (!sh) return fail(SD_ERR_INVALID_ARG, "sd_check_attn_inputs: shape is NULL");
+  if (sh->num_seqs < 0 || sh->total_q < 0 || sh->max_ctx < 0 || sh->max_block < 1 || sh->max_block > 64)
+    return fail(SD_ERR_INVALID_ARG, "sd_check_attn_inputs: num_seqs, total_q, max_ctx or max_block out of range");
+  if (!status || (sh->num_seqs > 0 && (!ctx_lens || !block_lens || !q_offsets)))
+    return fail(SD_ERR_INVALID_ARG, "sd_check_attn_inputs: NULL pointer argument");
+  sdb::CheckArgs a{};
+  a.ctx_lens = ctx_lens;
+  a.block_lens = block_lens;
+  a.q_offsets = q_offsets;
+  a.status = status;
+  a.S = sh->num_seqs;
+  a.total_q = sh->total_q;
+  a.max_ctx = sh->max_ctx;
+  a.min_block = 0;
+  a.max_block = sh->max_block;
+  hipLaunchKernelGGL(sdb::check_inputs_kernel, dim3(1), dim3(256), 0, (hipStream_t)stream, a);
+  return check_launch("sd_check_attn_inputs");
+}
+
+int sd_check_accept_inputs(const sd_accept_shape *sh, const int32_t *draft_tokens, const float *uniforms,
+                           const int32_t *block_lens, const int32_t *q_offsets, float temperature,
+                           int32_t *status, void *stream) {
+  if (!sh) return fail(SD_ERR_INVALID_ARG, "sd_check_accept_inputs: shape is NULL");
+  if (sh->num_seqs < 0 || sh->total_q < 0 || sh->vocab < 1 || sh->max_block < 1 || sh->max_block > 64)
+    return fail(SD_ERR_INVALID_ARG, "sd_check_accept_inputs: num_seqs, total_q, vocab or max_block out of range");
+  if (!(temperature >= 0.f) || isinf(temperature))
+    return fail(SD_ERR_INVALID_ARG, "temperature must be finite and >= 0");
+  if (!status || (sh->num_seqs > 0 && (!draft_tokens || !block_lens || !q_offsets || (temperature > 0.f && !uniforms))))
+    return fail(SD_ERR_INVALID_ARG, "sd_check_accept_inputs: NULL pointer argument");
+  sdb::CheckArgs a{};
+  a.block_lens = block_lens;
+  a.q_offsets = q_offsets;
+  a.draft_tokens = draft_tokens;
+  a.uniforms = temperature > 0.f ? uniforms : nullptr;
+  a.status = status;
+  a.S = sh->num_seqs;
+  a.total_q = sh->total_q;
+  a.min_block = 1;
+  a.max_block = sh->max_block;
+  a.vocab = sh->vocab;
+  hipLaunchKernelGGL(sdb::check_inputs_kernel, dim3(1), dim3(256), 0, (hipStream_t)stream, a);
+  return check_launch("sd_check_accept_inputs");
+}
+
 int sd_kv_append(const sd_attn_shape *sh, const void *k_new, const void *v_new, void *k_cache, void *v_cache,
                  const int32_t *ctx_lens, const int32_t *q_offsets, void *stream) {
   int rc = check_cache_shape(sh, "sd_kv_append");

@@ -46,6 +46,10 @@ def run_attn(p: AttnProblem, d=None, workspace=None, out=None) -> torch.Tensor:
     d = d or attn_to_device(p)
     log(f"sd_block_attn {p.name} S={p.S} Hq={p.Hq} Hkv={p.Hkv} D={p.D} dtype={p.dtype} mask={p.mask_mode} "
         f"ctx<={p.max_ctx} B<={p.max_block} total_q={p.total_q}")
+    if p.S:  # the per-sequence device values meet the documented ranges
+        st = sd.check_attn_inputs(d["ctx"], d["bl"], d["off"], total_q=p.total_q, max_ctx=p.max_ctx,
+                                  max_block=p.max_block)
+        assert st.cpu().tolist() == [0, -1, 0], st
     o = sd.block_attn(d["q"], d["k"], d["v"], d["ctx"], d["bl"], d["off"], p.mask_mode, max_ctx=p.max_ctx,
                       max_block=p.max_block, scale=p.scale, workspace=workspace, out=out)
     torch.cuda.synchronize()
@@ -120,6 +124,10 @@ def accept_to_device(p: AcceptProblem, device=None):
 def run_accept(p: AcceptProblem, d=None, workspace=None):
     d = d or accept_to_device(p)
     log(f"sd_accept {p.name} S={p.S} V={p.V} total_q={p.total_q} B<={p.max_block} T={p.temperature} dtype={p.dtype}")
+    if p.S:  # the per-sequence device values meet the documented ranges
+        st = sd.check_accept_inputs(d["tok"], d["u"], d["bl"], d["off"], p.temperature, vocab=p.V,
+                                    total_q=p.total_q, max_block=p.max_block)
+        assert st.cpu().tolist() == [0, -1, 0], st
     al, nt = sd.accept(d["t"], d["d"], d["tok"], d["u"], d["bl"], d["off"], p.temperature, max_block=p.max_block,
                        workspace=workspace)
     torch.cuda.synchronize()

@@ -119,6 +119,29 @@ def test_attn_append_call_errors_without_device():
     assert call_attn_append(good_attn_shape(total_q=0)) == L.SD_OK
 
 
+def test_check_calls_errors_without_device():
+    P = ctypes.c_void_p
+    f = L.lib().sd_check_attn_inputs
+    sh = good_attn_shape()
+    assert f(None, P(16), P(32), P(48), P(64), None) == L.SD_ERR_INVALID_ARG
+    assert f(ctypes.byref(good_attn_shape(max_block=65)), P(16), P(32), P(48), P(64), None) == L.SD_ERR_INVALID_ARG
+    assert f(ctypes.byref(good_attn_shape(max_ctx=-1)), P(16), P(32), P(48), P(64), None) == L.SD_ERR_INVALID_ARG
+    assert f(ctypes.byref(sh), P(16), P(32), P(48), None, None) == L.SD_ERR_INVALID_ARG      # no status
+    assert f(ctypes.byref(sh), None, P(32), P(48), P(64), None) == L.SD_ERR_INVALID_ARG
+    g = L.lib().sd_check_accept_inputs
+    ash = L.SdAcceptShape(num_seqs=8, vocab=151936, total_q=124, max_block=24, dtype=L.SD_BF16)
+    assert g(None, P(16), P(32), P(48), P(64), ctypes.c_float(1.0), P(80), None) == L.SD_ERR_INVALID_ARG
+    assert g(ctypes.byref(ash), P(16), None, P(48), P(64), ctypes.c_float(1.0), P(80), None) == L.SD_ERR_INVALID_ARG
+    assert g(ctypes.byref(ash), P(16), P(32), P(48), P(64), ctypes.c_float(-1.0), P(80), None) == L.SD_ERR_INVALID_ARG
+    assert g(ctypes.byref(ash), P(16), P(32), P(48), P(64), ctypes.c_float(float("nan")), P(80), None) == \
+        L.SD_ERR_INVALID_ARG
+    assert g(ctypes.byref(ash), None, P(32), P(48), P(64), ctypes.c_float(0.0), P(80), None) == L.SD_ERR_INVALID_ARG
+    bad_v = L.SdAcceptShape(num_seqs=8, vocab=0, total_q=124, max_block=24, dtype=L.SD_BF16)
+    assert g(ctypes.byref(bad_v), P(16), P(32), P(48), P(64), ctypes.c_float(0.0), P(80), None) == \
+        L.SD_ERR_INVALID_ARG
+    assert L.lib().sd_last_error().decode()
+
+
 def good_accept_shape(**kw):
     sh = L.SdAcceptShape(num_seqs=8, vocab=151936, total_q=124, max_block=24, dtype=L.SD_BF16)
     for k, v in kw.items():
