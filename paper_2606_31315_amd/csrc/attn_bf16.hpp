@@ -114,7 +114,10 @@ struct TileLoads {
   // table[k >> log2] at row k & (page_size - 1).  A load instruction covers RPI consecutive
   // keys of one page (tiles start on a multiple of 16 keys, pages hold a multiple of 16 keys,
   // and rows past key_last re-read key_last), so its page id is uniform: fetch_pages reads it
-  // with a scalar load one tile ahead of issue_paged.  (An LDS lookup would make the compiler
+  // with a scalar load one tile ahead of issue_paged, at the end of a tile's arithmetic.
+  // Scalar loads and LDS reads share one wait counter (lgkmcnt), so a page-id load issued
+  // before the arithmetic would stall its first LDS read for a memory round trip; issued
+  // after it, the load overlaps the next tile wait.  (An LDS lookup would make the compiler
   // drain every in-flight load-to-LDS transfer before it.)  Ids are clamped into the pool.
   __device__ void fetch_pages(const int *table, int max_pages, int num_pages, int log2, int key0, int key_last,
                               int wave, int (&pg)[T::LPW]) const {
@@ -306,7 +309,6 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   auto issue = [&](char SDB_LDS *stage, int key0) {
     if constexpr (PAGED) {
       ld.issue_paged(stage, kbase, vbase, key0, k1 - 1, pgn, a.page_log2, a.Hkv, g, wave);
-      ld.fetch_pages(table, a.max_pages, a.num_pages, a.page_log2, key0 + KT, k1 - 1, wave, pgn);
     } else if constexpr (APPEND) {
       if (key0 + KT > ctx) ld.issue_append(stage, kbase, vbase, knew, vnew, nstride, key0, k1 - 1, ctx, wave);
       else ld.issue(stage, kbase, vbase, key0, k1 - 1, wave);
@@ -317,10 +319,13 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
 
   // ---- pipeline prologue: tiles 0 .. NS-2 in flight ----
   const int ntiles = (k1 - k0 + KT - 1) / KT;
-  if constexpr (PAGED) ld.fetch_pages(table, a.max_pages, a.num_pages, a.page_log2, k0, k1 - 1, wave, pgn);
 #pragma unroll
   for (int t = 0; t < NS - 1; ++t)
-    if (t < ntiles) issue(ring + t * T::STAGEB, k0 + t * KT);
+    if (t < ntiles) {
+      if constexpr (PAGED) ld.fetch_pages(table, a.max_pages, a.num_pages, a.page_log2, k0 + t * KT, k1 - 1, wave, pgn);
+      issue(ring + t * T::STAGEB, k0 + t * KT);
+    }
+  if constexpr (PAGED) ld.fetch_pages(table, a.max_pages, a.num_pages, a.page_log2, k0 + (NS - 1) * KT, k1 - 1, wave, pgn);
   // keys every row can see: all of [k0, k1) when bidirectional, keys <= ctx when causal
   const int vis_all = a.causal ? min(k1, ctx + 1) : k1;
   const float sl2 = a.scale_log2;
@@ -393,6 +398,9 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
         pv_step<2, NDT, NSB>(sacc, stage, voff, oacc[j]);
         pv_step<3, NDT, NSB>(sacc, stage, voff, oacc[j]);
       }
+    }
+    if constexpr (PAGED) {
+      if (t + NS < ntiles) ld.fetch_pages(table, a.max_pages, a.num_pages, a.page_log2, k0 + (t + NS) * KT, k1 - 1, wave, pgn);
     }
   }
 
