@@ -140,3 +140,9 @@ def test_verify_step_greedy_three_steps():
 
 def test_verify_step_sampling_two_steps():
     _run_steps(1.0, steps=2, seed=4202)
+
+
+def test_verify_step_fp32_two_steps():
+    """fp32 caches and logits: the step appends with sd_kv_append and then attends (the fused
+    append is bf16 only); outputs at the fp32 tolerance, caches bit-exact."""
+    _run_steps(1.0, steps=2, seed=4203, dtype="f32")
