@@ -486,6 +486,12 @@ def main():
                      "traffic": measured_traffic()},
     }
     res["attn_frac_of_copy_rate"] = round(attn_gbps / copy_cal["gbps_read_plus_write"], 4)
+    res["step_frac_of_copy_rate"] = round(step_gbps / copy_cal["gbps_read_plus_write"], 4)
+    # rows a sequential acceptance would have read: target rows 0..accept_len and the drafts
+    # tested up to the first rejection (the data-parallel pass reads every row)
+    B_h = a.block_lens.astype(np.int64)
+    useful_rows = int((al_h + 1).sum() + (np.minimum(al_h + 1, B_h - 1) if T > 0 else 0 * B_h).sum())
+    res["accept_useful_bytes"] = useful_rows * acc.V * 2
     # the same step with greedy acceptance (T = 0): same target logits, drafts = the drafter's argmax
     acc0 = W.c3_ragged(temperatures=(0.0,), with_attn=False, dtype="bf16").accept[0.0]
     tok0 = torch.from_numpy(acc0.draft_tokens).to(dev)
@@ -501,8 +507,10 @@ def main():
         step0(i)
     ms0 = timed(step0, K)
     acc0_bytes = acc0.logit_bytes()
+    al0_h = al0.cpu().numpy()
     res["t0"] = {"ms_per_step": round(ms0, 6), "verified_draft_tokens_per_s": round(ntok / (ms0 * 1e-3), 1),
-                 "accept_bytes": acc0_bytes, "step_gbps": round((attn_bytes + acc0_bytes) / (ms0 * 1e-3) / 1e9, 1),
+                 "accept_bytes": acc0_bytes, "accept_useful_bytes": int((al0_h + 1).sum()) * acc0.V * 2,
+                 "step_gbps": round((attn_bytes + acc0_bytes) / (ms0 * 1e-3) / 1e9, 1),
                  "what": "the same step with greedy acceptance (T = 0): every target row read once"}
     res["paged_attn_us"] = {f"page_{ps}_shuffled": paged_run(torch, sd, a, bufs, ps, K) for ps in (16, 64, 256)}
     res["paged_attn_us"]["page_64_in_order"] = paged_run(torch, sd, a, bufs, 64, K, shuffle=False)
