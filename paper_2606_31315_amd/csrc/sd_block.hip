@@ -473,12 +473,15 @@ int sd_accept_workspace_size(const sd_accept_shape *shape, float temperature, si
   return ok();
 }
 
-int sd_accept(const sd_accept_shape *sh, const void *target_logits, const void *draft_logits,
-              const int32_t *draft_tokens, const float *uniforms, const int32_t *block_lens,
-              const int32_t *q_offsets, float temperature, int32_t *accept_len, int32_t *next_token,
-              void *workspace, size_t workspace_bytes, void *stream) {
-  AcceptPlan p;
-  int rc = accept_plan(sh, temperature, &p);
+namespace {
+
+// Host-side checks of an sd_accept call (shape, pointers, alignment, workspace); nothing is
+// enqueued.  Returns SD_OK with the plan filled in.
+int check_accept_call(const sd_accept_shape *sh, const void *target_logits, const void *draft_logits,
+                      const int32_t *draft_tokens, const float *uniforms, const int32_t *block_lens,
+                      const int32_t *q_offsets, float temperature, const int32_t *accept_len,
+                      const int32_t *next_token, const void *workspace, size_t workspace_bytes, AcceptPlan *p) {
+  int rc = accept_plan(sh, temperature, p);
   if (rc) return rc;
   if (sh->num_seqs == 0) return ok();
   const bool sample = temperature > 0.f;
@@ -490,8 +493,23 @@ int sd_accept(const sd_accept_shape *sh, const void *target_logits, const void *
   if (!aligned16(target_logits) || (sample && !aligned16(draft_logits)))
     return fail(SD_ERR_INVALID_ARG, "logits must be 16-byte aligned");
   if (((uintptr_t)workspace & 255u) != 0) return fail(SD_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
-  if (workspace_bytes < p.total)
-    return fail(SD_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, p.total);
+  if (workspace_bytes < p->total)
+    return fail(SD_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, p->total);
+  return ok();
+}
+
+}  // namespace
+
+int sd_accept(const sd_accept_shape *sh, const void *target_logits, const void *draft_logits,
+              const int32_t *draft_tokens, const float *uniforms, const int32_t *block_lens,
+              const int32_t *q_offsets, float temperature, int32_t *accept_len, int32_t *next_token,
+              void *workspace, size_t workspace_bytes, void *stream) {
+  AcceptPlan p;
+  int rc = check_accept_call(sh, target_logits, draft_logits, draft_tokens, uniforms, block_lens, q_offsets,
+                             temperature, accept_len, next_token, workspace, workspace_bytes, &p);
+  if (rc) return rc;
+  if (sh->num_seqs == 0) return ok();
+  const bool sample = temperature > 0.f;
 
   sdb::AcceptArgs a;
   a.target = target_logits;
@@ -669,6 +687,12 @@ int sd_verify_step(const sd_attn_shape *ash, int32_t num_layers, const sd_layer_
   int rc = sd_verify_step_workspace_size(ash, csh, temperature, &need);
   if (rc) return rc;
   if (workspace_bytes < need) return fail(SD_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
+  // the acceptance and commit arguments too, before the layers are enqueued
+  AcceptPlan cp;
+  rc = check_accept_call(csh, target_logits, draft_logits, draft_tokens, uniforms, block_lens, q_offsets, temperature,
+                         accept_len, next_token, workspace, workspace_bytes, &cp);
+  if (rc) return rc;
+  if (!ctx_lens) return fail(SD_ERR_INVALID_ARG, "sd_verify_step: ctx_lens is NULL");
   for (int l = 0; l < num_layers; ++l) {
     const sd_layer_buffers &L = layers[l];
     if (ash->dtype == SD_BF16) {  // append fused into the attention launch

@@ -119,6 +119,30 @@ def test_attn_append_call_errors_without_device():
     assert call_attn_append(good_attn_shape(total_q=0)) == L.SD_OK
 
 
+def test_verify_step_checks_everything_before_enqueueing():
+    """Bad acceptance or commit arguments are reported before any layer is enqueued: every
+    call below returns its status on the host (the fake addresses are never dereferenced)."""
+    P = ctypes.c_void_p
+    ash = good_attn_shape()
+    csh = L.SdAcceptShape(num_seqs=2, vocab=151936, total_q=20, max_block=16, dtype=L.SD_BF16)
+    layers = (L.SdLayerBuffers * 2)(*[L.SdLayerBuffers(1 << 20, 2 << 20, 3 << 20, 4 << 20, 5 << 20, 6 << 20)
+                                      for _ in range(2)])
+    n = ctypes.c_size_t(0)
+    assert L.lib().sd_verify_step_workspace_size(ctypes.byref(ash), ctypes.byref(csh), ctypes.c_float(1.0),
+                                                 ctypes.byref(n)) == L.SD_OK
+
+    def call(ctx=16, target=1 << 24, draft=2 << 24, tok=48, u=64, al=80, nt=96, T=1.0):
+        return L.lib().sd_verify_step(ctypes.byref(ash), 2, layers, P(ctx), P(32), P(112), 0, ctypes.byref(csh),
+                                      P(target), P(draft), P(tok), P(u), ctypes.c_float(T), P(al), P(nt),
+                                      P(1 << 28), n.value, None)
+    assert call(draft=0) == L.SD_ERR_INVALID_ARG          # T > 0 needs the draft logits
+    assert call(u=0) == L.SD_ERR_INVALID_ARG
+    assert call(al=0) == L.SD_ERR_INVALID_ARG
+    assert call(target=(1 << 24) + 8) == L.SD_ERR_INVALID_ARG   # misaligned logits
+    assert call(ctx=0) == L.SD_ERR_INVALID_ARG
+    assert "ctx_lens" in L.lib().sd_last_error().decode()
+
+
 def test_check_calls_errors_without_device():
     P = ctypes.c_void_p
     f = L.lib().sd_check_attn_inputs
