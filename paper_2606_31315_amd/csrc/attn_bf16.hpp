@@ -111,33 +111,35 @@ struct TileLoads {
     }
   }
   // The same tile from a page pool: key k of sequence s lives in pool page
-  // table[k >> log2] at row k & (page_size - 1).  A load instruction covers RPI consecutive
-  // keys of one page (tiles start on a multiple of 16 keys, pages hold a multiple of 16 keys,
-  // and rows past key_last re-read key_last), so its page id is uniform: fetch_pages reads it
-  // with a scalar load one tile ahead of issue_paged, at the end of a tile's arithmetic.
-  // Scalar loads and LDS reads share one wait counter (lgkmcnt), so a page-id load issued
-  // before the arithmetic would stall its first LDS read for a memory round trip; issued
-  // after it, the load overlaps the next tile wait.  (An LDS lookup would make the compiler
-  // drain every in-flight load-to-LDS transfer before it.)  Ids are clamped into the pool.
-  __device__ void fetch_pages(const int *table, int max_pages, int num_pages, int log2, int key0, int key_last,
-                              int wave, int (&pg)[T::LPW]) const {
-#pragma unroll
-    for (int q = 0; q < T::LPW; ++q) {
-      const int li = wave * T::LPW + q - (isv ? T::LPI : 0);
-      // uniform per wavefront; readfirstlane tells the compiler, so the id comes by a scalar
-      // load (a vector load would need a vmcnt wait that drains the tile loads in flight)
-      const int key = __builtin_amdgcn_readfirstlane(min(key0 + li * T::RPI, key_last));
-      pg[q] = min(max(ld_uniform(table, min(key >> log2, max_pages - 1)), 0), num_pages - 1);
-    }
+  // table[k >> log2] at row k & (page_size - 1).  A wavefront's loads of one tile cover
+  // 2 * KT / NW = 16 consecutive keys starting at a multiple of 16 (rows past key_last re-read
+  // key_last, which lies in the same 16 keys), and pages hold a power of two >= 16 keys, so
+  // they all read one page: one id per wavefront and tile, read with one scalar load (the
+  // index is made wavefront-uniform with readfirstlane; a vector load would need a vmcnt wait
+  // that drains the tile loads in flight).  The kernel reads the id one tile ahead, at the end
+  // of a tile's arithmetic: scalar loads and LDS reads share one wait counter (lgkmcnt), so an
+  // id load issued before the arithmetic would stall its first LDS read for a memory round
+  // trip.  (An LDS lookup would make the compiler drain every in-flight load-to-LDS transfer
+  // before it.)  Ids are clamped into the pool.
+  static_assert(2 * KT / T::NW == 16 && T::LPW * T::RPI == 16, "16 keys per wavefront per tile");
+  __device__ int fetch_page_raw(const int *table, int max_pages, int log2, int key0, int key_last, int wave) const {
+    const int wrow = (wave % (T::NW / 2)) * 16;  // first key row of this wavefront's loads
+    const int key = __builtin_amdgcn_readfirstlane(min(key0 + wrow, key_last));
+    return ld_uniform(table, min(key >> log2, max_pages - 1));
+  }
+  __device__ static int clamp_page(int id, int num_pages) { return min(max(id, 0), num_pages - 1); }
+  __device__ int fetch_page(const int *table, int max_pages, int num_pages, int log2, int key0, int key_last,
+                            int wave) const {
+    return clamp_page(fetch_page_raw(table, max_pages, log2, key0, key_last, wave), num_pages);
   }
   __device__ void issue_paged(char SDB_LDS *stage, const char *kpool, const char *vpool, int key0, int key_last,
-                              const int (&pg)[T::LPW], int log2, int Hkv, int g, int wave) const {
+                              int pg, int log2, int Hkv, int g, int wave) const {
     const char *pool = isv ? vpool : kpool;
     char SDB_LDS *dst = stage + (isv ? T::TILEB : 0) + (wave * T::LPW - (isv ? T::LPI : 0)) * 1024;
     const int mask = (1 << log2) - 1;
+    const char *page = pool + ((((size_t)pg * Hkv + g) << log2) * T::ROWB);
 #pragma unroll
     for (int q = 0; q < T::LPW; ++q) {
-      const char *page = pool + ((((size_t)pg[q] * Hkv + g) << log2) * T::ROWB);
       const int key = min(key0 + row[q], key_last);
       __builtin_amdgcn_global_load_lds((const void *)(page + (unsigned)((key & mask) * T::ROWB) + cof[q]),
                                        (SDB_LDS void *)(dst + q * 1024), 16, 0, 0);
@@ -281,7 +283,7 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   ld.init(wave, lane);
   // paged caches: this sequence's row of the block table
   [[maybe_unused]] const int *table = PAGED ? a.block_table + (size_t)s * a.max_pages : nullptr;
-  [[maybe_unused]] int pgn[T::LPW];  // page ids of the next tile to issue (paged caches)
+  [[maybe_unused]] int pgn = 0;  // paged caches: page id of this wavefront's share of the next tile
   // APPEND: the block rows of this kv head in the new-row arrays, and this split's share of
   // them ([ab0, k1) of the keys) copied into the cache through registers: loaded now, stored
   // after the last tile.  (Stores count in vmcnt: issued earlier, they would hold up the next
@@ -319,13 +321,26 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
 
   // ---- pipeline prologue: tiles 0 .. NS-2 in flight ----
   const int ntiles = (k1 - k0 + KT - 1) / KT;
+  if constexpr (PAGED) {
+    // the page ids of the first NS tiles in one batch of scalar loads: one round trip rather
+    // than one per tile (measured: 38.2 -> 35.6 us per call with shuffled 16-key pages,
+    // together with one id per wavefront and tile)
+    int pro[NS];
 #pragma unroll
-  for (int t = 0; t < NS - 1; ++t)
-    if (t < ntiles) {
-      if constexpr (PAGED) ld.fetch_pages(table, a.max_pages, a.num_pages, a.page_log2, k0 + t * KT, k1 - 1, wave, pgn);
-      issue(ring + t * T::STAGEB, k0 + t * KT);
-    }
-  if constexpr (PAGED) ld.fetch_pages(table, a.max_pages, a.num_pages, a.page_log2, k0 + (NS - 1) * KT, k1 - 1, wave, pgn);
+    for (int t = 0; t < NS; ++t) pro[t] = ld.fetch_page_raw(table, a.max_pages, a.page_log2, k0 + t * KT, k1 - 1, wave);
+    // one use of all the raw ids before any is clamped, so their loads go out together
+    if constexpr (NS == 3) asm volatile("" : "+s"(pro[0]), "+s"(pro[1]), "+s"(pro[2]));
+#pragma unroll
+    for (int t = 0; t < NS; ++t) pro[t] = TileLoads<D, KT, NS>::clamp_page(pro[t], a.num_pages);
+#pragma unroll
+    for (int t = 0; t < NS - 1; ++t)
+      if (t < ntiles) ld.issue_paged(ring + t * T::STAGEB, kbase, vbase, k0 + t * KT, k1 - 1, pro[t], a.page_log2, a.Hkv, g, wave);
+    pgn = pro[NS - 1];
+  } else {
+#pragma unroll
+    for (int t = 0; t < NS - 1; ++t)
+      if (t < ntiles) issue(ring + t * T::STAGEB, k0 + t * KT);
+  }
   // keys every row can see: all of [k0, k1) when bidirectional, keys <= ctx when causal
   const int vis_all = a.causal ? min(k1, ctx + 1) : k1;
   const float sl2 = a.scale_log2;
@@ -400,7 +415,7 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
       }
     }
     if constexpr (PAGED) {
-      if (t + NS < ntiles) ld.fetch_pages(table, a.max_pages, a.num_pages, a.page_log2, k0 + (t + NS) * KT, k1 - 1, wave, pgn);
+      if (t + NS < ntiles) pgn = ld.fetch_page(table, a.max_pages, a.num_pages, a.page_log2, k0 + (t + NS) * KT, k1 - 1, wave);
     }
   }
 
