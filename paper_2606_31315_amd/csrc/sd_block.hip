@@ -107,6 +107,16 @@ int attn_plan(const sd_attn_shape *sh, AttnPlan *p) {
   const int gran = (sh->dtype == SD_BF16) ? 16 : p->KT;
   long long sl = (max_L + want - 1) / want;
   sl = ((sl + gran - 1) / gran) * gran;
+  // bf16 splits longer than 2048 keys: size them for two waves at the maximum length instead.
+  // One wave of long workgroups ends with the slowest CU, and ragged lengths leave CUs idle;
+  // two or more waves let the dispatcher rebalance (16 sequences x 8 kv heads, bidirectional:
+  // contexts 1k-8k 98.7 -> 94.8 us, all at 8k 123.1 -> 109.4 us; three or more waves at the
+  // maximum length measured slower on the uniform batch, 116.5-133.0 us).
+  if (sh->dtype == SD_BF16 && sl > 2048) {
+    sl = (max_L * pairs + 2 * target_wgs - 1) / (2 * target_wgs);
+    sl = ((sl + gran - 1) / gran) * gran;
+    if (sl < 1024) sl = 1024;
+  }
   if (sl > 4096) sl = 4096;
   if (sl < p->KT) sl = p->KT;
   p->split_len = (int)sl;
