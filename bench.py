@@ -52,9 +52,15 @@ def parse():
     return ap.parse_args()
 
 
-def cpu_baseline(work, T, seconds):
+def cpu_baseline(work, T, seconds, gpu=None):
     """The fp64 oracle on the host cores, on the same step: attention for every block row and
-    head, then acceptance.  Repeated until `seconds` have elapsed (at least once)."""
+    head, then acceptance.  Repeated until `seconds` have elapsed (at least once).
+
+    With ``gpu`` = (attention output, accept_len, next_token) of the timed step on the same
+    inputs, the oracle's last results also check them under the parity rule: attention
+    max-abs within 2e-2 (bf16) or 1e-5 (fp32); accept_len and next_token equal, except that a
+    sequence whose accept test lies within 1e-5 of its threshold is counted and skipped, and a
+    final draw within 1e-5 of a CDF edge only has to fall inside the band's tokens."""
     sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
     import oracle
     a = work.attn
@@ -66,18 +72,44 @@ def cpu_baseline(work, T, seconds):
     dl = acc.draft.float().numpy() if acc.draft is not None else None
     reps, t0 = 0, time.perf_counter()
     while True:
-        oracle.block_attn(q, k, v, a.ctx_lens, a.block_lens, a.q_offsets, a.mask_mode)
-        oracle.accept(tl, dl, acc.draft_tokens, acc.uniforms, acc.block_lens, acc.q_offsets, T)
+        o_ref = oracle.block_attn(q, k, v, a.ctx_lens, a.block_lens, a.q_offsets, a.mask_mode)
+        r = oracle.accept(tl, dl, acc.draft_tokens, acc.uniforms, acc.block_lens, acc.q_offsets, T)
         reps += 1
         el = time.perf_counter() - t0
         if el >= seconds or reps >= 20:
             break
     per_step = el / reps
-    return {"value": work.verified_draft_tokens() / per_step, "unit": "verified draft tokens/s",
-            "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"the full step (attention for all {a.total_q} block rows x {a.Hq} heads + acceptance of "
-                      f"{a.S} sequences at T={T:g}), {reps} repetition(s), {per_step * 1e3:.1f} ms per step",
-            "ms_per_step": per_step * 1e3}
+    res = {"value": work.verified_draft_tokens() / per_step, "unit": "verified draft tokens/s",
+           "cores": oracle.num_threads(), "kind": "oracle",
+           "sample": f"the full step (attention for all {a.total_q} block rows x {a.Hq} heads + acceptance of "
+                     f"{a.S} sequences at T={T:g}), {reps} repetition(s), {per_step * 1e3:.1f} ms per step",
+           "ms_per_step": per_step * 1e3}
+    if gpu is not None:
+        attn_gpu, al_g, nt_g = gpu
+        err = float(np.abs(attn_gpu.astype(np.float64) - o_ref).max()) if o_ref.size else 0.0
+        tol = 2e-2 if a.dtype == "bf16" else 1e-5
+        band = 1e-5
+        compared = ties_a = ties_s = mism = 0
+        for s in range(acc.S):
+            if T > 0 and r.accept_margin[s] < band:
+                ties_a += 1
+                continue
+            compared += 1
+            ok = al_g[s] == r.accept_len[s]
+            if T == 0 or r.sample_margin[s] >= band:
+                ok = ok and nt_g[s] == r.next_token[s]
+            else:
+                ties_s += 1
+                ok = ok and r.sample_lo[s] <= nt_g[s] <= r.sample_hi[s]
+            mism += int(not ok)
+        res["parity"] = {"attn_max_abs": err, "attn_tol": tol, "attn_ok": bool(err <= tol),
+                         "accept_compared": compared, "accept_near_ties": ties_a, "sample_near_ties": ties_s,
+                         "accept_mismatches": mism,
+                         "what": "the timed step's own outputs against the oracle's on the same inputs"}
+        if err > tol or mism:
+            print(f"bench.py: parity FAILED on the timed step: attention max-abs {err:.3g} (tol {tol}), "
+                  f"{mism} acceptance mismatches", file=sys.stderr)
+    return res
 
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -464,6 +496,7 @@ def main():
     acc_gbps = acc_bytes / (acc_us * 1e-6) / 1e9
     step_gbps = step_bytes / (ms_per_step * 1e-3) / 1e9
     al_h, nt_h = al.cpu().numpy(), nt.cpu().numpy()
+    attn_h = outs[0].float().cpu().numpy()
 
     res = {
         "metric": METRIC, "value": round(value, 1), "unit": "verified draft tokens/s", "n_gpus": 1, "steps": K,
@@ -523,7 +556,7 @@ def main():
     if args.verify_layers > 0:
         res["verify_step"] = verify_step_run(torch, sd, work, T, args.verify_layers, args.verify_steps)
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(work, T, args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(work, T, args.cpu_seconds, gpu=(attn_h, al_h, nt_h))
     print(json.dumps(res), flush=True)
     return 0
 
