@@ -117,7 +117,7 @@ int attn_plan(const sd_attn_shape *sh, AttnPlan *p) {
     sl = ((sl + gran - 1) / gran) * gran;
     if (sl < 1024) sl = 1024;
   }
-  if (sl > 4096) sl = 4096;
+  if (sl > sdb::kLongSplit) sl = sdb::kLongSplit;
   if (sl < p->KT) sl = p->KT;
   p->split_len = (int)sl;
   p->max_splits = (int)((max_L + sl - 1) / sl);

@@ -156,3 +156,27 @@ def test_dense_plan_many_sequences(mode):
     device numbers the existing splits densely (a prefix sum over 64 sequences per round, two
     rounds here), with empty blocks at the round's edge; every output row compared."""
     G.check_attn(_many_sequences(7301, 100, mode, "dense_many_seqs"))
+
+
+def _long_split_sequences(seed, S, ctx_hi, mode, name):
+    """S sequences x 4 kv heads whose plan reaches the 4096-key split cap (dense numbering of
+    full splits, then the partial last splits longest first): lengths that are exact multiples
+    of the split, one key past one, empty blocks and an empty context."""
+    rs = W._streams(seed)
+    ctx = rs["ctx"].integers(1, ctx_hi, endpoint=True, size=S).astype(np.int32)
+    B = rs["B"].integers(1, 24, endpoint=True, size=S).astype(np.int32)
+    B[[1, S - 2]] = 0
+    ctx[2], B[2] = 8192 - 16, 16      # two full splits, no partial
+    ctx[5], B[5] = 4096, 1            # one full split and a one-key partial
+    ctx[7], B[7] = 0, 5               # no context
+    ctx[9], B[9] = ctx_hi - 24, 24    # the longest sequence
+    return W.make_attn(rs, S=S, Hq=8, Hkv=4, D=128, ctx_lens=ctx, block_lens=B, dtype="bf16", mask_mode=mode,
+                       name=name)
+
+
+@pytest.mark.parametrize("S,ctx_hi", [(40, 14000), (80, 12000)], ids=["ranked_S40", "seq_order_S80"])
+@pytest.mark.parametrize("mode", [CAUSAL, BIDIR])
+def test_dense_plan_long_splits(S, ctx_hi, mode):
+    """Plans at the split cap: up to 64 sequences the partial splits are ranked by length on
+    the device, beyond that they follow sequence order; every output row compared."""
+    G.check_attn(_long_split_sequences(7400 + S, S, ctx_hi, mode, f"long_splits_S{S}"))
