@@ -106,3 +106,11 @@ def test_append_dense_plan(mode):
     B[3] = max(int(B[3]), 1)
     _check(W.make_attn(rs, S=S, Hq=8, Hkv=2, D=128, ctx_lens=ctx, block_lens=B, dtype="bf16", mask_mode=mode,
                        name="append_dense"))
+
+
+@pytest.mark.parametrize("S,ctx_hi", [(40, 14000), (80, 12000)], ids=["ranked_S40", "seq_order_S80"])
+def test_append_dense_plan_long_splits(S, ctx_hi):
+    """The fused append on plans at the 4096-key split cap (full splits, then partial splits
+    longest first), including a block whose keys straddle two splits."""
+    from test_gpu_attn import _long_split_sequences
+    _check(_long_split_sequences(7600 + S, S, ctx_hi, BIDIR, f"append_long_splits_S{S}"))

@@ -107,3 +107,19 @@ def test_paged_dense_plan_many_sequences():
     got = _paged_run(p, kp, vp, table).cpu()
     ref = G.run_attn(p).cpu()
     assert torch.equal(got, ref)
+
+
+@pytest.mark.parametrize("S,ctx_hi", [(40, 14000), (80, 12000)], ids=["ranked_S40", "seq_order_S80"])
+def test_paged_dense_plan_long_splits(S, ctx_hi):
+    """Plans at the 4096-key split cap (full splits, then partial splits longest first) through
+    page pools of 64 keys: bit-identical to the contiguous kernel on the same keys."""
+    from test_gpu_attn import _long_split_sequences
+    p = _long_split_sequences(7500 + S, S, ctx_hi, CAUSAL, f"paged_long_splits_S{S}")
+    rs = W._streams(7501 + S)
+    Lp = ((p.Lmax + 63) // 64) * 64
+    k = torch.nn.functional.pad(p.k_cache, (0, 0, 0, Lp - p.Lmax), value=float("nan"))
+    v = torch.nn.functional.pad(p.v_cache, (0, 0, 0, Lp - p.Lmax), value=float("nan"))
+    kp, vp, table = W.paginate(rs, k, v, 64)
+    got = _paged_run(p, kp, vp, table).cpu()
+    ref = G.run_attn(p).cpu()
+    assert torch.equal(got, ref)
