@@ -64,6 +64,7 @@ class AcceptResult:
     sample_margin: np.ndarray
     sample_lo: np.ndarray
     sample_hi: np.ndarray
+    sample_tie_p: np.ndarray
 
 
 class Oracle:
@@ -77,7 +78,7 @@ class Oracle:
             ctypes.c_int, ctypes.c_double, ctypes.c_long, P, P, P]
         lib.oracle_accept.restype = ctypes.c_int
         lib.oracle_accept.argtypes = [ctypes.c_int, ctypes.c_int, P, P, P, P, P, P,
-                                      ctypes.c_double, ctypes.c_double, P, P, P, P, P, P]
+                                      ctypes.c_double, ctypes.c_double, P, P, P, P, P, P, P]
         lib.oracle_num_threads.restype = ctypes.c_int
         lib.oracle_set_threads.argtypes = [ctypes.c_int]
         self.lib = lib
@@ -138,11 +139,12 @@ class Oracle:
         sm = np.zeros(S, dtype=np.float64)
         lo = np.zeros(S, dtype=np.int32)
         hi = np.zeros(S, dtype=np.int32)
+        tp = np.zeros(S, dtype=np.float64)
         rc = self.lib.oracle_accept(S, V, _p(t), _p(d), _p(tok), _p(u), _p(bl), _p(off), float(temperature),
-                                   float(band), _p(al), _p(nt), _p(am), _p(sm), _p(lo), _p(hi))
+                                   float(band), _p(al), _p(nt), _p(am), _p(sm), _p(lo), _p(hi), _p(tp))
         if rc != 0:
             raise ValueError("oracle_accept: bad arguments")
-        return AcceptResult(al, nt, am, sm, lo, hi)
+        return AcceptResult(al, nt, am, sm, lo, hi, tp)
 
 
 _default = None

@@ -210,12 +210,16 @@ static int inverse_cdf(const double *r, int V, double target) {
  *   accept_margin  min over the tested positions of |u_i - min(1, rho_i)| (+inf at T = 0 or none)
  *   sample_margin  distance of u*S to the nearer edge of the chosen token's CDF interval, over S
  *   sample_lo/hi   tokens an inverse-CDF draw picks at (u* -/+ band)*S, clamped into [0, S]
+ *   sample_tie_p   probability, over a uniform u*, that the final draw lands within band*S of
+ *                  an edge of its token's interval: sum over x of min(r(x)/S, 2 band); the
+ *                  expected rate of final-draw near-ties (0 at T = 0)
  * Block length 0 yields accept_len 0, next_token -1.
  */
 int oracle_accept(int S, int V, const float *target, const float *draft, const int *draft_tokens,
                   const float *uniforms, const int *block_lens, const int *q_offsets,
                   double temperature, double band, int *accept_len, int *next_token,
-                  double *accept_margin, double *sample_margin, int *sample_lo, int *sample_hi) {
+                  double *accept_margin, double *sample_margin, int *sample_lo, int *sample_hi,
+                  double *sample_tie_p) {
   if (S < 0 || V <= 0 || !(temperature >= 0) || isinf(temperature)) return -1;
   int bad = 0;
 #pragma omp parallel
@@ -230,6 +234,7 @@ int oracle_accept(int S, int V, const float *target, const float *draft, const i
       const long doff = off - s;
       accept_margin[s] = INFINITY;
       sample_margin[s] = INFINITY;
+      sample_tie_p[s] = 0.0;
       if (B <= 0) {
         accept_len[s] = 0;
         next_token[s] = -1;
@@ -292,6 +297,14 @@ int oracle_accept(int S, int V, const float *target, const float *draft, const i
       if (hi_t > tot) hi_t = tot;
       sample_lo[s] = inverse_cdf(r, V, lo_t);
       sample_hi[s] = inverse_cdf(r, V, hi_t);
+      /* Token x owns [below_x, below_x + r(x)) of [0, S); the near-tie part of it is the
+       * band*S next to each edge, or all of it when the interval is narrower than 2 band S. */
+      double ptie = 0.0;
+      for (int v = 0; v < V; ++v) {
+        const double w = r[v] / tot;
+        ptie += w < 2.0 * band ? w : 2.0 * band;
+      }
+      sample_tie_p[s] = ptie;
     }
     free(p);
     free(qd);

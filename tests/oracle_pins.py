@@ -362,6 +362,141 @@ def pin_sampling_temperature(orc):
         assert (a.next_token[ok] == b.next_token[ok]).all()
 
 
+# Rows with exactly known distributions: logits of 0 and -inf give probabilities that are
+# exact binary fractions (1/4, 1/2, 1/8), so every margin, interval edge and band below is
+# a hand-computed number, not a re-evaluation of the oracle's formulas.
+NEG = np.float32(-np.inf)
+
+
+def _quarter_row(V=4):
+    """Target row with p = 1/4 on tokens 0..3 and 0 elsewhere."""
+    t = np.full(V, NEG, dtype=np.float32)
+    t[:4] = 0.0
+    return t
+
+
+def _half_row(V=4):
+    """Draft row with q = 1/2 on tokens 0 and 1 and 0 elsewhere."""
+    d = np.full(V, NEG, dtype=np.float32)
+    d[:2] = 0.0
+    return d
+
+
+def pin_accept_margin(orc):
+    """The accept near-tie margin is |u - min(1, rho)| at the tested positions only (the
+    parity rule's band, exempting positions whose test the rounding could flip).
+
+    p = (1/4,1/4,1/4,1/4), q = (1/2,1/2,0,0) and a draft of token 0 give rho = 1/2 exactly;
+    q = 1/8 everywhere with the same p gives rho = 2, whose accept probability min(1, rho)
+    is 1.  Expected margins are the hand-computed distances of the chosen fp32 uniforms."""
+    t, d = _quarter_row(), _half_row()
+    off = _offsets([2])
+    tok = np.array([0], np.int32)
+    # rho = 1/2, u just above: rejected, margin 2^-15 (outside the 1e-5 band)
+    r = orc.accept(np.stack([t, t]), d[None], tok, np.array([0.5 + 2 ** -15, 0.3], np.float32), [2], off, 1.0)
+    assert r.accept_len[0] == 0 and r.accept_margin[0] == 2.0 ** -15, (r.accept_len, r.accept_margin)
+    # rho = 1/2, u just below: accepted, margin 2^-18 (a near-tie inside the band)
+    r = orc.accept(np.stack([t, t]), d[None], tok, np.array([0.5 - 2 ** -18, 0.3], np.float32), [2], off, 1.0)
+    assert r.accept_len[0] == 1 and r.accept_margin[0] == 2.0 ** -18, (r.accept_len, r.accept_margin)
+    # rho = 2: accept probability 1, margin 1 - u = 2^-17, not |u - rho|
+    t8 = _quarter_row(8)
+    d8 = np.zeros(8, np.float32)
+    r = orc.accept(np.stack([t8, t8]), d8[None], np.array([1], np.int32),
+                   np.array([1 - 2 ** -17, 0.3], np.float32), [2], off, 1.0)
+    assert r.accept_len[0] == 1 and r.accept_margin[0] == 2.0 ** -17, (r.accept_len, r.accept_margin)
+    # three drafts, rho = 1/2 each: position 0 accepted at margin 2^-13, position 1 rejected at
+    # margin 0.4 - 0.5 in fp32, position 2 untested (its margin 2^-20 must not count): the margin
+    # is the minimum over the tested positions, 2^-13
+    u = np.array([0.5 - 2 ** -13, 0.9, 0.5 + 2 ** -20, 0.3], np.float32)
+    r = orc.accept(np.stack([t] * 4), np.stack([d] * 3), np.zeros(3, np.int32), u, [4], _offsets([4]), 1.0)
+    assert r.accept_len[0] == 1 and r.accept_margin[0] == 2.0 ** -13, (r.accept_len, r.accept_margin)
+    # no tested position (B = 1) and greedy acceptance: no accept margin
+    r = orc.accept(t[None], np.zeros((1, 4), np.float32), np.zeros(0, np.int32), np.array([0.5], np.float32),
+                   [1], _offsets([1]), 1.0)
+    assert r.accept_margin[0] == np.inf
+    r = orc.accept(np.stack([t, t]), None, tok, None, [2], off, 0.0)
+    assert r.accept_margin[0] == np.inf and r.sample_margin[0] == np.inf and r.sample_tie_p[0] == 0.0
+    assert r.sample_lo[0] == r.sample_hi[0] == r.next_token[0]
+
+
+# (u*, token, margin, band low token, band high token) for a final draw from the bonus row
+# p = (1/4,1/4,1/4,1/4): interval edges at 0, 1/4, 1/2, 3/4, 1; band 1e-5
+_BONUS_CASES = [
+    (0.5 + 2 ** -20, 2, 2.0 ** -20, 1, 2),   # just past the edge at 1/2
+    (0.5, 2, 0.0, 1, 2),                     # exactly on an edge: the upper token, margin 0
+    (0.375, 1, 0.125, 1, 1),                 # mid-interval
+    (0.0, 0, 0.0, 0, 0),                     # the bottom edge; the band clamps at 0
+    (0.25 - 2 ** -21, 0, 2.0 ** -21, 0, 1),  # just below the edge at 1/4
+    (1 - 2 ** -24, 3, 2.0 ** -24, 3, 3),     # top: the band clamps at S, whose draw is the last token
+]
+# the same for the residual max(0, p - q) = (0, 0, 1/4, 1/4) of q = (1/2,1/2,0,0), S = 1/2:
+# edges at 0 (tokens 0 and 1 have no mass), 1/4 and 1/2 of S = relative 0, 1/2, 1
+_RESIDUAL_CASES = [
+    (0.5 + 2 ** -16, 3, 2.0 ** -16, 3, 3),   # margin 2^-17 absolute is 2^-16 of S; band = 1e-5 S
+    (0.5 - 2 ** -18, 2, 2.0 ** -18, 2, 3),
+    (0.25, 2, 0.25, 2, 2),
+    (0.0, 2, 0.0, 2, 2),                     # the first token with mass, not token 0
+]
+
+
+def pin_sample_margin_band(orc):
+    """The final draw's near-tie margin (distance of u* S to the chosen token's interval
+    edges, relative to S) and the band of tokens reachable from (u* -/+ 1e-5) S, on
+    distributions whose cumulative masses are exact binary fractions."""
+    t, d = _quarter_row(), _half_row()
+    for ustar, x, m, lo, hi in _BONUS_CASES:
+        r = orc.accept(t[None], np.zeros((1, 4), np.float32), np.zeros(0, np.int32), np.array([ustar], np.float32),
+                       [1], _offsets([1]), 1.0, band=1e-5)
+        got = (int(r.next_token[0]), float(r.sample_margin[0]), int(r.sample_lo[0]), int(r.sample_hi[0]))
+        assert got[0] == x and abs(got[1] - m) <= 1e-15 and got[2:] == (lo, hi), ("bonus", ustar, got)
+    for ustar, x, m, lo, hi in _RESIDUAL_CASES:
+        # draft token 0, u_0 = 0.75 >= rho = 1/2: rejected at position 0, residual draw
+        r = orc.accept(np.stack([t, t]), d[None], np.array([0], np.int32), np.array([0.75, ustar], np.float32),
+                       [2], _offsets([2]), 1.0, band=1e-5)
+        got = (int(r.next_token[0]), float(r.sample_margin[0]), int(r.sample_lo[0]), int(r.sample_hi[0]))
+        assert r.accept_len[0] == 0, "draft must be rejected"
+        assert got[0] == x and abs(got[1] - m) <= 1e-15 and got[2:] == (lo, hi), ("residual", ustar, got)
+
+
+def pin_sample_tie_probability(orc):
+    """The reported near-tie probability of the final draw: hand values on exact
+    distributions (each token of p = 1/4 contributes twice the band; tokens without mass
+    nothing; a token narrower than twice the band all of its mass), then the frequency of
+    sample_margin < band over many uniform u* on a row with wide and narrow tokens, which
+    ties the probability to the margin it predicts."""
+    t, d = _quarter_row(), _half_row()
+    one = _offsets([1])
+    r = orc.accept(t[None], np.zeros((1, 4), np.float32), np.zeros(0, np.int32), np.array([0.3], np.float32),
+                   [1], one, 1.0, band=1e-5)
+    assert abs(r.sample_tie_p[0] - 8e-5) < 1e-18, r.sample_tie_p
+    r = orc.accept(np.stack([t, t]), d[None], np.array([0], np.int32), np.array([0.75, 0.3], np.float32),
+                   [2], _offsets([2]), 1.0, band=1e-5)
+    assert abs(r.sample_tie_p[0] - 4e-5) < 1e-18, r.sample_tie_p
+    # p = (1/2, 1/4, 1/8, 1/16, 1/16) from logits 0, -ln2, -2ln2, ... is not exact in fp32;
+    # use -inf padding instead: masses 1/2 and 1/2 over tokens 0, 1 with band 0.3 -> each
+    # interval (width 1/2) is narrower than 2 band = 0.6, so the probability is 1
+    two = np.full(6, NEG, np.float32)
+    two[:2] = 0.0
+    r = orc.accept(two[None], np.zeros((1, 6), np.float32), np.zeros(0, np.int32), np.array([0.3], np.float32),
+                   [1], one, 1.0, band=0.3)
+    assert abs(r.sample_tie_p[0] - 1.0) < 1e-15, r.sample_tie_p
+    # frequency check: one token with almost all mass and 40 narrow ones
+    rng = np.random.default_rng(29)
+    V, N, band = 41, 40_000, 0.01
+    row = np.full(V, -4.0, np.float32)
+    row[0] = 0.0
+    u = rng.random(N, dtype=np.float32)
+    r = orc.accept(np.tile(row, (N, 1)), np.zeros((1, V), np.float32), np.zeros(0, np.int32), u,
+                   np.ones(N, np.int32), _offsets(np.ones(N, np.int32)), 1.0, band=band)
+    p = float(r.sample_tie_p[0])
+    assert np.allclose(r.sample_tie_p, p)
+    w = _softmax(row)
+    assert w[1] < 2 * band < w[0]  # the row has both kinds of interval
+    freq = float((r.sample_margin < band).mean())
+    se = np.sqrt(p * (1 - p) / N)
+    assert abs(freq - p) < 4 * se, (freq, p, se)
+
+
 def _lossless_trials(orc, N, seed):
     """N independent steps over one fixed block: B=4 (3 drafts), V=16.  Draft tokens are
     drawn from q_j, uniforms iid U[0,1)."""
@@ -440,7 +575,8 @@ def pin_geometric_form(orc, N=100_000):
 
 ACCEPT_PINS = [pin_greedy_numpy_prefix, pin_greedy_constructed, pin_greedy_ties_lowest,
                pin_sampling_identical_rows, pin_sampling_residual, pin_sampling_u_zero,
-               pin_sampling_temperature, pin_lossless_chi2, pin_expected_accept_len, pin_geometric_form]
+               pin_sampling_temperature, pin_accept_margin, pin_sample_margin_band, pin_sample_tie_probability,
+               pin_lossless_chi2, pin_expected_accept_len, pin_geometric_form]
 
 ALL_PINS = ATTN_PINS + ACCEPT_PINS
 

@@ -37,6 +37,24 @@ MUTANTS = {
                            "const double ustar = (double)uniforms[off + a];"),
     "greedy_next_row_shift": ("next_token[s] = argmax_lowest(target + (size_t)(off + a) * V, V);",
                               "next_token[s] = argmax_lowest(target + (size_t)(off + (a ? a - 1 : 0)) * V, V);"),
+    # the parity harness's near-tie outputs
+    "accept_margin_rho_unclamped": ("fabs(u - (rho < 1.0 ? rho : 1.0))", "fabs(u - rho)"),
+    "accept_margin_last_tested": ("if (m < accept_margin[s]) accept_margin[s] = m;", "accept_margin[s] = m;"),
+    "accept_margin_untested_too": ("if (!(u < rho)) break; /* R7 */",
+                                   "if (!(u < rho)) { for (int k = a + 1; k < n; ++k) { const double uk = "
+                                   "(double)uniforms[off + k]; if (fabs(uk - 0.5) < accept_margin[s]) "
+                                   "accept_margin[s] = fabs(uk - 0.5); } break; }"),
+    "sample_margin_zero": ("sample_margin[s] = m1 < m2 ? m1 : m2;", "sample_margin[s] = 0;"),
+    "sample_margin_unscaled": ("double m1 = (tgt - below) / tot, m2 = (below + r[x] - tgt) / tot;",
+                               "double m1 = (tgt - below), m2 = (below + r[x] - tgt);"),
+    "sample_margin_far_edge": ("sample_margin[s] = m1 < m2 ? m1 : m2;", "sample_margin[s] = m1 > m2 ? m1 : m2;"),
+    "band_whole_vocab": ("double lo_t = tgt - band * tot, hi_t = tgt + band * tot;", "double lo_t = 0, hi_t = tot;"),
+    "band_unscaled": ("double lo_t = tgt - band * tot, hi_t = tgt + band * tot;",
+                      "double lo_t = tgt - band, hi_t = tgt + band;"),
+    "band_whole_and_margin_zero": ("double lo_t = tgt - band * tot, hi_t = tgt + band * tot;\n",
+                                   "double lo_t = 0, hi_t = tot; m1 = m2 = 0; sample_margin[s] = 0;\n"),
+    "tie_p_band_only": ("ptie += w < 2.0 * band ? w : 2.0 * band;", "ptie += w > 0 ? 2.0 * band : 0.0;"),
+    "tie_p_mass_only": ("ptie += w < 2.0 * band ? w : 2.0 * band;", "ptie += w;"),
 }
 
 _RUNNER = r"""

@@ -77,7 +77,8 @@ def _run_all(orc, store):
     for case in ACCEPT_CASES:
         x = _accept_inputs(case)
         r = orc.accept(x["target"], x["draft"], x["tokens"], x["uniforms"], x["block_lens"], x["q_offsets"], x["T"])
-        for f in ("accept_len", "next_token", "accept_margin", "sample_margin", "sample_lo", "sample_hi"):
+        for f in ("accept_len", "next_token", "accept_margin", "sample_margin", "sample_lo", "sample_hi",
+                  "sample_tie_p"):
             store[f"{case[0]}_{f}"] = getattr(r, f)
 
 
