@@ -139,6 +139,23 @@ def _dtype_code(t: torch.Tensor) -> int:
     raise TypeError(f"unsupported dtype {t.dtype}; use bfloat16 or float32")
 
 
+def _shape(t: Optional[torch.Tensor], name: str, *dims) -> None:
+    """t must have len(dims) dimensions; an int entry must equal that size, None is free.
+    Checked before any pointer reaches the library: a wrongly sized buffer would make the
+    kernels read or write outside it."""
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dim() != len(dims) or any(d is not None and t.shape[i] != d for i, d in enumerate(dims)):
+        want = "[" + ", ".join("*" if d is None else str(d) for d in dims) + "]"
+        raise ValueError(f"{name} has shape {list(t.shape)}, expected {want}")
+
+
+def _lens_shapes(S: int, **named) -> None:
+    """Per-sequence int32 arrays: q_offsets has S + 1 entries, the others S."""
+    for name, t in named.items():
+        _shape(t, name, S + 1 if name == "q_offsets" else S)
+
+
 def _need(t: torch.Tensor, name: str, dtype=None, device=None):
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch.Tensor")
@@ -192,6 +209,13 @@ def block_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, ct
     """Block attention (sd_block_attn).  q [total_q, Hq, D]; caches [S, Hkv, Lmax, D];
     ctx_lens, block_lens [S] and q_offsets [S+1] int32 on the device; max_ctx and
     max_block are host-known bounds of the device lengths."""
+    _shape(k_cache, "k_cache", None, None, None, None)
+    S, Hkv, Lmax, D = k_cache.shape
+    _shape(q, "q", None, None, D)
+    _shape(v_cache, "v_cache", S, Hkv, Lmax, D)
+    _lens_shapes(S, ctx_lens=ctx_lens, block_lens=block_lens, q_offsets=q_offsets)
+    if out is not None:
+        _shape(out, "out", *q.shape)
     dev = q.device
     _need(q, "q", device=dev)
     _need(k_cache, "k_cache", q.dtype, dev)
@@ -218,6 +242,15 @@ def block_attn_append(q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
                       stream=None) -> torch.Tensor:
     """Block attention with the block's keys/values read from k_new, v_new [total_q, Hkv, D] and
     written into the caches by the same launch (sd_block_attn_append); bf16."""
+    _shape(k_cache, "k_cache", None, None, None, None)
+    S, Hkv, Lmax, D = k_cache.shape
+    _shape(q, "q", None, None, D)
+    _shape(v_cache, "v_cache", S, Hkv, Lmax, D)
+    _shape(k_new, "k_new", q.shape[0], Hkv, D)
+    _shape(v_new, "v_new", q.shape[0], Hkv, D)
+    _lens_shapes(S, ctx_lens=ctx_lens, block_lens=block_lens, q_offsets=q_offsets)
+    if out is not None:
+        _shape(out, "out", *q.shape)
     dev = q.device
     _need(q, "q", torch.bfloat16, dev)
     for name, t in (("k_new", k_new), ("v_new", v_new), ("k_cache", k_cache), ("v_cache", v_cache)):
@@ -244,6 +277,13 @@ def block_attn_paged(q: torch.Tensor, k_pages: torch.Tensor, v_pages: torch.Tens
                      workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """Block attention over paged caches (sd_block_attn_paged).  k_pages, v_pages
     [num_pages, Hkv, page_size, D] bf16; block_table [S, max_pages] int32 on the device."""
+    _shape(k_pages, "k_pages", None, None, None, None)
+    _shape(v_pages, "v_pages", *k_pages.shape)
+    _shape(q, "q", None, None, k_pages.shape[3])
+    _shape(block_table, "block_table", None, None)
+    _lens_shapes(block_table.shape[0], ctx_lens=ctx_lens, block_lens=block_lens, q_offsets=q_offsets)
+    if out is not None:
+        _shape(out, "out", *q.shape)
     dev = q.device
     _need(q, "q", torch.bfloat16, dev)
     _need(k_pages, "k_pages", torch.bfloat16, dev)
@@ -271,6 +311,12 @@ def block_attn_paged(q: torch.Tensor, k_pages: torch.Tensor, v_pages: torch.Tens
 def kv_append_paged(k_new: torch.Tensor, v_new: torch.Tensor, k_pages: torch.Tensor, v_pages: torch.Tensor,
                     block_table: torch.Tensor, ctx_lens: torch.Tensor, q_offsets: torch.Tensor, stream=None) -> None:
     """sd_kv_append into page pools [num_pages, Hkv, page_size, D] through block_table [S, max_pages]."""
+    _shape(k_pages, "k_pages", None, None, None, None)
+    _shape(v_pages, "v_pages", *k_pages.shape)
+    _shape(k_new, "k_new", None, k_pages.shape[1], k_pages.shape[3])
+    _shape(v_new, "v_new", *k_new.shape)
+    _shape(block_table, "block_table", None, None)
+    _lens_shapes(block_table.shape[0], ctx_lens=ctx_lens, q_offsets=q_offsets)
     dev = k_new.device
     _need(k_new, "k_new", device=dev)
     _need(v_new, "v_new", k_new.dtype, dev)
@@ -302,9 +348,22 @@ def accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor], dr
            *, max_block: int, accept_len: Optional[torch.Tensor] = None, next_token: Optional[torch.Tensor] = None,
            workspace: Optional[torch.Tensor] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
     """Speculative acceptance (sd_accept).  Returns device int32 (accept_len[S], next_token[S])."""
+    _shape(block_lens, "block_lens", None)
+    S = block_lens.shape[0]
+    _shape(target_logits, "target_logits", None, None)
+    total_q, V = target_logits.shape
+    _lens_shapes(S, q_offsets=q_offsets)
+    _shape(draft_tokens, "draft_tokens", None)
+    if draft_tokens.shape[0] < total_q - S:
+        raise ValueError(f"draft_tokens has {draft_tokens.shape[0]} entries, needs total_q - S = {total_q - S}")
+    if temperature > 0:
+        _shape(draft_logits, "draft_logits", total_q - S, V)
+        _shape(uniforms, "uniforms", total_q)
+    for name, t in (("accept_len", accept_len), ("next_token", next_token)):
+        if t is not None:
+            _shape(t, name, S)
     dev = target_logits.device
     _need(target_logits, "target_logits", device=dev)
-    S = block_lens.shape[0]
     if temperature > 0:
         _need(draft_logits, "draft_logits", target_logits.dtype, dev)
         _need(uniforms, "uniforms", torch.float32, dev)
@@ -331,6 +390,10 @@ def check_attn_inputs(ctx_lens: torch.Tensor, block_lens: torch.Tensor, q_offset
                       stream=None) -> torch.Tensor:
     """sd_check_attn_inputs: device int32 [3] = (OR of SD_CHECK_* bits, first offending
     sequence or -1, number of offending sequences)."""
+    _shape(block_lens, "block_lens", None)
+    _lens_shapes(block_lens.shape[0], ctx_lens=ctx_lens, q_offsets=q_offsets)
+    if status is not None:
+        _shape(status, "status", 3)
     dev = block_lens.device
     for name, t in (("ctx_lens", ctx_lens), ("block_lens", block_lens), ("q_offsets", q_offsets)):
         _need(t, name, torch.int32, dev)
@@ -349,6 +412,16 @@ def check_accept_inputs(draft_tokens: torch.Tensor, uniforms: Optional[torch.Ten
                         q_offsets: torch.Tensor, temperature: float, *, vocab: int, total_q: int, max_block: int,
                         status: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """sd_check_accept_inputs: device int32 [3], as check_attn_inputs."""
+    _shape(block_lens, "block_lens", None)
+    S = block_lens.shape[0]
+    _lens_shapes(S, q_offsets=q_offsets)
+    _shape(draft_tokens, "draft_tokens", None)
+    if draft_tokens.shape[0] < total_q - S:
+        raise ValueError(f"draft_tokens has {draft_tokens.shape[0]} entries, needs total_q - S = {total_q - S}")
+    if temperature > 0:
+        _shape(uniforms, "uniforms", total_q)
+    if status is not None:
+        _shape(status, "status", 3)
     dev = block_lens.device
     for name, t in (("draft_tokens", draft_tokens), ("block_lens", block_lens), ("q_offsets", q_offsets)):
         _need(t, name, torch.int32, dev)
@@ -369,6 +442,12 @@ def kv_append(k_new: torch.Tensor, v_new: torch.Tensor, k_cache: torch.Tensor, v
               ctx_lens: torch.Tensor, q_offsets: torch.Tensor, stream=None) -> None:
     """Write the block's keys and values into the caches at rows [ctx_s, ctx_s + B_s) (sd_kv_append).
     k_new, v_new [total_q, Hkv, D]; caches [S, Hkv, Lmax, D]; ctx_lens [S], q_offsets [S+1] int32."""
+    _shape(k_cache, "k_cache", None, None, None, None)
+    S, Hkv, Lmax, D = k_cache.shape
+    _shape(v_cache, "v_cache", S, Hkv, Lmax, D)
+    _shape(k_new, "k_new", None, Hkv, D)
+    _shape(v_new, "v_new", *k_new.shape)
+    _lens_shapes(S, ctx_lens=ctx_lens, q_offsets=q_offsets)
     dev = k_new.device
     _need(k_new, "k_new", device=dev)
     _need(v_new, "v_new", k_new.dtype, dev)
@@ -384,6 +463,8 @@ def kv_append(k_new: torch.Tensor, v_new: torch.Tensor, k_cache: torch.Tensor, v
 
 def commit(accept_len: torch.Tensor, ctx_lens: torch.Tensor, stream=None) -> None:
     """ctx_lens += accept_len + 1 on the device (sd_commit)."""
+    _shape(ctx_lens, "ctx_lens", None)
+    _shape(accept_len, "accept_len", ctx_lens.shape[0])
     _need(accept_len, "accept_len", torch.int32)
     _need(ctx_lens, "ctx_lens", torch.int32, accept_len.device)
     _check(lib().sd_commit(int(ctx_lens.shape[0]), _ptr(accept_len), _ptr(ctx_lens), _stream(stream)))
@@ -400,6 +481,29 @@ def verify_step(layers, ctx_lens: torch.Tensor, block_lens: torch.Tensor, q_offs
     if len(layers) < 1:
         raise ValueError("at least one layer")
     l0 = layers[0]
+    _shape(l0["k_cache"], "layers[0].k_cache", None, None, None, None)
+    S, Hkv, Lmax, D = l0["k_cache"].shape
+    _shape(l0["q"], "layers[0].q", None, None, D)
+    total_q, Hq = l0["q"].shape[0], l0["q"].shape[1]
+    for i, L_ in enumerate(layers):
+        _shape(L_["q"], f"layers[{i}].q", total_q, Hq, D)
+        _shape(L_["out"], f"layers[{i}].out", total_q, Hq, D)
+        for key in ("k_new", "v_new"):
+            _shape(L_[key], f"layers[{i}].{key}", total_q, Hkv, D)
+        for key in ("k_cache", "v_cache"):
+            _shape(L_[key], f"layers[{i}].{key}", S, Hkv, Lmax, D)
+    _lens_shapes(S, ctx_lens=ctx_lens, block_lens=block_lens, q_offsets=q_offsets)
+    _shape(target_logits, "target_logits", total_q, None)
+    V = target_logits.shape[1]
+    _shape(draft_tokens, "draft_tokens", None)
+    if draft_tokens.shape[0] < total_q - S:
+        raise ValueError(f"draft_tokens has {draft_tokens.shape[0]} entries, needs total_q - S = {total_q - S}")
+    if temperature > 0:
+        _shape(draft_logits, "draft_logits", total_q - S, V)
+        _shape(uniforms, "uniforms", total_q)
+    for name, t in (("accept_len", accept_len), ("next_token", next_token)):
+        if t is not None:
+            _shape(t, name, S)
     dev = l0["q"].device
     for i, L_ in enumerate(layers):
         _need(L_["q"], f"layers[{i}].q", l0["q"].dtype, dev)
@@ -446,6 +550,20 @@ def block_size_policy(last_logits: torch.Tensor, w1: torch.Tensor, b1: torch.Ten
                       workspace: Optional[torch.Tensor] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
     """Block-size policy (sd_block_size_policy): last-token logits [P, V] -> (scores [P, 2k+1] fp32,
     block sizes [P] int32).  Weights bf16 [out, in], biases fp32; 2k+1 = w3.shape[0]."""
+    _shape(last_logits, "last_logits", None, None)
+    P, V = last_logits.shape
+    _shape(w1, "w1", None, V)
+    H = w1.shape[0]
+    _shape(b1, "b1", H)
+    _shape(w2, "w2", H, H)
+    _shape(b2, "b2", H)
+    _shape(w3, "w3", None, H)
+    C = w3.shape[0]
+    _shape(b3, "b3", C)
+    if scores is not None:
+        _shape(scores, "scores", P, C)
+    if block_size is not None:
+        _shape(block_size, "block_size", P)
     dev = last_logits.device
     _need(last_logits, "last_logits", device=dev)
     for name, t in (("w1", w1), ("w2", w2), ("w3", w3)):
@@ -484,6 +602,9 @@ def survival_tau(gamma: torch.Tensor, cands, train_block: int, alpha: float, b_h
                  *, lipschitz: bool = True, stream=None):
     """Prefix-survival model (sd_survival_tau): gamma [N, P] fp32 -> (tau [N, C] fp64, B* [N] int32,
     regret [N] fp64 or None, L_tau [N] fp64 or None)."""
+    _shape(gamma, "gamma", None, None)
+    if b_hat is not None:
+        _shape(b_hat, "b_hat", gamma.shape[0])
     dev = gamma.device
     _need(gamma, "gamma", torch.float32)
     if b_hat is not None:
@@ -503,6 +624,7 @@ def survival_sample(gamma: torch.Tensor, cands, train_block: int, alpha: float, 
                     hist: bool = True, stream=None):
     """Monte Carlo of the accepted length (sd_survival_sample): -> (mean [N, C] fp64,
     histogram [N, C, P + 1] int32 or None)."""
+    _shape(gamma, "gamma", None, None)
     dev = gamma.device
     _need(gamma, "gamma", torch.float32)
     shape = survival_shape(gamma, cands, train_block, alpha)
