@@ -108,7 +108,7 @@ def test_attn_many_sequences_random_faults():
 
 
 def test_attn_no_sequences():
-    assert run_attn_check(np.zeros(1, np.int32), np.zeros(1, np.int32)[:0], np.zeros(1, np.int32), 0, 10, 4) == \
+    assert run_attn_check(np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(1, np.int32), 0, 10, 4) == \
         [0, -1, 0]
 
 
