@@ -199,6 +199,29 @@ int sd_accept(const sd_accept_shape *shape, const void *target_logits, const voi
               const int32_t *q_offsets, float temperature, int32_t *accept_len, int32_t *next_token,
               void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * sd_accept without a workspace argument, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).  The
+ * arguments, the kernels and the results are those of sd_accept; the scratch space is a fixed
+ * array of SD_ACCEPT_NOALLOC_SCRATCH_BYTES in device memory that the library holds on each
+ * device it runs on until the process ends.  Its address is looked up once per device, on the
+ * first call made with that device current.  The call allocates nothing, and its scratch
+ * needs no clearing (every byte a kernel reads was written earlier in the same call).
+ *
+ * Every call on one device shares that device's array: two calls that may run at the same
+ * time on one device (different streams, or different host threads without ordering) race on
+ * it and give undefined results.  Order them on one stream, or use sd_accept with a workspace
+ * each.
+ * Errors: as sd_accept; SD_ERR_WORKSPACE when the shape needs more scratch than the array holds
+ * (sd_accept_workspace_size reports the need; about 2 * S * max_block * ceil(V / 16384) * 16
+ * bytes at T > 0 with bf16 logits), SD_ERR_HIP if the array's address cannot be found.
+ */
+#define SD_ACCEPT_NOALLOC_SCRATCH_BYTES ((size_t)4 << 20)
+int sd_accept_noalloc(const sd_accept_shape *shape, const void *target_logits, const void *draft_logits,
+                      const int32_t *draft_tokens, const float *uniforms, const int32_t *block_lens,
+                      const int32_t *q_offsets, float temperature, int32_t *accept_len, int32_t *next_token,
+                      void *stream);
+
 /* ==========================================================================
  * Checks of the per-sequence values the calls above read from device memory and take on
  * trust.  For tests and debugging, not for the hot path: one small launch files an error

@@ -22,7 +22,10 @@ EXPORTS = ["sd_last_error", "sd_version", "sd_block_attn_workspace_size", "sd_bl
            "sd_accept_workspace_size", "sd_accept", "sd_kv_append", "sd_commit", "sd_verify_step_workspace_size",
            "sd_verify_step", "sd_policy_workspace_size", "sd_block_size_policy", "sd_block_attn_paged",
            "sd_kv_append_paged", "sd_survival_tau", "sd_survival_sample", "sd_block_attn_append",
-           "sd_check_attn_inputs", "sd_check_accept_inputs"]
+           "sd_check_attn_inputs", "sd_check_accept_inputs", "sd_accept_noalloc"]
+
+# bytes of the fixed device scratch behind sd_accept_noalloc (SD_ACCEPT_NOALLOC_SCRATCH_BYTES)
+ACCEPT_NOALLOC_SCRATCH_BYTES = 4 << 20
 
 SD_CHECK_CTX, SD_CHECK_BLOCK, SD_CHECK_OFFSETS, SD_CHECK_TOKEN, SD_CHECK_UNIFORM = 1, 2, 4, 8, 16
 
@@ -84,6 +87,8 @@ def lib() -> ctypes.CDLL:
         L.sd_accept_workspace_size.argtypes = [ctypes.POINTER(SdAcceptShape), ctypes.c_float, ctypes.POINTER(Z)]
         L.sd_accept.restype = ctypes.c_int
         L.sd_accept.argtypes = [ctypes.POINTER(SdAcceptShape), P, P, P, P, P, P, ctypes.c_float, P, P, P, Z, P]
+        L.sd_accept_noalloc.restype = ctypes.c_int
+        L.sd_accept_noalloc.argtypes = [ctypes.POINTER(SdAcceptShape), P, P, P, P, P, P, ctypes.c_float, P, P, P]
         L.sd_block_attn_paged.restype = ctypes.c_int
         L.sd_block_attn_paged.argtypes = [ctypes.POINTER(SdAttnShape), I, I, I, P, P, P, P, P, P, P, I, P, P, Z, P]
         L.sd_block_attn_append.restype = ctypes.c_int
@@ -343,11 +348,9 @@ def accept_workspace_size(shape: SdAcceptShape, temperature: float) -> int:
     return n.value
 
 
-def accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor], draft_tokens: torch.Tensor,
-           uniforms: Optional[torch.Tensor], block_lens: torch.Tensor, q_offsets: torch.Tensor, temperature: float,
-           *, max_block: int, accept_len: Optional[torch.Tensor] = None, next_token: Optional[torch.Tensor] = None,
-           workspace: Optional[torch.Tensor] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
-    """Speculative acceptance (sd_accept).  Returns device int32 (accept_len[S], next_token[S])."""
+def _accept_checks(target_logits, draft_logits, draft_tokens, uniforms, block_lens, q_offsets, temperature,
+                   accept_len, next_token) -> int:
+    """Shape, dtype and device checks of an acceptance call; returns S."""
     _shape(block_lens, "block_lens", None)
     S = block_lens.shape[0]
     _shape(target_logits, "target_logits", None, None)
@@ -369,6 +372,20 @@ def accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor], dr
         _need(uniforms, "uniforms", torch.float32, dev)
     for name, t in (("draft_tokens", draft_tokens), ("block_lens", block_lens), ("q_offsets", q_offsets)):
         _need(t, name, torch.int32, dev)
+    for name, t in (("accept_len", accept_len), ("next_token", next_token)):
+        if t is not None:
+            _need(t, name, torch.int32, dev)
+    return S
+
+
+def accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor], draft_tokens: torch.Tensor,
+           uniforms: Optional[torch.Tensor], block_lens: torch.Tensor, q_offsets: torch.Tensor, temperature: float,
+           *, max_block: int, accept_len: Optional[torch.Tensor] = None, next_token: Optional[torch.Tensor] = None,
+           workspace: Optional[torch.Tensor] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Speculative acceptance (sd_accept).  Returns device int32 (accept_len[S], next_token[S])."""
+    S = _accept_checks(target_logits, draft_logits, draft_tokens, uniforms, block_lens, q_offsets, temperature,
+                       accept_len, next_token)
+    dev = target_logits.device
     if accept_len is None:
         accept_len = torch.empty(S, dtype=torch.int32, device=dev)
     if next_token is None:
@@ -382,6 +399,22 @@ def accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor], dr
                            _ptr(uniforms if temperature > 0 else None), _ptr(block_lens), _ptr(q_offsets),
                            float(temperature), _ptr(accept_len), _ptr(next_token), _ptr(workspace),
                            workspace.numel() * workspace.element_size(), _stream(stream)))
+    return accept_len, next_token
+
+
+def accept_noalloc(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor], draft_tokens: torch.Tensor,
+                   uniforms: Optional[torch.Tensor], block_lens: torch.Tensor, q_offsets: torch.Tensor,
+                   temperature: float, *, max_block: int, accept_len: torch.Tensor, next_token: torch.Tensor,
+                   stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """sd_accept_noalloc: acceptance into caller-given accept_len[S], next_token[S], with the
+    library's fixed device scratch instead of a workspace (the call allocates nothing)."""
+    S = _accept_checks(target_logits, draft_logits, draft_tokens, uniforms, block_lens, q_offsets, temperature,
+                       accept_len, next_token)
+    shape = accept_shape(target_logits, S, max_block)
+    _check(lib().sd_accept_noalloc(ctypes.byref(shape), _ptr(target_logits),
+                                   _ptr(draft_logits if temperature > 0 else None), _ptr(draft_tokens),
+                                   _ptr(uniforms if temperature > 0 else None), _ptr(block_lens), _ptr(q_offsets),
+                                   float(temperature), _ptr(accept_len), _ptr(next_token), _stream(stream)))
     return accept_len, next_token
 
 

@@ -9,6 +9,8 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
+#include <mutex>
 #include <string>
 
 #include "accept.hpp"
@@ -510,15 +512,13 @@ int check_accept_call(const sd_accept_shape *sh, const void *target_logits, cons
 
 }  // namespace
 
-int sd_accept(const sd_accept_shape *sh, const void *target_logits, const void *draft_logits,
-              const int32_t *draft_tokens, const float *uniforms, const int32_t *block_lens,
-              const int32_t *q_offsets, float temperature, int32_t *accept_len, int32_t *next_token,
-              void *workspace, size_t workspace_bytes, void *stream) {
-  AcceptPlan p;
-  int rc = check_accept_call(sh, target_logits, draft_logits, draft_tokens, uniforms, block_lens, q_offsets,
-                             temperature, accept_len, next_token, workspace, workspace_bytes, &p);
-  if (rc) return rc;
-  if (sh->num_seqs == 0) return ok();
+namespace {
+
+// Enqueue the acceptance kernels of a checked call; `workspace` holds at least p.total bytes.
+int accept_enqueue(const sd_accept_shape *sh, const AcceptPlan &p, const void *target_logits,
+                   const void *draft_logits, const int32_t *draft_tokens, const float *uniforms,
+                   const int32_t *block_lens, const int32_t *q_offsets, float temperature, int32_t *accept_len,
+                   int32_t *next_token, void *workspace, void *stream) {
   const bool sample = temperature > 0.f;
 
   sdb::AcceptArgs a;
@@ -571,6 +571,77 @@ int sd_accept(const sd_accept_shape *sh, const void *target_logits, const void *
   }
 #undef SDB_STATS
   return check_launch("sd_accept");
+}
+
+// ---- the fixed scratch of sd_accept_noalloc ----
+// Device memory for the acceptance workspace of callers that cannot allocate.  Each device
+// the library runs on holds its own copy until the process ends.  Host code never uses the
+// array's name as an address: the name is a host-side stand-in, so kernels get the device
+// address that hipGetSymbolAddress returns, looked up once per device with that device current.
+constexpr size_t kNoAllocScratchBytes = SD_ACCEPT_NOALLOC_SCRATCH_BYTES;
+constexpr int kNoAllocMaxDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+std::atomic<void *> g_scratch_ptr[kNoAllocMaxDevices];
+std::mutex g_scratch_mu;
+
+int noalloc_scratch(void **ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(SD_ERR_HIP, "sd_accept_noalloc: hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kNoAllocMaxDevices)
+    return fail(SD_ERR_UNSUPPORTED, "sd_accept_noalloc: device %d beyond the %d devices served", dev,
+                kNoAllocMaxDevices);
+  void *p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (e != hipSuccess || !p)
+        return fail(SD_ERR_HIP, "sd_accept_noalloc: hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                    hipGetErrorString(e));
+      g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *ptr = p;
+  return ok();
+}
+
+}  // namespace
+
+int sd_accept(const sd_accept_shape *sh, const void *target_logits, const void *draft_logits,
+              const int32_t *draft_tokens, const float *uniforms, const int32_t *block_lens,
+              const int32_t *q_offsets, float temperature, int32_t *accept_len, int32_t *next_token,
+              void *workspace, size_t workspace_bytes, void *stream) {
+  AcceptPlan p;
+  int rc = check_accept_call(sh, target_logits, draft_logits, draft_tokens, uniforms, block_lens, q_offsets,
+                             temperature, accept_len, next_token, workspace, workspace_bytes, &p);
+  if (rc) return rc;
+  if (sh->num_seqs == 0) return ok();
+  return accept_enqueue(sh, p, target_logits, draft_logits, draft_tokens, uniforms, block_lens, q_offsets,
+                        temperature, accept_len, next_token, workspace, stream);
+}
+
+int sd_accept_noalloc(const sd_accept_shape *sh, const void *target_logits, const void *draft_logits,
+                      const int32_t *draft_tokens, const float *uniforms, const int32_t *block_lens,
+                      const int32_t *q_offsets, float temperature, int32_t *accept_len, int32_t *next_token,
+                      void *stream) {
+  AcceptPlan p;
+  int rc = accept_plan(sh, temperature, &p);
+  if (rc) return rc;
+  if (p.total > kNoAllocScratchBytes)
+    return fail(SD_ERR_WORKSPACE,
+                "sd_accept_noalloc: this shape needs %zu bytes of scratch, the library holds %zu; "
+                "call sd_accept with a workspace instead", p.total, kNoAllocScratchBytes);
+  if (sh->num_seqs == 0) return ok();
+  void *ws = nullptr;
+  rc = noalloc_scratch(&ws);
+  if (rc) return rc;
+  rc = check_accept_call(sh, target_logits, draft_logits, draft_tokens, uniforms, block_lens, q_offsets,
+                         temperature, accept_len, next_token, ws, kNoAllocScratchBytes, &p);
+  if (rc) return rc;
+  return accept_enqueue(sh, p, target_logits, draft_logits, draft_tokens, uniforms, block_lens, q_offsets,
+                        temperature, accept_len, next_token, ws, stream);
 }
 
 // ---------------------------------------------------------------------------

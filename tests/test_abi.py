@@ -281,3 +281,22 @@ def test_survival_call_errors_without_device():
     # no samples: nothing to do, no device work
     assert call_survival_tau(good_survival_shape(num_samples=0), gamma=0) == L.SD_OK
     assert call_survival_sample(good_survival_shape(num_samples=0), gamma=0) == L.SD_OK
+
+
+def test_accept_noalloc_rejects_shapes_beyond_its_scratch():
+    """The allocation-free acceptance call refuses, before touching a device, a shape whose
+    workspace exceeds the fixed scratch, and says so; a shape that fits passes its host checks."""
+    big = L.SdAcceptShape(num_seqs=64, vocab=1 << 26, total_q=64 * 64, max_block=64, dtype=L.SD_BF16)
+    n = ctypes.c_size_t(0)
+    assert L.lib().sd_accept_workspace_size(ctypes.byref(big), 1.0, ctypes.byref(n)) == L.SD_OK
+    assert n.value > L.ACCEPT_NOALLOC_SCRATCH_BYTES
+    z = ctypes.c_void_p(0)
+    rc = L.lib().sd_accept_noalloc(ctypes.byref(big), z, z, z, z, z, z, 1.0, z, z, z)
+    assert rc == L.SD_ERR_WORKSPACE
+    assert "scratch" in L.lib().sd_last_error().decode()
+    # a zero-sequence call needs no device and returns SD_OK
+    empty = L.SdAcceptShape(num_seqs=0, vocab=151936, total_q=0, max_block=16, dtype=L.SD_BF16)
+    assert L.lib().sd_accept_noalloc(ctypes.byref(empty), z, z, z, z, z, z, 1.0, z, z, z) == L.SD_OK
+    # bad arguments are reported as for sd_accept
+    bad = L.SdAcceptShape(num_seqs=2, vocab=151936, total_q=1, max_block=16, dtype=L.SD_BF16)
+    assert L.lib().sd_accept_noalloc(ctypes.byref(bad), z, z, z, z, z, z, 1.0, z, z, z) == L.SD_ERR_INVALID_ARG
