@@ -129,6 +129,15 @@ __device__ __forceinline__ int owner_of_row(const int *off, int S, int r, int dr
   return lo;
 }
 
+// max(a, b, c) in one instruction.  Written as an instruction so that the compiler's IEEE-mode
+// lowering of fmaxf, which first quiets each operand with an extra v_max_f32 x, x (one per
+// unpacked element here), is not applied; logits are never signalling NaNs.
+__device__ __forceinline__ float max3f(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
 // ---- greedy (T = 0) helpers: (value, index) with ties to the lower index ----
 __device__ __forceinline__ void argmax_merge(float &bv, int &bi, float v, int i) {
   if (v > bv || (v == bv && i < bi)) { bv = v; bi = i; }
@@ -143,11 +152,17 @@ __device__ __forceinline__ void lse_merge(float &m, float &sum, float m2, float 
   m = mn;
 }
 
+#ifndef SDB_STATS_GROUP
+#define SDB_STATS_GROUP 2
+#endif
 constexpr int kStatsVecs = 8;     // 16-byte vectors per thread per stats item
-constexpr int kMassVecs = 4;      // vectors per thread per batch in the mass kernel
 constexpr int kLocThreads = 256;  // locate kernel workgroup
-constexpr int kLocVecs = 8;       // vectors per thread kept in registers by the locate kernel
 constexpr int kMaxChunks2 = 4096; // sampling chunks per sequence
+// Sampling chunks hold at most 256 whole vectors, so one vector per thread of the mass and
+// locate kernels covers a chunk, unless the vocabulary needs more than kMaxChunks2 such
+// chunks; then both kernels run with kTailVecsWide vectors per thread per round and the
+// locate kernel recomputes runs longer than that element by element.
+constexpr int kTailVecsWide = 8;
 
 // One stats item in flight: its loads, issued together, and what processing it needs.  A
 // statistics chunk is kStatsChunk whole vectors of the row (the last chunk holds the rest
@@ -242,37 +257,63 @@ __device__ __forceinline__ void stats_process(const AcceptArgs &a, StatsItem<kSt
   float bv = -INFINITY;  // greedy: best value / SAMPLE: the wavefront's max
   int bi = INT_MAX;      // greedy: index of best
   float sum = 0.f;       // SAMPLE: sum of exp2((x - bv) c)
-  // a full chunk needs no padding: its arithmetic runs without the per-vector selects
-  auto reduce = [&](auto padc) {
-    constexpr bool PAD = decltype(padc)::value;
-    auto vec_at = [&](int u) {
-      return (!PAD || (VECS && tid + 256 * u < it.nvc)) ? it.v[u] : u32x4{kPad, kPad, kPad, kPad};
-    };
+  // Vectors past the end of a partial chunk were loaded from a clamped address; they become
+  // padding in place (a full chunk skips this), so one reduction serves every chunk and the
+  // registers hold one copy of the data.
+  if (!VECS || it.nvc < kStatsChunk) {
+#pragma unroll
+    for (int u = 0; u < kStatsVecs; ++u)
+      if (!(VECS && tid + 256 * u < it.nvc)) it.v[u] = u32x4{kPad, kPad, kPad, kPad};
+  }
+  auto vec_at = [&](int u) { return it.v[u]; };
+  auto reduce = [&]() {
+    if constexpr (SAMPLE) {
+      // One pass over the elements, each unpacked once: a running (m, sum of exp2((x - m) c))
+      // per thread, folded a group of two vectors at a time -- the group's maximum by v_max3,
+      // one rescale of the running sum when the maximum moved, then exp2 per element.  About
+      // five VALU instructions per element (unpack, max3/2, fma, exp2, add) against ten for a
+      // max pass and an exp pass that each unpack.
+      float m = -INFINITY;
+      auto fold = [&](const float *x, auto nc) {
+        constexpr int N = decltype(nc)::value;
+        float mv = m;
+#pragma unroll
+        for (int e = 0; e < N; e += 2) mv = max3f(mv, x[e], x[e + 1]);
+        // m = -inf: exp2(-inf) = 0 clears the empty sum; an unchanged maximum keeps it
+        sum *= (mv > m) ? fast_exp2((m - mv) * a.c) : 1.f;
+        m = mv;
+        const float off = (mv == -INFINITY) ? 0.f : -mv * a.c;  // all padding so far: terms are 0
+#pragma unroll
+        for (int e = 0; e < N; ++e) sum += fast_exp2(fmaf(x[e], a.c, off));
+      };
+      constexpr int G = SDB_STATS_GROUP;  // vectors per group
+      static_assert(kStatsVecs % G == 0, "whole groups");
+#pragma unroll
+      for (int u = 0; u < kStatsVecs; u += G) {
+        float x[G * VEC];
+#pragma unroll
+        for (int g = 0; g < G; ++g) unpack<BF16>(vec_at(u + g), x + g * VEC);
+        fold(x, std::integral_constant<int, G * VEC>{});
+      }
+      const float ht[2] = {xh, xt};
+      fold(ht, std::integral_constant<int, 2>{});
+      // the wavefront's reference maximum, and this thread's sum rescaled to it
+      bv = wave_max_f(m);
+      sum = (m == -INFINITY) ? 0.f : sum * fast_exp2((m - bv) * a.c);
+      return;
+    }
     float bm = fmaxf(xh, xt);
 #pragma unroll
     for (int u = 0; u < kStatsVecs; ++u) {
       float x[VEC];
       unpack<BF16>(vec_at(u), x);
 #pragma unroll
-      for (int e = 0; e < VEC; e += 2) bm = fmaxf(bm, fmaxf(x[e], x[e + 1]));
+      for (int e = 0; e < VEC; e += 2) bm = max3f(bm, x[e], x[e + 1]);
     }
     // re-unpack in the second pass rather than keep every unpacked value live across it
 #pragma unroll
     for (int u = 0; u < kStatsVecs; ++u) reg_barrier(it.v[u]);
-    if constexpr (SAMPLE) {
-      bv = wave_max_f(bm);  // the wavefront's reference maximum
-      if (bv != -INFINITY) {
-        const float off = -bv * a.c;
-#pragma unroll
-        for (int u = 0; u < kStatsVecs; ++u) {
-          float x[VEC];
-          unpack<BF16>(vec_at(u), x);
-#pragma unroll
-          for (int e = 0; e < VEC; ++e) sum += fast_exp2(fmaf(x[e], a.c, off));
-        }
-        sum += fast_exp2(fmaf(xh, a.c, off)) + fast_exp2(fmaf(xt, a.c, off));
-      }
-    } else if (bm != -INFINITY) {  // first index of the maximum among this thread's elements
+    if (bm != -INFINITY) {  // first index of the maximum among this thread's elements
       int idx = INT_MAX;
 #pragma unroll
       for (int u = kStatsVecs - 1; u >= 0; --u) {
@@ -312,8 +353,7 @@ __device__ __forceinline__ void stats_process(const AcceptArgs &a, StatsItem<kSt
     }
   }
 
-  if (VECS && it.nvc == kStatsChunk) reduce(std::false_type{});
-  else reduce(std::true_type{});
+  reduce();
   if constexpr (SAMPLE) {
     sum = wave_sum_f(sum);
     xd = wave_max_f(xd);
@@ -347,7 +387,10 @@ __device__ __forceinline__ void stats_process(const AcceptArgs &a, StatsItem<kSt
 // second item's loads in flight per workgroup: the pass is as much arithmetic as traffic,
 // and more resident workgroups hide both.
 template <bool BF16, bool SAMPLE, bool VECS>
-__global__ __launch_bounds__(256) void accept_stats_kernel(AcceptArgs a) {
+#ifndef SDB_STATS_MINW
+#define SDB_STATS_MINW 1
+#endif
+__global__ __launch_bounds__(256, SDB_STATS_MINW) void accept_stats_kernel(AcceptArgs a) {
   __shared__ float sh_v[8];
   __shared__ float sh_s[4];
   __shared__ int sh_i[4];
@@ -486,7 +529,9 @@ __device__ __forceinline__ void elem_masses(float t, float q, const SampleParams
 
 // Sampling masses, grid = (sequence, vocab chunk).  Every workgroup makes the decision,
 // then sums the residual (or p at the bonus row) and p over its chunk of the selected row.
-template <bool BF16>
+// NV: vectors per thread per round; the plan sizes chunks so that one round of NV = 1 covers
+// a chunk, which keeps the dependent chain at one round of row loads after the decision.
+template <bool BF16, int NV>
 __global__ __launch_bounds__(256) void accept_mass_kernel(AcceptArgs a) {
   constexpr int VEC = BF16 ? 8 : 4;
   __shared__ float4 sh_si[2];
@@ -525,21 +570,21 @@ __global__ __launch_bounds__(256) void accept_mass_kernel(AcceptArgs a) {
   const char *tbase = reinterpret_cast<const char *>(a.target) + ch.vb * 16;
   const char *dbase = reinterpret_cast<const char *>(a.draft) + (ch.vb + (da0 - ta0) / VEC) * 16;
   const unsigned nvc = (unsigned)(ch.ve - ch.vb);
-  for (unsigned r0 = tid; r0 < nvc; r0 += 256u * kMassVecs) {
-    u32x4 tb[kMassVecs], qb[kMassVecs];
+  for (unsigned r0 = tid; r0 < nvc; r0 += 256u * NV) {
+    u32x4 tb[NV], qb[NV];
 #pragma unroll
-    for (int u = 0; u < kMassVecs; ++u) {  // clamped: no per-load branch (r0 < nvc here)
+    for (int u = 0; u < NV; ++u) {  // clamped: no per-load branch (r0 < nvc here)
       const unsigned r = min(r0 + 256u * u, nvc - 1u);
       tb[u] = *reinterpret_cast<const u32x4 *>(tbase + r * 16u);
       qb[u] = u32x4{0u, 0u, 0u, 0u};
     }
     if (residual && dvec) {
 #pragma unroll
-      for (int u = 0; u < kMassVecs; ++u)
+      for (int u = 0; u < NV; ++u)
         qb[u] = *reinterpret_cast<const u32x4 *>(dbase + min(r0 + 256u * u, nvc - 1u) * 16u);
     }
 #pragma unroll
-    for (int u = 0; u < kMassVecs; ++u) {
+    for (int u = 0; u < NV; ++u) {
       const unsigned r = r0 + 256u * u;
       float t[VEC], q[VEC];
       unpack<BF16>(tb[u], t);
@@ -590,8 +635,11 @@ __global__ __launch_bounds__(256) void accept_mass_kernel(AcceptArgs a) {
 // thread takes a contiguous run of that chunk's vectors (thread 0 also the unaligned head,
 // the last thread the tail), the runs' masses are scanned across the workgroup, and the one
 // thread whose interval holds the target walks its run in vocabulary order.  A residual with
-// no mass (rounding only) draws from p instead.
-template <bool BF16>
+// no mass (rounding only) draws from p instead.  NV: the longest run kept in registers (runs
+// of the planned chunk sizes fit; longer ones are recomputed element by element).
+constexpr int kLocSums = 4;  // chunk sums per lane held in registers by the chunk search
+
+template <bool BF16, int NV>
 __global__ __launch_bounds__(kLocThreads) void accept_locate_kernel(AcceptArgs a) {
   constexpr int VEC = BF16 ? 8 : 4;
   constexpr int NW = kLocThreads / 64;
@@ -609,42 +657,56 @@ __global__ __launch_bounds__(kLocThreads) void accept_locate_kernel(AcceptArgs a
   const double ustar = (double)si1.z;
 
   if (wave == 0) {
-    // chunk search, 64 chunks per pass; consecutive intervals meet exactly across passes
+    // chunk search, 64 chunks per pass; consecutive intervals meet exactly across passes.  Up to
+    // 64 * kLocSums chunk sums are loaded in one round; more are loaded pass by pass.
     const double2 *cs = a.samp + (size_t)s * a.nch2;
-    auto chunk_sums = [&](int k0) {  // clamped: no per-load branch
-      double2 cm = cs[min(k0 + lane, a.nch2 - 1)];
-      if (k0 + lane >= a.nch2) cm = double2{0.0, 0.0};
-      return cm;
+    const int passes = (a.nch2 + 63) / 64;
+    double2 cm[kLocSums];
+#pragma unroll
+    for (int k = 0; k < kLocSums; ++k) {  // clamped: no per-load branch
+      cm[k] = cs[min(64 * k + lane, a.nch2 - 1)];
+      if (64 * k + lane >= a.nch2) cm[k] = double2{0.0, 0.0};
+    }
+    auto chunk_sums = [&](int k) {
+      if (k < kLocSums) {
+        double2 r = cm[0];
+#pragma unroll
+        for (int q = 1; q < kLocSums; ++q)
+          if (q == k) r = cm[q];
+        return r;
+      }
+      double2 r = cs[min(64 * k + lane, a.nch2 - 1)];
+      if (64 * k + lane >= a.nch2) r = double2{0.0, 0.0};
+      return r;
     };
-    const double2 cm0 = chunk_sums(0);
-    bool any_r = __ballot(cm0.x > 0.0) != 0;
-    for (int k0 = 64; k0 < a.nch2; k0 += 64) any_r |= __ballot(chunk_sums(k0).x > 0.0) != 0;
+    bool any_r = false;
+    for (int k = 0; k < passes; ++k) any_r |= __ballot(chunk_sums(k).x > 0.0) != 0;
     const bool use_p = !any_r;  // residual without mass (rounding only): draw from p
     double carry = 0.0;
-    for (int k0 = 0; k0 < a.nch2; k0 += 64) {
-      const double2 cm = k0 ? chunk_sums(k0) : cm0;
+    for (int k = 0; k < passes; ++k) {
+      const double2 c2 = chunk_sums(k);
       double ex;
-      const double in = wave_scan_d(use_p ? cm.y : cm.x, &ex);
+      const double in = wave_scan_d(use_p ? c2.y : c2.x, &ex);
       carry += readlane_d(in, 63);
     }
     const double tgt = ustar * carry;
     int kc = -1, klast = -1;
     double cex = 0.0;
     carry = 0.0;
-    for (int k0 = 0; k0 < a.nch2; k0 += 64) {
-      const double2 cm = k0 ? chunk_sums(k0) : cm0;
-      const double m = use_p ? cm.y : cm.x;
+    for (int k = 0; k < passes; ++k) {
+      const double2 c2 = chunk_sums(k);
+      const double m = use_p ? c2.y : c2.x;
       double ex;
       const double in = wave_scan_d(m, &ex);
       const double lo = carry + ex, hi = carry + in;
       const unsigned long long hit = __ballot(m > 0.0 && lo <= tgt && tgt < hi);
       if (hit && kc < 0) {
         const int l = __ffsll((long long)hit) - 1;
-        kc = k0 + l;
+        kc = 64 * k + l;
         cex = readlane_d(lo, l);
       }
       const unsigned long long pos = __ballot(m > 0.0);
-      if (pos) klast = k0 + 63 - __clzll((long long)pos);
+      if (pos) klast = 64 * k + 63 - __clzll((long long)pos);
       carry = carry + readlane_d(in, 63);
     }
     if (lane == 0) {
@@ -685,24 +747,24 @@ __global__ __launch_bounds__(kLocThreads) void accept_locate_kernel(AcceptArgs a
       own += (double)m;
       if (m > 0.f) elast = e;
     }
-  float mreg[kLocVecs * VEC];
+  float mreg[NV * VEC];
   const char *tb = reinterpret_cast<const char *>(a.target) + cc.vb * 16;
   const char *db = reinterpret_cast<const char *>(a.draft) + (cc.vb + (da0 - ta0) / VEC) * 16;
-  if (rv <= kLocVecs) {
-    u32x4 tv[kLocVecs], qv[kLocVecs];
+  if (rv <= NV) {
+    u32x4 tv[NV], qv[NV];
 #pragma unroll
-    for (int u = 0; u < kLocVecs; ++u) tv[u] = qv[u] = u32x4{0u, 0u, 0u, 0u};
+    for (int u = 0; u < NV; ++u) tv[u] = qv[u] = u32x4{0u, 0u, 0u, 0u};
     if (nvc > 0) {  // clamped: no per-load branch
       const bool ld_q = use_q && dvec;
 #pragma unroll
-      for (int u = 0; u < kLocVecs; ++u) {
+      for (int u = 0; u < NV; ++u) {
         const unsigned r = (unsigned)min(v0 + u, nvc - 1);
         tv[u] = *reinterpret_cast<const u32x4 *>(tb + r * 16u);
         if (ld_q) qv[u] = *reinterpret_cast<const u32x4 *>(db + r * 16u);
       }
     }
 #pragma unroll
-    for (int u = 0; u < kLocVecs; ++u) {
+    for (int u = 0; u < NV; ++u) {
       float t[VEC], q[VEC];
       unpack<BF16>(tv[u], t);
       unpack<BF16>(qv[u], q);
@@ -755,9 +817,9 @@ __global__ __launch_bounds__(kLocThreads) void accept_locate_kernel(AcceptArgs a
     };
     if (tid == 0)
       for (int e = cc.hb; e < cc.he; ++e) step(e, scalar_mass(e));
-    if (rv <= kLocVecs) {
+    if (rv <= NV) {
 #pragma unroll
-      for (int u = 0; u < kLocVecs; ++u)
+      for (int u = 0; u < NV; ++u)
 #pragma unroll
         for (int i = 0; i < VEC; ++i)
           if (v0 + u < v1) step((int)((cc.vb + v0 + u) * VEC - ta0) + i, mreg[u * VEC + i]);

@@ -177,7 +177,7 @@ void launch_attn_all(const sdb::AttnArgs &a, int grid, int MT, hipStream_t st) {
 // acceptance planning
 // ---------------------------------------------------------------------------
 struct AcceptPlan {
-  int rows, nch, nch2, stats_grid;
+  int rows, nch, nch2, stats_grid, tail_wide;
   size_t off_stats, off_samp, off_seq, total;
 };
 
@@ -202,18 +202,25 @@ int accept_plan(const sd_accept_shape *sh, float temperature, AcceptPlan *p) {
   // thread); a row holds vecs or vecs - 1 whole vectors, the last chunk takes the rest
   long long nch = (vecs + sdb::kStatsChunk - 1) / sdb::kStatsChunk;
   if (nch < 1) nch = 1;
-  // sampling chunks: about 512 workgroups in the mass kernel, and chunks short enough for
-  // the locate kernel to hold one run of at most kLocVecs vectors per thread in registers
-  long long nch2 = S > 0 ? (512 + S - 1) / S : 1;
-  const long long loc_cap = (long long)sdb::kLocThreads * sdb::kLocVecs - 2;  // vectors per chunk
-  if (nch2 < (vecs + loc_cap - 1) / loc_cap) nch2 = (vecs + loc_cap - 1) / loc_cap;
-  if (nch2 > sdb::kMaxChunks2) nch2 = sdb::kMaxChunks2;
+  // sampling chunks: at most 256 whole vectors each, so the mass and locate kernels hold one
+  // vector per thread and reach the selected row in one round of loads (ragged Qwen3-4B batch
+  // at T = 1); vocabularies that would need
+  // more than kMaxChunks2 chunks take wider chunks and the kernels' multi-vector rounds
+  long long nch2 = (vecs + sdb::kLocThreads - 1) / sdb::kLocThreads;
+  int tail_wide = 0;
+  if (nch2 > sdb::kMaxChunks2) {
+    tail_wide = 1;
+    const long long per = (long long)sdb::kLocThreads * sdb::kTailVecsWide;
+    nch2 = (vecs + per - 1) / per;
+    if (nch2 > sdb::kMaxChunks2) nch2 = sdb::kMaxChunks2;
+  }
   if (nch2 < 1) nch2 = 1;
   if (rows * nch > (1LL << 30)) return fail(SD_ERR_INVALID_ARG, "problem too large");
   const long long items = rows * nch;
   p->rows = (int)rows;
   p->nch = (int)nch;
   p->nch2 = (int)nch2;
+  p->tail_wide = tail_wide;
   p->stats_grid = (int)(items > 0 ? items : 1);
   const size_t kinds = sample ? 2 : 1;
   size_t off = 0;
@@ -554,15 +561,20 @@ int accept_enqueue(const sd_accept_shape *sh, const AcceptPlan &p, const void *t
     if (vecs) hipLaunchKernelGGL((sdb::accept_stats_kernel<BF, SMP, true>), dim3(g1), dim3(256), 0, st, a);  \
     else hipLaunchKernelGGL((sdb::accept_stats_kernel<BF, SMP, false>), dim3(g1), dim3(256), 0, st, a);      \
   } while (0)
+#define SDB_TAIL(BF, NV)                                                                                      \
+  do {                                                                                                       \
+    hipLaunchKernelGGL((sdb::accept_mass_kernel<BF, NV>), dim3(S * p.nch2), dim3(256), 0, st, a);             \
+    hipLaunchKernelGGL((sdb::accept_locate_kernel<BF, NV>), dim3(S), dim3(sdb::kLocThreads), 0, st, a);       \
+  } while (0)
   if (sample) {
     if (bf) {
       SDB_STATS(true, true);
-      hipLaunchKernelGGL((sdb::accept_mass_kernel<true>), dim3(S * p.nch2), dim3(256), 0, st, a);
-      hipLaunchKernelGGL((sdb::accept_locate_kernel<true>), dim3(S), dim3(sdb::kLocThreads), 0, st, a);
+      if (p.tail_wide) SDB_TAIL(true, sdb::kTailVecsWide);
+      else SDB_TAIL(true, 1);
     } else {
       SDB_STATS(false, true);
-      hipLaunchKernelGGL((sdb::accept_mass_kernel<false>), dim3(S * p.nch2), dim3(256), 0, st, a);
-      hipLaunchKernelGGL((sdb::accept_locate_kernel<false>), dim3(S), dim3(sdb::kLocThreads), 0, st, a);
+      if (p.tail_wide) SDB_TAIL(false, sdb::kTailVecsWide);
+      else SDB_TAIL(false, 1);
     }
   } else {
     if (bf) SDB_STATS(true, false);
@@ -570,6 +582,7 @@ int accept_enqueue(const sd_accept_shape *sh, const AcceptPlan &p, const void *t
     hipLaunchKernelGGL(sdb::accept_greedy_kernel, dim3(S), dim3(64), 0, st, a);
   }
 #undef SDB_STATS
+#undef SDB_TAIL
   return check_launch("sd_accept");
 }
 
