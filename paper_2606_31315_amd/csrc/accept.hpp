@@ -213,9 +213,13 @@ __device__ __forceinline__ void stats_issue(const AcceptArgs &a, int item, Stats
     // the chunk's vectors; an empty chunk reads the row's last whole vector and discards it
     const char *cb = base + (a0 + h) * (BF16 ? 2 : 4) + (unsigned)min(v0, nv - 1) * 16u;
     const unsigned lastv = (unsigned)max(it.nvc, 1) - 1u;
+    // non-temporal: each logit is read once by this pass (measured on the ragged Qwen3-4B batch
+    // at T = 1: sd_accept 25.4 -> 24.5 us)
 #pragma unroll
-    for (int u = 0; u < kStatsVecs; ++u)
-      it.v[u] = *reinterpret_cast<const u32x4 *>(cb + min((unsigned)tid + 256u * u, lastv) * 16u);
+    for (int u = 0; u < kStatsVecs; ++u) {
+      const v4u32 w = __builtin_nontemporal_load(reinterpret_cast<const v4u32 *>(cb + min((unsigned)tid + 256u * u, lastv) * 16u));
+      it.v[u] = u32x4{w.x, w.y, w.z, w.w};
+    }
     it.xh = load_elem<BF16>(base, a0 + min(tid, a.V - 1));
     it.xt = load_elem<BF16>(base, a0 + min(it.tb + tid, a.V - 1));
   } else {

@@ -19,6 +19,8 @@
 //     4x4 blocks of 16-bit elements across each 16-lane group.
 //   * Tiles every row can see entirely skip the per-element mask; the O rescale is
 //     skipped when no row's running maximum moved.
+//   * K/V loads carry the non-temporal cache policy: each key row is read once per call
+//     (ragged Qwen3-4B batch, 7 interleaved rounds: 36.6 -> 34.5 us per call).
 #pragma once
 
 #include <type_traits>
@@ -142,7 +144,7 @@ struct TileLoads {
     for (int q = 0; q < T::LPW; ++q) {
       const int key = min(key0 + row[q], key_last);
       __builtin_amdgcn_global_load_lds((const void *)(page + (unsigned)((key & mask) * T::ROWB) + cof[q]),
-                                       (SDB_LDS void *)(dst + q * 1024), 16, 0, 0);
+                                       (SDB_LDS void *)(dst + q * 1024), 16, 0, kLoadNT);
     }
   }
   // The tile starting at key0 when the block's own keys are not in the cache yet: key
@@ -157,7 +159,7 @@ struct TileLoads {
     for (int q = 0; q < T::LPW; ++q) {
       const int key = min(key0 + row[q], key_last);
       const char *src = key < ctx ? base + (size_t)key * T::ROWB + cof[q] : nbase + (size_t)(key - ctx) * nstride + cof[q];
-      __builtin_amdgcn_global_load_lds((const void *)src, (SDB_LDS void *)(dst + q * 1024), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const void *)src, (SDB_LDS void *)(dst + q * 1024), 16, 0, kLoadNT);
     }
   }
   // Issue the loads of the tile starting at key0 into `stage`; rows past key_last
@@ -169,13 +171,13 @@ struct TileLoads {
     if (key0 + T::KT - 1 <= key_last) {
 #pragma unroll
       for (int q = 0; q < T::LPW; ++q)
-        __builtin_amdgcn_global_load_lds((const void *)(base + src[q]), (SDB_LDS void *)(dst + q * 1024), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds((const void *)(base + src[q]), (SDB_LDS void *)(dst + q * 1024), 16, 0, kLoadNT);
     } else {
 #pragma unroll
       for (int q = 0; q < T::LPW; ++q) {
         const int shift = min(row[q], key_last - key0) - row[q];  // <= 0: back to the last valid key
         __builtin_amdgcn_global_load_lds((const void *)(base + src[q] + shift * T::ROWB), (SDB_LDS void *)(dst + q * 1024),
-                                         16, 0, 0);
+                                         16, 0, kLoadNT);
       }
     }
   }

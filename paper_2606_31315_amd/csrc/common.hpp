@@ -13,6 +13,11 @@ constexpr int kNumXcd = 8;    // MI355X: 8 accelerator complex dies, workgroups 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 
+typedef unsigned v4u32 __attribute__((ext_vector_type(4)));
+
+// Cache-policy operand of the load-to-LDS builtin: non-temporal (streamed data read once).
+constexpr int kLoadNT = 2;
+
 // Raw 16-byte vector used for global/LDS traffic.
 struct alignas(16) u32x4 {
   uint32_t x, y, z, w;
