@@ -11,6 +11,14 @@ One step = one attention call + one acceptance call over one batch.  Inputs are 
 in HBM before the timed region; the step cycles through copies of every input whose total
 exceeds 1 GB so the 256 MB Infinity Cache cannot serve them.  Prints one JSON line.
 
+The line's `roofline` is the step's: algorithmic bytes of both calls over the step time,
+against the 8 TB/s HBM3E peak and against this GPU's streaming-read ceiling measured in the
+same run (`read_ceiling`); `roofline.per_call` splits it into sd_block_attn and sd_accept,
+each with its counter-measured HBM traffic from profiles/ (null once the kernel sources
+differ from the profiled ones).  Per-call and step times are also given per batch
+(`*_us_batches`).  `cpu_baseline` is the fp64 oracle on the host: median of three runs at
+every OpenMP thread and single-threaded, with the CPU model.
+
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--temperature T] [--no-cpu-baseline]
 """
 from __future__ import annotations
@@ -52,9 +60,31 @@ def parse():
     return ap.parse_args()
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (lscpu, else /proc/cpuinfo)."""
+    import subprocess
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.lower().startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(work, T, seconds, gpu=None):
     """The fp64 oracle on the host cores, on the same step: attention for every block row and
-    head, then acceptance.  Repeated until `seconds` have elapsed (at least once).
+    head, then acceptance.  Timed three times single-threaded and three times with every
+    thread the oracle's OpenMP runtime uses (OMP_NUM_THREADS, else the core count); each
+    leg reports the median (a leg stops early once `seconds` have elapsed).
 
     With ``gpu`` = (attention output, accept_len, next_token) of the timed step on the same
     inputs, the oracle's last results also check them under the parity rule: attention
@@ -70,20 +100,32 @@ def cpu_baseline(work, T, seconds, gpu=None):
     v = a.v_cache.float().numpy()
     tl = acc.target.float().numpy()
     dl = acc.draft.float().numpy() if acc.draft is not None else None
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        o_ref = oracle.block_attn(q, k, v, a.ctx_lens, a.block_lens, a.q_offsets, a.mask_mode)
-        r = oracle.accept(tl, dl, acc.draft_tokens, acc.uniforms, acc.block_lens, acc.q_offsets, T)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= seconds or reps >= 20:
-            break
-    per_step = el / reps
-    res = {"value": work.verified_draft_tokens() / per_step, "unit": "verified draft tokens/s",
-           "cores": oracle.num_threads(), "kind": "oracle",
+    nthreads = oracle.num_threads()
+
+    def leg(threads):
+        oracle.set_threads(threads)
+        times, t_start = [], time.perf_counter()
+        for _ in range(3):
+            t0 = time.perf_counter()
+            o_ref = oracle.block_attn(q, k, v, a.ctx_lens, a.block_lens, a.q_offsets, a.mask_mode)
+            r = oracle.accept(tl, dl, acc.draft_tokens, acc.uniforms, acc.block_lens, acc.q_offsets, T)
+            times.append(time.perf_counter() - t0)
+            if time.perf_counter() - t_start >= seconds:
+                break
+        return float(np.median(times)), times, o_ref, r
+
+    t1, times1, _, _ = leg(1)
+    tn, timesn, o_ref, r = leg(nthreads)
+    oracle.set_threads(nthreads)
+    ntok = work.verified_draft_tokens()
+    res = {"value": round(ntok / tn, 1), "unit": "verified draft tokens/s", "cores": nthreads, "kind": "oracle",
            "sample": f"the full step (attention for all {a.total_q} block rows x {a.Hq} heads + acceptance of "
-                     f"{a.S} sequences at T={T:g}), {reps} repetition(s), {per_step * 1e3:.1f} ms per step",
-           "ms_per_step": per_step * 1e3}
+                     f"{a.S} sequences at T={T:g}), median of {len(timesn)} runs at {nthreads} threads: "
+                     f"{tn * 1e3:.1f} ms per step",
+           "ms_per_step": round(tn * 1e3, 2), "runs_ms": [round(x * 1e3, 2) for x in timesn],
+           "single_thread": {"value": round(ntok / t1, 1), "cores": 1, "ms_per_step": round(t1 * 1e3, 2),
+                             "runs_ms": [round(x * 1e3, 2) for x in times1]},
+           "cpu_model": cpu_model(), "host_cores": os.cpu_count()}
     if gpu is not None:
         attn_gpu, al_g, nt_g = gpu
         err = float(np.abs(attn_gpu.astype(np.float64) - o_ref).max()) if o_ref.size else 0.0
@@ -131,19 +173,22 @@ def kernel_source_hash() -> str:
 
 
 def measured_traffic():
-    """HBM bytes per sd_block_attn call from the committed counter runs (FETCH_SIZE and
-    WRITE_SIZE scaled by a plain copy), or None once the kernel sources have changed since
-    those counters were taken."""
+    """HBM bytes per sd_block_attn and per sd_accept call from the committed counter runs
+    (FETCH_SIZE and WRITE_SIZE scaled by a plain copy): {"sd_block_attn": n, "sd_accept": n},
+    with None for each once the kernel sources have changed since those counters were taken."""
+    out = {"sd_block_attn": None, "sd_accept": None}
     try:
         with open(COUNTERS) as fh:
             text = fh.read()
     except OSError:
-        return None
-    m_b = re.search(r"^traffic-bytes-per-call: (\d+)$", text, re.M)
+        return out
     m_h = re.search(r"^source-sha256: ([0-9a-f]{64})$", text, re.M)
-    if not (m_b and m_h) or m_h.group(1) != kernel_source_hash():
-        return None
-    return int(m_b.group(1))
+    if not m_h or m_h.group(1) != kernel_source_hash():
+        return out
+    for key in out:
+        m_b = re.search(r"^traffic-bytes-per-call %s: (\d+)$" % key, text, re.M)
+        out[key] = int(m_b.group(1)) if m_b else None
+    return out
 
 
 def copy_calibration(torch, dev, nbytes=1 << 29, reps=3):
@@ -164,6 +209,46 @@ def copy_calibration(torch, dev, nbytes=1 << 29, reps=3):
     del src, dst
     return {"bytes_read": nbytes, "bytes_written": nbytes, "us": round(ms * 1e3, 2),
             "gbps_read_plus_write": round(2 * nbytes / (ms * 1e-3) / 1e9, 1)}
+
+
+def read_ceiling(torch, dev, nbuf=4, nbytes=1 << 28, grids=(256, 512, 1024, 2048, 4096), reps=20):
+    """Streaming-read ceiling of this GPU: 16-byte non-temporal loads (libsdbench.so, a
+    measurement kernel outside the library) over nbuf rotating buffers of nbytes each (1 GiB
+    in all, so the 256 MB Infinity Cache cannot serve them), at several grid sizes.  GB/s of
+    bytes read per second of event-timed kernel time; the best grid is the ceiling."""
+    import ctypes
+    from paper_2606_31315_amd import build_lib
+    lib = ctypes.CDLL(build_lib.BENCH_LIB)
+    lib.sdbench_stream_read.restype = ctypes.c_int
+    lib.sdbench_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_ulonglong, ctypes.c_int, ctypes.c_void_p,
+                                        ctypes.c_void_p]
+    bufs = [torch.empty(nbytes, dtype=torch.uint8, device=dev).random_() for _ in range(nbuf)]
+    sink = torch.zeros(max(grids), dtype=torch.int32, device=dev)
+    st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    res = {}
+    for grid in grids:
+        def call(i):
+            rc = lib.sdbench_stream_read(ctypes.c_void_p(bufs[i % nbuf].data_ptr()), nbytes, grid,
+                                         ctypes.c_void_p(sink.data_ptr()), st)
+            if rc != 0:
+                raise RuntimeError(f"sdbench_stream_read failed ({rc})")
+        for i in range(4):
+            call(i)
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0.record()
+        for i in range(reps):
+            call(i)
+        t1.record()
+        torch.cuda.synchronize()
+        res[grid] = nbytes / (t0.elapsed_time(t1) / reps * 1e-3) / 1e9
+    del bufs
+    torch.cuda.empty_cache()
+    best = max(res, key=res.get)
+    return {"gbps": round(res[best], 1), "grid": best, "by_grid": {str(g): round(v, 1) for g, v in res.items()},
+            "bytes_per_call": nbytes, "buffers": nbuf,
+            "what": "16-byte non-temporal loads, 512-thread workgroups each reading one contiguous share, "
+                    "rotating over 1 GiB"}
 
 
 def verify_step_run(torch, sd, work, T, layers, steps, warmup=3):
@@ -305,6 +390,73 @@ def survival_run(torch, sd, N, trials, reps=20):
                     "sd_survival_sample over the first 2^16, Philox4x64-10 draws"}
 
 
+def c2_run(torch, sd, reps=200):
+    """The Qwen3-4B verify step at batch 1 (ctx 2048, B = 16, causal, acceptance at T = 1 over
+    V = 151936) on its seeded inputs, rotated over copies totalling >= 1 GB: attention and
+    acceptance per call (median of 5 batches), the step, and algorithmic GB/s."""
+    from paper_2606_31315_amd import workloads as W
+    dev = torch.device("cuda:0")
+    w = W.c2_qwen3_4b_verify(temperatures=(1.0,))
+    a, acc = w.attn, w.accept[1.0]
+    attn_bytes, acc_bytes = a.kv_bytes() + a.qo_bytes(), acc.logit_bytes()
+    copies = max(2, int(np.ceil(1.0e9 / (attn_bytes + acc_bytes))))
+    bufs = [dict(q=a.q.to(dev), k=a.k_cache.to(dev), v=a.v_cache.to(dev), t=acc.target.to(dev),
+                 d=acc.draft.to(dev)) for _ in range(copies)]
+    ctx, bl, off = (torch.from_numpy(x).to(dev) for x in (a.ctx_lens, a.block_lens, a.q_offsets))
+    tok, u = torch.from_numpy(acc.draft_tokens).to(dev), torch.from_numpy(acc.uniforms).to(dev)
+    o = torch.empty_like(bufs[0]["q"])
+    al = torch.empty(a.S, dtype=torch.int32, device=dev)
+    nt = torch.empty(a.S, dtype=torch.int32, device=dev)
+
+    def attn(i):
+        b = bufs[i % copies]
+        sd.block_attn(b["q"], b["k"], b["v"], ctx, bl, off, a.mask_mode, max_ctx=a.max_ctx, max_block=a.max_block,
+                      out=o)
+
+    def accept(i):
+        b = bufs[i % copies]
+        sd.accept(b["t"], b["d"], tok, u, bl, off, 1.0, max_block=a.max_block, accept_len=al, next_token=nt)
+
+    def step(i):
+        attn(i)
+        accept(i)
+
+    for i in range(20):
+        step(i)
+    a_us, c_us, s_us = (batched_us(torch, fn, reps) for fn in (attn, accept, step))
+    del bufs
+    torch.cuda.empty_cache()
+    med = lambda x: float(np.median(x))
+    return {"num_seqs": a.S, "ctx": int(a.ctx_lens[0]), "block_len": int(a.block_lens[0]), "temperature": 1.0,
+            "attn_us": round(med(a_us), 2), "attn_bytes": attn_bytes,
+            "attn_gbps": round(attn_bytes / (med(a_us) * 1e-6) / 1e9, 1),
+            "accept_us": round(med(c_us), 2), "accept_bytes": acc_bytes,
+            "accept_gbps": round(acc_bytes / (med(c_us) * 1e-6) / 1e9, 1),
+            "step_us": round(med(s_us), 2),
+            "step_gbps": round((attn_bytes + acc_bytes) / (med(s_us) * 1e-6) / 1e9, 1),
+            "step_hbm_frac": round((attn_bytes + acc_bytes) / (med(s_us) * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+            "verified_draft_tokens_per_s": round(w.verified_draft_tokens() / (med(s_us) * 1e-6), 1),
+            "input_copies": copies,
+            "what": "Qwen3-4B verify step, batch 1 (seeded inputs): latency-bound at 18 MB per step"}
+
+
+def batched_us(torch, fn, n, nb=5):
+    """Mean us per call of each of nb batches of n // nb back-to-back calls (events on the
+    launch stream)."""
+    per = max(1, n // nb)
+    out = []
+    for b in range(nb):
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0.record()
+        for i in range(per):
+            fn(b * per + i)
+        t1.record()
+        torch.cuda.synchronize()
+        out.append(t0.elapsed_time(t1) / per * 1e3)
+    return out
+
+
 def other_configs_run(torch, sd, reps=20):
     """The drafter pass (16 sequences, ctx U{1024..8192}, B U{8..32}, bidirectional) and the
     long-context serving step (32 sequences, ctx U{8192..32768}, B U{4..32}, causal attention,
@@ -314,7 +466,7 @@ def other_configs_run(torch, sd, reps=20):
     dev = torch.device("cuda:0")
     g = torch.Generator(device=dev).manual_seed(17)
     Hq, Hkv, D, V = 32, 8, 128, 151936
-    out = {}
+    out = {"qwen3_4b_verify_S1_ctx2048_B16": c2_run(torch, sd)}
 
     def timed(fn, n):
         fn()
@@ -422,6 +574,7 @@ def main():
 
     T = float(args.temperature)
     copy_cal = copy_calibration(torch, torch.device("cuda:0"))
+    ceiling = read_ceiling(torch, torch.device("cuda:0"))
     temps = tuple(sorted({T}))
     work = W.c3_ragged(temperatures=temps)
     a = work.attn
@@ -485,10 +638,13 @@ def main():
     # timed region: exactly K whole steps, nothing else on the stream
     K = args.steps
     ms_per_step = timed(step, K)
-    # per-call durations: K calls of each operation back to back (an event between every
-    # call would add a few microseconds of its own to each)
-    attn_us = timed(attn_call, K) * 1e3
-    acc_us = timed(accept_call, K) * 1e3
+    # spread: the same steps again in 5 batches; per-call durations: K calls of each operation
+    # back to back in 5 batches (an event between every call would add a few microseconds of
+    # its own to each); each reported as the median batch mean with the batch range
+    step_b = batched_us(torch, step, K)
+    attn_b = batched_us(torch, attn_call, K)
+    acc_b = batched_us(torch, accept_call, K)
+    attn_us, acc_us = float(np.median(attn_b)), float(np.median(acc_b))
 
     ntok = work.verified_draft_tokens()
     value = ntok / (ms_per_step * 1e-3)
@@ -498,6 +654,17 @@ def main():
     al_h, nt_h = al.cpu().numpy(), nt.cpu().numpy()
     attn_h = outs[0].float().cpu().numpy()
 
+    traffic = measured_traffic()
+    rc_gbps = ceiling["gbps"]
+
+    def call_entry(us, nbytes, kernels, tr):
+        gbps = nbytes / (us * 1e-6) / 1e9
+        return {"kernels": kernels, "us": round(us, 2), "algorithmic_bytes": int(nbytes), "achieved": round(gbps, 1),
+                "frac": round(gbps / HBM_PEAK_GBPS, 4), "frac_of_read_ceiling": round(gbps / rc_gbps, 4),
+                "traffic": tr}
+
+    step_traffic = (traffic["sd_block_attn"] + traffic["sd_accept"]
+                    if traffic["sd_block_attn"] is not None and traffic["sd_accept"] is not None else None)
     res = {
         "metric": METRIC, "value": round(value, 1), "unit": "verified draft tokens/s", "n_gpus": 1, "steps": K,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 6), "higher_is_better": True, "scaling": "weak",
@@ -506,20 +673,32 @@ def main():
                    "ctx": int(a.ctx_lens[0]), "block_lens": [int(b) for b in a.block_lens], "vocab": acc.V,
                    "temperature": T, "mask": "causal_in_block", "layers_timed": 1, "input_copies": copies},
         "step_gbps": round(step_gbps, 1), "step_hbm_frac": round(step_gbps / HBM_PEAK_GBPS, 4),
+        "step_us_batches": [round(x, 2) for x in step_b],
         "attn_us": round(attn_us, 2), "attn_gbps": round(attn_gbps, 1),
+        "attn_us_batches": [round(x, 2) for x in attn_b],
         "accept_us": round(acc_us, 2), "accept_gbps": round(acc_gbps, 1),
+        "accept_us_batches": [round(x, 2) for x in acc_b],
         "bytes": {"attn": attn_bytes, "accept": acc_bytes, "step": step_bytes},
         "verify_rows_per_s": round(a.total_q / (ms_per_step * 1e-3), 1),
         "committed_tokens_per_s": round(float((al_h + 1).sum()) / (ms_per_step * 1e-3), 1),
         "mean_accept_len": float(al_h.mean()),
         "copy_calibration": copy_cal,
-        "roofline": {"bound": "hbm", "kernel": "block_attn_bf16_kernel + block_attn_merge_kernel (one sd_block_attn call)",
-                     "achieved": round(attn_gbps, 1),
-                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
-                     "traffic": measured_traffic()},
+        "read_ceiling": ceiling,
+        # the metric's unit is the step: algorithmic bytes of one attention call and one
+        # acceptance call over the step's event-timed duration; per call below, each with its
+        # counter-measured HBM traffic
+        "roofline": {"bound": "hbm", "scope": "step = sd_block_attn (one layer) + sd_accept",
+                     "achieved": round(step_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(step_gbps / HBM_PEAK_GBPS, 4), "traffic": step_traffic,
+                     "read_ceiling_gbps": rc_gbps, "frac_of_read_ceiling": round(step_gbps / rc_gbps, 4),
+                     "per_call": {
+                         "sd_block_attn": call_entry(attn_us, attn_bytes,
+                                                     "block_attn_bf16_kernel + block_attn_merge_kernel",
+                                                     traffic["sd_block_attn"]),
+                         "sd_accept": call_entry(acc_us, acc_bytes,
+                                                 "accept_stats_kernel + accept_mass_kernel + accept_locate_kernel",
+                                                 traffic["sd_accept"])}},
     }
-    res["attn_frac_of_copy_rate"] = round(attn_gbps / copy_cal["gbps_read_plus_write"], 4)
-    res["step_frac_of_copy_rate"] = round(step_gbps / copy_cal["gbps_read_plus_write"], 4)
     # rows a sequential acceptance would have read: target rows 0..accept_len and the drafts
     # tested up to the first rejection (the data-parallel pass reads every row)
     B_h = a.block_lens.astype(np.int64)
@@ -541,9 +720,11 @@ def main():
     ms0 = timed(step0, K)
     acc0_bytes = acc0.logit_bytes()
     al0_h = al0.cpu().numpy()
+    gbps0 = (attn_bytes + acc0_bytes) / (ms0 * 1e-3) / 1e9
     res["t0"] = {"ms_per_step": round(ms0, 6), "verified_draft_tokens_per_s": round(ntok / (ms0 * 1e-3), 1),
                  "accept_bytes": acc0_bytes, "accept_useful_bytes": int((al0_h + 1).sum()) * acc0.V * 2,
-                 "step_gbps": round((attn_bytes + acc0_bytes) / (ms0 * 1e-3) / 1e9, 1),
+                 "step_gbps": round(gbps0, 1), "step_hbm_frac": round(gbps0 / HBM_PEAK_GBPS, 4),
+                 "frac_of_read_ceiling": round(gbps0 / rc_gbps, 4),
                  "what": "the same step with greedy acceptance (T = 0): every target row read once"}
     res["paged_attn_us"] = {f"page_{ps}_shuffled": paged_run(torch, sd, a, bufs, ps, K) for ps in (16, 64, 256)}
     res["paged_attn_us"]["page_64_in_order"] = paged_run(torch, sd, a, bufs, 64, K, shuffle=False)

@@ -9,6 +9,9 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "sd_block.hip")
 LIB = os.path.join(PKG, "libsdblock.so")
+# the benchmark's streaming-read ceiling kernel (not part of the library's ABI)
+BENCH_SRC = os.path.join(PKG, "csrc", "bench_read.hip")
+BENCH_LIB = os.path.join(PKG, "libsdbench.so")
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
@@ -18,12 +21,20 @@ HIPCC_FLAGS = [
 ]
 
 
-def build(out: str = LIB, extra=()) -> str:
+def _hipcc(src: str, out: str, extra=()) -> str:
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
     tmp = out + ".tmp"
-    cmd = [hipcc, *HIPCC_FLAGS, *extra, "-I", os.path.join(ROOT, "include"), "-o", tmp, SRC]
+    cmd = [hipcc, *HIPCC_FLAGS, *extra, "-I", os.path.join(ROOT, "include"), "-o", tmp, src]
     subprocess.run(cmd, check=True)
     os.replace(tmp, out)
+    return out
+
+
+def build(out: str = LIB, extra=()) -> str:
+    """libsdblock.so, and libsdbench.so beside it when building the default library."""
+    _hipcc(SRC, out, extra)
+    if out == LIB:
+        _hipcc(BENCH_SRC, BENCH_LIB, extra)
     return out
 
 
