@@ -50,6 +50,22 @@ def test_vocab_edges(V, dtype, T):
     G.check_accept(p)
 
 
+@pytest.mark.parametrize("V,dtype,S,bl_range,T", [
+    (32768, "bf16", 3, (1, 12), 1.0),     # shares of 128 vectors: many slots per row
+    (131072, "f32", 7, (1, 20), 1.0),     # fp32 rows of 32768 vectors
+    (262144, "bf16", 1, (2, 2), 0.0),     # shares shorter than one round
+    (262144, "bf16", 3, (4, 12), 1.0),
+    (151936, "bf16", 71, (1, 24), 1.0),   # more workgroups than CUs (shares capped at 7 rows)
+    (151936, "bf16", 40, (1, 40), 0.0),
+])
+def test_large_vocab_shapes(V, dtype, S, bl_range, T):
+    """Large vocabularies (rows of 4096 to 32768 16-byte vectors) in bf16 and fp32, from one
+    sequence to more sequences than a wave of workgroups covers."""
+    p = _many_seq_problem(V + S + int(T), S, V, bl_range, dtype, T, target_sigma=3.0, noise_sigma=1.0,
+                          name=f"large_V{V}_S{S}")
+    G.check_accept(p)
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_greedy_ties_lowest_index(dtype):
     """Integer-valued logits at V=151936: the maximum is tied in many rows, and across vocabulary
