@@ -233,6 +233,14 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   const int l16 = lane & 15;
   const int kgrp = lane >> 4;
   const int nmt = (M + 15) >> 4;
+  // Wavefront w runs on SIMD w % 4.  With 5 or 6 m-tiles, m-tiles 4 and 5 would put two whole
+  // m-tiles of work on one SIMD while others idle, so wavefronts 4-7 instead take the two key
+  // halves of m-tiles 4 and 5 (each keeps its own online-softmax state over its 32 keys of
+  // every tile; the halves are merged once, after the last tile): at most 1.5 m-tiles of work
+  // per SIMD instead of 2.
+  const bool hsplit = MT == 1 && (nmt == 5 || nmt == 6);
+  const int hlf = (hsplit && wave >= 4) ? ((wave - 4) & 1) : -1;  // key half, or -1: whole tiles
+  auto mtile = [&](int j) { return (hlf >= 0) ? 4 + ((wave - 4) >> 1) : wave + T::NW * j; };
 
   const char *kbase = reinterpret_cast<const char *>(a.k);
   const char *vbase = reinterpret_cast<const char *>(a.v);
@@ -249,7 +257,7 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   bool act[MT];
 #pragma unroll
   for (int j = 0; j < MT; ++j) {
-    const int mt = wave + T::NW * j;
+    const int mt = mtile(j);
     const int m = mt * 16 + l16;
     act[j] = mt < nmt;
     m_run[j] = -INFINITY;
@@ -347,6 +355,66 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   const int vis_all = a.causal ? min(k1, ctx + 1) : k1;
   const float sl2 = a.scale_log2;
 
+  // One wavefront's work on one m-tile over NSBW 16-key sub-blocks of a tile, starting at key
+  // kb (LDS rows from stg): scores, mask, online softmax, P.V.
+  auto tile_work = [&](auto nsbw_c, int j, unsigned stg, int kb, bool full) {
+    constexpr int NSBW = decltype(nsbw_c)::value;
+    // S^T = K Q^T: sacc[sb][r] is key kb + sb*16 + kgrp*4 + r of row l16 (unscaled)
+    f32x4 sacc[NSBW];
+#pragma unroll
+    for (int sb = 0; sb < NSBW; ++sb) sacc[sb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int st = 0; st < NST; ++st) {
+      const char SDB_LDS *kp = (const char SDB_LDS *)(uintptr_t)(stg + koff[st]);
+#pragma unroll
+      for (int sb = 0; sb < NSBW; ++sb) {
+        const bf16x8 av = *(const bf16x8 SDB_LDS *)(kp + sb * 16 * T::ROWB);
+        sacc[sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qop[j][st], sacc[sb], 0, 0, 0);
+      }
+    }
+    // online softmax in the log2 domain: max of the raw scores, then one FMA per score
+    if (!full) {
+      const int lim = a.causal ? min(k1, ctx + row_i[j] + 1) : k1;
+#pragma unroll
+      for (int sb = 0; sb < NSBW; ++sb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (kb + sb * 16 + kgrp * 4 + r >= lim) sacc[sb][r] = -INFINITY;
+    }
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int sb = 0; sb < NSBW; ++sb)
+      tmax = fmaxf(tmax, fmaxf(fmaxf(sacc[sb][0], sacc[sb][1]), fmaxf(sacc[sb][2], sacc[sb][3])));
+    tmax = fmaxf(tmax, shfl_xor_f(tmax, 16));
+    tmax = fmaxf(tmax, shfl_xor_f(tmax, 32));
+    const float mnew = fmaxf(m_run[j], tmax * sl2);
+    const float muse = (mnew == -INFINITY) ? 0.f : mnew;
+    float psum = 0.f;
+#pragma unroll
+    for (int sb = 0; sb < NSBW; ++sb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        sacc[sb][r] = fast_exp2(fmaf(sacc[sb][r], sl2, -muse));
+        psum += sacc[sb][r];
+      }
+    if (__any(mnew != m_run[j])) {
+      const float alpha = fast_exp2(m_run[j] - muse);
+      l_run[j] *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) oacc[j][dt] *= alpha;
+    }
+    m_run[j] = mnew;
+    l_run[j] += psum;
+
+    // O^T += V^T P^T over these keys in 32-key steps
+    pv_step<0, NDT, NSBW>(sacc, stg, voff, oacc[j]);
+    if constexpr (NSBW > 2) pv_step<1, NDT, NSBW>(sacc, stg, voff, oacc[j]);
+    if constexpr (NSBW > 4) {
+      pv_step<2, NDT, NSBW>(sacc, stg, voff, oacc[j]);
+      pv_step<3, NDT, NSBW>(sacc, stg, voff, oacc[j]);
+    }
+  };
+
   for (int t = 0; t < ntiles; ++t) {
     const int kt = k0 + t * KT;
     const int ahead = min(ntiles - 1 - t, NS - 2);  // tiles issued after tile t
@@ -361,60 +429,9 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
     for (int j = 0; j < MT; ++j) {
       if (!act[j]) continue;  // uniform per wavefront
-      // S^T = K Q^T: sacc[sb][r] is key kt + sb*16 + kgrp*4 + r of row l16 (unscaled)
-      f32x4 sacc[NSB];
-#pragma unroll
-      for (int sb = 0; sb < NSB; ++sb) sacc[sb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int st = 0; st < NST; ++st) {
-        const char SDB_LDS *kp = (const char SDB_LDS *)(uintptr_t)(stage + koff[st]);
-#pragma unroll
-        for (int sb = 0; sb < NSB; ++sb) {
-          const bf16x8 av = *(const bf16x8 SDB_LDS *)(kp + sb * 16 * T::ROWB);
-          sacc[sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qop[j][st], sacc[sb], 0, 0, 0);
-        }
-      }
-      // online softmax in the log2 domain: max of the raw scores, then one FMA per score
-      if (!full) {
-        const int lim = a.causal ? min(k1, ctx + row_i[j] + 1) : k1;
-#pragma unroll
-        for (int sb = 0; sb < NSB; ++sb)
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (kt + sb * 16 + kgrp * 4 + r >= lim) sacc[sb][r] = -INFINITY;
-      }
-      float tmax = -INFINITY;
-#pragma unroll
-      for (int sb = 0; sb < NSB; ++sb)
-        tmax = fmaxf(tmax, fmaxf(fmaxf(sacc[sb][0], sacc[sb][1]), fmaxf(sacc[sb][2], sacc[sb][3])));
-      tmax = fmaxf(tmax, shfl_xor_f(tmax, 16));
-      tmax = fmaxf(tmax, shfl_xor_f(tmax, 32));
-      const float mnew = fmaxf(m_run[j], tmax * sl2);
-      const float muse = (mnew == -INFINITY) ? 0.f : mnew;
-      float psum = 0.f;
-#pragma unroll
-      for (int sb = 0; sb < NSB; ++sb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          sacc[sb][r] = fast_exp2(fmaf(sacc[sb][r], sl2, -muse));
-          psum += sacc[sb][r];
-        }
-      if (__any(mnew != m_run[j])) {
-        const float alpha = fast_exp2(m_run[j] - muse);
-        l_run[j] *= alpha;
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) oacc[j][dt] *= alpha;
-      }
-      m_run[j] = mnew;
-      l_run[j] += psum;
-
-      // O^T += V^T P^T over the tile's keys in 32-key steps
-      pv_step<0, NDT, NSB>(sacc, stage, voff, oacc[j]);
-      pv_step<1, NDT, NSB>(sacc, stage, voff, oacc[j]);
-      if constexpr (NSB > 4) {
-        pv_step<2, NDT, NSB>(sacc, stage, voff, oacc[j]);
-        pv_step<3, NDT, NSB>(sacc, stage, voff, oacc[j]);
-      }
+      if (hlf < 0) tile_work(std::integral_constant<int, NSB>{}, j, stage, kt, full);
+      else tile_work(std::integral_constant<int, NSB / 2>{}, j, stage + (unsigned)(hlf * (KT / 2) * T::ROWB),
+                     kt + hlf * (KT / 2), full);
     }
     if constexpr (PAGED) {
       if (t + NS < ntiles) pgn = ld.fetch_page(table, a.max_pages, a.num_pages, a.page_log2, k0 + (t + NS) * KT, k1 - 1, wave);
@@ -438,6 +455,38 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
     }
   }
 
+  // ---- key halves of m-tiles 4 and 5: the second half's state joins the first's ----
+  if (hsplit) {  // uniform
+    constexpr int XS = NDT * 4 + 2;  // floats per lane: O, then m and l
+    float SDB_LDS *xch = (float SDB_LDS *)(SDB_LDS void *)ring_raw;  // the ring is no longer read
+    __syncthreads();
+    if (hlf == 1 && act[0]) {
+      float SDB_LDS *dst = xch + ((wave - 4) >> 1) * 64 * XS + lane;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dst[(dt * 4 + r) * 64] = oacc[0][dt][r];
+      dst[(NDT * 4) * 64] = m_run[0];
+      dst[(NDT * 4 + 1) * 64] = l_run[0];
+    }
+    __syncthreads();
+    if (hlf == 0 && act[0]) {
+      const float SDB_LDS *src = xch + ((wave - 4) >> 1) * 64 * XS + lane;
+      const float mb = src[(NDT * 4) * 64], lb = src[(NDT * 4 + 1) * 64];
+      const float mn = fmaxf(m_run[0], mb);
+      const float mu = (mn == -INFINITY) ? 0.f : mn;
+      const float sa = (m_run[0] == -INFINITY) ? 0.f : fast_exp2(m_run[0] - mu);
+      const float sb = (mb == -INFINITY) ? 0.f : fast_exp2(mb - mu);
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) oacc[0][dt][r] = oacc[0][dt][r] * sa + src[(dt * 4 + r) * 64] * sb;
+      l_run[0] = l_run[0] * sa + lb * sb;
+      m_run[0] = mn;
+    }
+    if (hlf == 1) act[0] = false;  // merged into the first half's wavefront
+  }
+
   // ---- epilogue: row sums over the four key groups, then output or partials ----
 #pragma unroll
   for (int j = 0; j < MT; ++j) {
@@ -447,7 +496,7 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   if (nsplit == 1) {
 #pragma unroll
     for (int j = 0; j < MT; ++j) {
-      const int m = (wave + T::NW * j) * 16 + l16;
+      const int m = mtile(j) * 16 + l16;
       if (!act[j] || m >= M) continue;
       const float inv = 1.f / l_run[j];
       char *orow = reinterpret_cast<char *>(a.out) + ((size_t)(qoff + m / a.G) * a.Hq + g * a.G + m % a.G) * D * EB;
@@ -462,7 +511,7 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   const size_t wrow = (size_t)it.slot * a.Mpad;
 #pragma unroll
   for (int j = 0; j < MT; ++j) {
-    const int m = (wave + T::NW * j) * 16 + l16;
+    const int m = mtile(j) * 16 + l16;
     if (!act[j] || m >= M) continue;
     float *prow = a.part_o + (wrow + m) * D;
 #pragma unroll
