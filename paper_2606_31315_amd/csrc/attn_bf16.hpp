@@ -514,9 +514,16 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
     const int m = mtile(j) * 16 + l16;
     if (!act[j] || m >= M) continue;
     float *prow = a.part_o + (wrow + m) * D;
+    // non-temporal: the partials are read once, by the merge kernel, so they go to memory now
+    // instead of waiting dirty in L2 for the write-back at the kernel's end (ragged Qwen3-4B
+    // batch, 7 interleaved rounds: 35.0 -> 34.0 us per call)
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) *reinterpret_cast<f32x4 *>(prow + dt * 16 + kgrp * 4) = oacc[j][dt];
-    if (kgrp == 0) a.part_ml[wrow + m] = float2{m_run[j], l_run[j]};
+    for (int dt = 0; dt < NDT; ++dt)
+      __builtin_nontemporal_store(oacc[j][dt], reinterpret_cast<f32x4 *>(prow + dt * 16 + kgrp * 4));
+    if (kgrp == 0) {
+      typedef float f2v __attribute__((ext_vector_type(2)));
+      __builtin_nontemporal_store(f2v{m_run[j], l_run[j]}, reinterpret_cast<f2v *>(a.part_ml + wrow + m));
+    }
   }
 }
 

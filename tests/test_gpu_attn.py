@@ -35,10 +35,43 @@ def test_drafter_bidirectional():
     G.check_attn(W.c4_drafter().attn)
 
 
-def test_long_context_sampled_rows():
-    """32 sequences, ctx U{8192..32768}, B U{4..32}: sampled rows against the oracle."""
+@pytest.fixture(scope="module")
+def long_context_run():
+    """The long-context batch (32 sequences, ctx U{8192..32768}, B U{4..32}) through the GPU once."""
     p = W.c5_long_context(with_accept=False).attn
-    G.check_attn(p, full=False, per_seq=8)
+    got = G.run_attn(p).float().cpu().numpy().astype(np.float64)
+    return p, got
+
+
+def test_long_context_sampled_rows(long_context_run):
+    """Sampled rows of every sequence of the long-context batch against the oracle."""
+    p, got = long_context_run
+    assert np.isfinite(got).all()
+    toks, heads = G.sample_rows(p, per_seq=8)
+    err = np.abs(got[toks, heads] - G.oracle_attn_rows(p, toks, heads)).max()
+    G.log(f"  sampled rows: max-abs error {err:.3e}")
+    assert err <= G.ATTN_TOL[p.dtype]
+
+
+def test_long_context_longest_sequences_every_row(long_context_run):
+    """Every output row (all block rows x all 32 query heads) of the four longest sequences of
+    the long-context batch: the splits at the 4096-key cap, full splits first then the
+    partial ones, compared row by row."""
+    p, got = long_context_run
+    longest = np.argsort(-(p.ctx_lens.astype(np.int64) + p.block_lens))[:4]
+    toks, heads = [], []
+    for s in longest:
+        base, b = int(p.q_offsets[s]), int(p.block_lens[s])
+        for i in range(b):
+            for h in range(p.Hq):
+                toks.append(base + i)
+                heads.append(h)
+    toks, heads = np.array(toks, np.int64), np.array(heads, np.int32)
+    G.log(f"  sequences {longest.tolist()} (ctx {p.ctx_lens[longest].tolist()}, B {p.block_lens[longest].tolist()}): "
+          f"{len(toks)} rows")
+    err = np.abs(got[toks, heads] - G.oracle_attn_rows(p, toks, heads)).max()
+    G.log(f"  every row of the longest sequences: max-abs error {err:.3e}")
+    assert err <= G.ATTN_TOL[p.dtype]
 
 
 @pytest.mark.parametrize("mode", [CAUSAL, BIDIR])
