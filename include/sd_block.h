@@ -213,7 +213,7 @@ int sd_accept(const sd_accept_shape *shape, const void *target_logits, const voi
  * it and give undefined results.  Order them on one stream, or use sd_accept with a workspace
  * each.
  * Errors: as sd_accept; SD_ERR_WORKSPACE when the shape needs more scratch than the array holds
- * (sd_accept_workspace_size reports the need; about 2 * S * max_block * ceil(V / 16384) * 16
+ * (sd_accept_workspace_size reports the need; about 2 * S * max_block * ceil(V / 32768) * 16
  * bytes at T > 0 with bf16 logits), SD_ERR_HIP if the array's address cannot be found.
  */
 #define SD_ACCEPT_NOALLOC_SCRATCH_BYTES ((size_t)4 << 20)
