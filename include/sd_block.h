@@ -163,7 +163,8 @@ typedef struct sd_accept_shape {
   int32_t dtype;     /* SD_BF16 or SD_F32: element type of both logit arrays */
 } sd_accept_shape;
 
-/* Workspace bytes sd_accept needs for this shape at this temperature (host-only). */
+/* Workspace bytes sd_accept needs for this shape at this temperature (host-only): enough for
+ * the single-launch path described under sd_accept where the shape allows it. */
 int sd_accept_workspace_size(const sd_accept_shape *shape, float temperature, size_t *bytes);
 
 /*
@@ -192,7 +193,17 @@ int sd_accept_workspace_size(const sd_accept_shape *shape, float temperature, si
  * S <= total_q <= S * max_block; vocab <= 2^28.  Softmax statistics and per-chunk masses are
  * accumulated in fp32, the acceptance ratio and the final draw's cumulative sums in fp64;
  * decisions within about 1e-6 of a boundary may differ from an fp64 evaluation.
- * Errors: SD_ERR_INVALID_ARG, SD_ERR_WORKSPACE, SD_ERR_HIP.  S == 0 returns SD_OK.
+ *
+ * Paths.  At T = 0, where the shape allows it (at most 8 statistics chunks of 32768 bf16 /
+ * 16384 fp32 logits per row, at most 1024 sequences), the workspace holds
+ * sd_accept_workspace_size bytes and the stream is not capturing a graph, acceptance runs as
+ * one launch whose workgroups hand the per-chunk records on through tagged words in the
+ * workspace; otherwise, and at T > 0 always, as two launches (three at T > 0).  Both give
+ * identical results.  The single launch needs one waiting workgroup per sequence resident; if
+ * a wait gives up (after about a second, e.g. when other work holds the device), that sequence
+ * reports -1 in accept_len and next_token.
+ * Errors: SD_ERR_INVALID_ARG, SD_ERR_WORKSPACE (smaller than the multi-launch path needs),
+ * SD_ERR_HIP.  S == 0 returns SD_OK.
  */
 int sd_accept(const sd_accept_shape *shape, const void *target_logits, const void *draft_logits,
               const int32_t *draft_tokens, const float *uniforms, const int32_t *block_lens,
@@ -221,6 +232,14 @@ int sd_accept_noalloc(const sd_accept_shape *shape, const void *target_logits, c
                       const int32_t *draft_tokens, const float *uniforms, const int32_t *block_lens,
                       const int32_t *q_offsets, float temperature, int32_t *accept_len, int32_t *next_token,
                       void *stream);
+
+/*
+ * Test hook for the acceptance paths of the calls enqueued after it, process-wide:
+ *   mode 0 (default): the single launch where sd_accept's "Paths" allow it; 1: never.
+ *   spin_limit > 0: polls before a wait of the single launch gives up; <= 0: the default.
+ * Errors: SD_ERR_INVALID_ARG for another mode.
+ */
+int sd_accept_set_path(int32_t mode, int32_t spin_limit);
 
 /* ==========================================================================
  * Checks of the per-sequence values the calls above read from device memory and take on

@@ -20,12 +20,12 @@ check_attn_inputs and check_accept_inputs: an error word for the per-sequence de
 values the calls above take on trust.
 """
 from ._lib import (SD_BF16, SD_F32, SD_MASK_BIDIR_IN_BLOCK, SD_MASK_CAUSAL_IN_BLOCK, SdError, Workspace,
-                   accept, accept_noalloc, accept_shape, accept_workspace_size, attn_shape, attn_workspace_size, block_attn,
+                   accept, accept_noalloc, accept_set_path, accept_shape, accept_workspace_size, attn_shape, attn_workspace_size, block_attn,
                    block_attn_append, block_attn_paged, block_size_policy, check_accept_inputs, check_attn_inputs,
                    commit, kv_append_paged,
                    kv_append, lib, survival_sample, survival_tau, verify_step, version)
 
-__all__ = ["block_attn", "block_attn_append", "check_attn_inputs", "check_accept_inputs", "block_attn_paged", "kv_append_paged", "accept", "accept_noalloc", "kv_append", "commit", "verify_step", "block_size_policy", "survival_tau", "survival_sample", "attn_shape", "accept_shape",
+__all__ = ["block_attn", "block_attn_append", "check_attn_inputs", "check_accept_inputs", "block_attn_paged", "kv_append_paged", "accept", "accept_noalloc", "accept_set_path", "kv_append", "commit", "verify_step", "block_size_policy", "survival_tau", "survival_sample", "attn_shape", "accept_shape",
            "attn_workspace_size", "accept_workspace_size",
            "Workspace", "SdError", "lib", "version", "SD_BF16", "SD_F32", "SD_MASK_CAUSAL_IN_BLOCK",
            "SD_MASK_BIDIR_IN_BLOCK"]

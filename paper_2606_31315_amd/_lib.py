@@ -22,7 +22,7 @@ EXPORTS = ["sd_last_error", "sd_version", "sd_block_attn_workspace_size", "sd_bl
            "sd_accept_workspace_size", "sd_accept", "sd_kv_append", "sd_commit", "sd_verify_step_workspace_size",
            "sd_verify_step", "sd_policy_workspace_size", "sd_block_size_policy", "sd_block_attn_paged",
            "sd_kv_append_paged", "sd_survival_tau", "sd_survival_sample", "sd_block_attn_append",
-           "sd_check_attn_inputs", "sd_check_accept_inputs", "sd_accept_noalloc"]
+           "sd_check_attn_inputs", "sd_check_accept_inputs", "sd_accept_noalloc", "sd_accept_set_path"]
 
 # bytes of the fixed device scratch behind sd_accept_noalloc (SD_ACCEPT_NOALLOC_SCRATCH_BYTES)
 ACCEPT_NOALLOC_SCRATCH_BYTES = 4 << 20
@@ -115,6 +115,8 @@ def lib() -> ctypes.CDLL:
         L.sd_survival_sample.argtypes = [ctypes.POINTER(SdSurvivalShape), P, ctypes.c_uint64, I, P, P, P]
         L.sd_check_attn_inputs.restype = ctypes.c_int
         L.sd_check_attn_inputs.argtypes = [ctypes.POINTER(SdAttnShape), P, P, P, P, P]
+        L.sd_accept_set_path.restype = ctypes.c_int
+        L.sd_accept_set_path.argtypes = [I, I]
         L.sd_check_accept_inputs.restype = ctypes.c_int
         L.sd_check_accept_inputs.argtypes = [ctypes.POINTER(SdAcceptShape), P, P, P, P, ctypes.c_float, P, P]
         _lib = L
@@ -416,6 +418,13 @@ def accept_noalloc(target_logits: torch.Tensor, draft_logits: Optional[torch.Ten
                                    _ptr(uniforms if temperature > 0 else None), _ptr(block_lens), _ptr(q_offsets),
                                    float(temperature), _ptr(accept_len), _ptr(next_token), _stream(stream)))
     return accept_len, next_token
+
+
+def accept_set_path(mode: int, spin_limit: int = 0) -> None:
+    """sd_accept_set_path (a test hook): mode 0 lets acceptance run as one launch where the
+    shape, workspace and stream allow it, mode 1 always uses the multi-launch path; spin_limit
+    bounds the single launch's waits (<= 0: the library default)."""
+    _check(lib().sd_accept_set_path(int(mode), int(spin_limit)))
 
 
 def check_attn_inputs(ctx_lens: torch.Tensor, block_lens: torch.Tensor, q_offsets: torch.Tensor, *, total_q: int,

@@ -58,7 +58,33 @@ struct AcceptArgs {
                       //         (draft max, 1/draft sum, u*, -)   (T > 0)
   int S, V, total_q, rows, mb, nch, nch2;
   float c;            // log2(e) / T (T > 0)
+  // Single-launch greedy path (accept_fused_kernel): records handed between workgroups as
+  // tagged words, (tag << 32) | payload bits, each written and read by one 64-bit agent-scope
+  // atomic access.  Word k of a record carries tag + k * kTagStep, and a record counts only
+  // when all three words carry their tags.  The block position is the last index, so that a
+  // wavefront polling one word of every position touches one or two cache lines.
+  unsigned long long *trec;  // [S, nch, 3, mb] record words (the T = 0 records above)
+  unsigned tag;              // this call's tag (a bijective hash of a per-process call counter)
+  int n_items;               // statistics workgroups; workgroups past them run the tail
+  int spin_limit;            // polls before a waiting workgroup gives up
 };
+
+// ---- tagged words: one relaxed 64-bit atomic store or load at agent scope each ----
+// A relaxed atomic access is single-copy atomic and coherent across the XCDs' L2 caches, so
+// the payload read with this call's tag is the one written with it; no fence orders one word
+// after another, and none is needed, since every word carries its own tag.
+__device__ __forceinline__ void tag_put(unsigned long long *p, unsigned tag, uint32_t bits) {
+  __hip_atomic_store(p, ((unsigned long long)tag << 32) | bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned long long tag_get(const unsigned long long *p) {
+  return __hip_atomic_load(const_cast<unsigned long long *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ bool tag_is(unsigned long long w, unsigned tag) { return (unsigned)(w >> 32) == tag; }
+// Tag step between the words of a record: leftover contents pass for a record only if every
+// word's upper half matches its own tag -- about 2^-96 for a record of any earlier data, and
+// never for memory filled with one repeated word.
+constexpr unsigned kTagStep = 0x9e3779b9u;
+__device__ __forceinline__ float tag_f(unsigned long long w) { return __uint_as_float((uint32_t)w); }
 
 // Chunk `c` of `nch` of a row that starts at absolute element a0 and holds V elements.
 // Elements are grouped in 16-byte vectors of VEC elements on absolute boundaries, spread
@@ -246,7 +272,7 @@ __device__ __forceinline__ void stats_issue(const AcceptArgs &a, int item, Stats
 // Reduce one landed item to its record: T > 0 (max, sum of exp2((x - max) c)) with one
 // rescale per item, and the drafted token's logit taken from the register that holds it;
 // T = 0 (max, lowest index).
-template <bool BF16, bool SAMPLE, bool VECS>
+template <bool BF16, bool SAMPLE, bool VECS, bool FUSED = false>
 __device__ __forceinline__ void stats_process(const AcceptArgs &a, StatsItem<kStatsVecs> &it, float *sh_v,
                                               float *sh_s, int *sh_i) {
   constexpr int VEC = BF16 ? 8 : 4;
@@ -306,24 +332,43 @@ __device__ __forceinline__ void stats_process(const AcceptArgs &a, StatsItem<kSt
       sum = (m == -INFINITY) ? 0.f : sum * fast_exp2((m - bv) * a.c);
       return;
     }
-    float bm = fmaxf(xh, xt);
+    // One pass: each vector's maximum (v_max3 over its elements), then the thread's maximum,
+    // the first vector that holds it, and the first element of that vector equal to it --
+    // about 2.3 VALU instructions per element against 7-8 for a compare and select on every
+    // element (measured on MI355X).
+    float vm[kStatsVecs];
 #pragma unroll
     for (int u = 0; u < kStatsVecs; ++u) {
       float x[VEC];
       unpack<BF16>(vec_at(u), x);
+      float m = max3f(x[0], x[1], x[2]);
 #pragma unroll
-      for (int e = 0; e < VEC; e += 2) bm = max3f(bm, x[e], x[e + 1]);
+      for (int e = 3; e + 1 < VEC; e += 2) m = max3f(m, x[e], x[e + 1]);
+      if constexpr (VEC % 2 == 0) m = max3f(m, x[VEC - 1], x[VEC - 1]);
+      vm[u] = m;
     }
-    // re-unpack in the second pass rather than keep every unpacked value live across it
+    float bm = max3f(xh, xt, xt);
 #pragma unroll
-    for (int u = 0; u < kStatsVecs; ++u) reg_barrier(it.v[u]);
+    for (int u = 0; u < kStatsVecs; u += 2) bm = max3f(bm, vm[u], vm[u + 1]);
+    static_assert(kStatsVecs % 2 == 0, "vector maxima are merged in pairs");
     if (bm != -INFINITY) {  // first index of the maximum among this thread's elements
-      int idx = INT_MAX;
+      int su = -1;
+      u32x4 sel = vec_at(0);
 #pragma unroll
-      for (int u = kStatsVecs - 1; u >= 0; --u) {
+      for (int u = kStatsVecs - 1; u >= 0; --u) {  // selects, not branches
+        const bool hit = vm[u] == bm;
+        const u32x4 w = vec_at(u);
+        su = hit ? u : su;
+        sel.x = hit ? w.x : sel.x;
+        sel.y = hit ? w.y : sel.y;
+        sel.z = hit ? w.z : sel.z;
+        sel.w = hit ? w.w : sel.w;
+      }
+      int idx = INT_MAX;
+      if (su >= 0) {
         float x[VEC];
-        unpack<BF16>(vec_at(u), x);
-        const int eb = it.e0 + (tid + 256 * u) * VEC;
+        unpack<BF16>(sel, x);
+        const int eb = it.e0 + (tid + 256 * su) * VEC;
 #pragma unroll
         for (int e = VEC - 1; e >= 0; --e)
           if (x[e] == bm) idx = eb + e;
@@ -381,9 +426,18 @@ __device__ __forceinline__ void stats_process(const AcceptArgs &a, StatsItem<kSt
         argmax_merge(bv, bi, sh_v[w2], sh_i[w2]);
       }
     }
-    if (it.rec >= 0)
-      a.stats[(size_t)it.rec * a.nch + it.c] =
-          SAMPLE ? float4{bv, sum, xd, it.uj} : float4{bv, __int_as_float(bi), __int_as_float(it.tok), 0.f};
+    if (it.rec >= 0) {
+      if constexpr (FUSED) {  // (max, sum, drafted logit) or (max, index, drafted token); u_j is an input
+        const int ks = it.rec / a.mb, j = it.rec - ks * a.mb;
+        unsigned long long *w = a.trec + ((size_t)ks * a.nch + it.c) * 3 * a.mb + j;
+        tag_put(w, a.tag, __float_as_uint(bv));
+        tag_put(w + a.mb, a.tag + kTagStep, SAMPLE ? __float_as_uint(sum) : (uint32_t)bi);
+        tag_put(w + 2 * a.mb, a.tag + 2 * kTagStep, SAMPLE ? __float_as_uint(xd) : (uint32_t)it.tok);
+      } else {
+        a.stats[(size_t)it.rec * a.nch + it.c] =
+            SAMPLE ? float4{bv, sum, xd, it.uj} : float4{bv, __int_as_float(bi), __int_as_float(it.tok), 0.f};
+      }
+    }
   }
 }
 
@@ -486,13 +540,12 @@ struct SampleSel {
   float tm, ts, qm, qs, ustar;
 };
 
-__device__ SampleSel sampling_decision(const AcceptArgs &a, int s, int B) {
+// The decision from the merged records of lane i's block position: target (tm, ts, td),
+// draft (qm, qs, dd), uniform u.
+__device__ __forceinline__ SampleSel sample_select(const AcceptArgs &a, int B, float tm, float ts, float td, float u,
+                                                   float qm, float qs, float dd) {
   const int lane = threadIdx.x & 63;
   const int n = B - 1;
-  float tm = -INFINITY, ts = 0.f, qm = -INFINITY, qs = 0.f, td = NAN, dd = NAN, u = 0.f;
-  if (lane < a.mb)  // issued before B arrives; positions >= B are ignored below
-    merge_records2(a.stats + (size_t)(s * a.mb + lane) * a.nch, a.stats + (size_t)((a.S + s) * a.mb + lane) * a.nch,
-                   a.nch, a.c, tm, ts, td, u, qm, qs, dd);
   bool rejects = false;
   if (lane < n) {
     // rho = p(d) / q(d) = exp2((td - tm) c - (dd - qm) c) * qs / ts; q(d) = 0 accepts.  A token
@@ -511,6 +564,15 @@ __device__ SampleSel sampling_decision(const AcceptArgs &a, int s, int B) {
   r.qs = __shfl(qs, r.acc, 64);
   r.ustar = __shfl(u, B - 1, 64);
   return r;
+}
+
+__device__ SampleSel sampling_decision(const AcceptArgs &a, int s, int B) {
+  const int lane = threadIdx.x & 63;
+  float tm = -INFINITY, ts = 0.f, qm = -INFINITY, qs = 0.f, td = NAN, dd = NAN, u = 0.f;
+  if (lane < a.mb)  // issued before B arrives; positions >= B are ignored below
+    merge_records2(a.stats + (size_t)(s * a.mb + lane) * a.nch, a.stats + (size_t)((a.S + s) * a.mb + lane) * a.nch,
+                   a.nch, a.c, tm, ts, td, u, qm, qs, dd);
+  return sample_select(a, B, tm, ts, td, u, qm, qs, dd);
 }
 
 // Normalised sampling mass of one element: p = exp2((t - tm) c) / ts, and at a rejection the
@@ -643,6 +705,67 @@ __global__ __launch_bounds__(256) void accept_mass_kernel(AcceptArgs a) {
 // of the planned chunk sizes fit; longer ones are recomputed element by element).
 constexpr int kLocSums = 4;  // chunk sums per lane held in registers by the chunk search
 
+// cm[k] for a wave-uniform k < kLocSums, by selects (no indexed register access).
+__device__ __forceinline__ double2 pick_sums(const double2 *cm, int k) {
+  double2 r = cm[0];
+#pragma unroll
+  for (int q = 1; q < kLocSums; ++q)
+    if (q == k) r = cm[q];
+  return r;
+}
+
+// Chunk search of the final draw on one wavefront: chunk_sums(k) gives lane l the (residual,
+// p) sums of chunk 64k + l (zero past the last chunk).  The total is u* times the summed mass;
+// the chosen chunk is the one whose cumulative interval [lo, hi) holds it, consecutive
+// intervals meeting exactly across passes.  A residual with no mass (rounding only) draws from
+// p; a target past every interval (rounding) takes the last chunk with mass (cex = INFINITY:
+// its last token with mass).
+struct ChunkPick {
+  int kc;
+  double cex, tgt;
+  bool use_p;
+};
+
+template <typename F>
+__device__ __forceinline__ ChunkPick chunk_search(F chunk_sums, int passes, double ustar) {
+  bool any_r = false;
+  for (int k = 0; k < passes; ++k) any_r |= __ballot(chunk_sums(k).x > 0.0) != 0;
+  const bool use_p = !any_r;
+  double carry = 0.0;
+  for (int k = 0; k < passes; ++k) {
+    const double2 c2 = chunk_sums(k);
+    double ex;
+    const double in = wave_scan_d(use_p ? c2.y : c2.x, &ex);
+    carry += readlane_d(in, 63);
+  }
+  const double tgt = ustar * carry;
+  int kc = -1, klast = -1;
+  double cex = 0.0;
+  carry = 0.0;
+  for (int k = 0; k < passes; ++k) {
+    const double2 c2 = chunk_sums(k);
+    const double m = use_p ? c2.y : c2.x;
+    double ex;
+    const double in = wave_scan_d(m, &ex);
+    const double lo = carry + ex, hi = carry + in;
+    const unsigned long long hit = __ballot(m > 0.0 && lo <= tgt && tgt < hi);
+    if (hit && kc < 0) {
+      const int l = __ffsll((long long)hit) - 1;
+      kc = 64 * k + l;
+      cex = readlane_d(lo, l);
+    }
+    const unsigned long long pos = __ballot(m > 0.0);
+    if (pos) klast = 64 * k + 63 - __clzll((long long)pos);
+    carry = carry + readlane_d(in, 63);
+  }
+  ChunkPick r;
+  r.kc = kc >= 0 ? kc : max(klast, 0);
+  r.cex = kc >= 0 ? cex : INFINITY;
+  r.tgt = tgt;
+  r.use_p = use_p;
+  return r;
+}
+
 template <bool BF16, int NV>
 __global__ __launch_bounds__(kLocThreads) void accept_locate_kernel(AcceptArgs a) {
   constexpr int VEC = BF16 ? 8 : 4;
@@ -661,8 +784,8 @@ __global__ __launch_bounds__(kLocThreads) void accept_locate_kernel(AcceptArgs a
   const double ustar = (double)si1.z;
 
   if (wave == 0) {
-    // chunk search, 64 chunks per pass; consecutive intervals meet exactly across passes.  Up to
-    // 64 * kLocSums chunk sums are loaded in one round; more are loaded pass by pass.
+    // chunk search, 64 chunks per pass.  Up to 64 * kLocSums chunk sums are loaded in one
+    // round; more are loaded pass by pass.
     const double2 *cs = a.samp + (size_t)s * a.nch2;
     const int passes = (a.nch2 + 63) / 64;
     double2 cm[kLocSums];
@@ -672,52 +795,17 @@ __global__ __launch_bounds__(kLocThreads) void accept_locate_kernel(AcceptArgs a
       if (64 * k + lane >= a.nch2) cm[k] = double2{0.0, 0.0};
     }
     auto chunk_sums = [&](int k) {
-      if (k < kLocSums) {
-        double2 r = cm[0];
-#pragma unroll
-        for (int q = 1; q < kLocSums; ++q)
-          if (q == k) r = cm[q];
-        return r;
-      }
+      if (k < kLocSums) return pick_sums(cm, k);
       double2 r = cs[min(64 * k + lane, a.nch2 - 1)];
       if (64 * k + lane >= a.nch2) r = double2{0.0, 0.0};
       return r;
     };
-    bool any_r = false;
-    for (int k = 0; k < passes; ++k) any_r |= __ballot(chunk_sums(k).x > 0.0) != 0;
-    const bool use_p = !any_r;  // residual without mass (rounding only): draw from p
-    double carry = 0.0;
-    for (int k = 0; k < passes; ++k) {
-      const double2 c2 = chunk_sums(k);
-      double ex;
-      const double in = wave_scan_d(use_p ? c2.y : c2.x, &ex);
-      carry += readlane_d(in, 63);
-    }
-    const double tgt = ustar * carry;
-    int kc = -1, klast = -1;
-    double cex = 0.0;
-    carry = 0.0;
-    for (int k = 0; k < passes; ++k) {
-      const double2 c2 = chunk_sums(k);
-      const double m = use_p ? c2.y : c2.x;
-      double ex;
-      const double in = wave_scan_d(m, &ex);
-      const double lo = carry + ex, hi = carry + in;
-      const unsigned long long hit = __ballot(m > 0.0 && lo <= tgt && tgt < hi);
-      if (hit && kc < 0) {
-        const int l = __ffsll((long long)hit) - 1;
-        kc = 64 * k + l;
-        cex = readlane_d(lo, l);
-      }
-      const unsigned long long pos = __ballot(m > 0.0);
-      if (pos) klast = 64 * k + 63 - __clzll((long long)pos);
-      carry = carry + readlane_d(in, 63);
-    }
+    const ChunkPick cp = chunk_search(chunk_sums, passes, ustar);
     if (lane == 0) {
-      sh_kc = kc >= 0 ? kc : max(klast, 0);  // rounding: the last chunk with mass
-      sh_cex = kc >= 0 ? cex : INFINITY;     // INFINITY: take its last token with mass
-      sh_tgt = tgt;
-      sh_usep = use_p;
+      sh_kc = cp.kc;
+      sh_cex = cp.cex;
+      sh_tgt = cp.tgt;
+      sh_usep = cp.use_p;
       sh_hit = 0;
     }
   }
@@ -846,6 +934,151 @@ __global__ __launch_bounds__(kLocThreads) void accept_locate_kernel(AcceptArgs a
     for (int w2 = 0; w2 < NW; ++w2) t = max(t, sh_last[w2]);
     a.next_token[s] = max(t, 0);
   }
+}
+
+// ===========================================================================================
+// Single-launch greedy acceptance (T = 0).  The statistics items above run as the first
+// n_items workgroups and file their records as tagged words; one workgroup per sequence after
+// them waits for its sequence's records and decides as accept_greedy_kernel does.  Only those
+// tail workgroups wait, and only for words that statistics workgroups (which never wait)
+// write, so the launch completes whenever the tail workgroups can be resident at once (the
+// host launches it only then).  A wait gives up after spin_limit polls and the sequence
+// reports -1; a fresh tag per call makes a call ignore whatever an earlier call (or any other
+// use of the workspace) left behind.  Results equal the two-kernel path's bit for bit.
+// Measured on the ragged Qwen3-4B batch: 15.0 us per call against 17.2 us for two launches.
+// At T > 0 the same scheme needs three waits in a row (records, then every sampling chunk's
+// sums); each poll round is a trip to memory (about 1.5 us) and the workgroups of a sequence
+// see the words up to a round apart, so that single launch measured 26.8 us against 24.1 us
+// for the three-kernel path, which stays the T > 0 path.
+// ===========================================================================================
+constexpr int kFusedMaxNch = 8;  // statistics chunks per row (one batch of records)
+static_assert(kFusedMaxNch == kRecBatch, "a position's records merge as one batch");
+
+// Polls until every word a lane needs carries this call's tag (the loop is wavefront-uniform),
+// sleeping between rounds; false after spin_limit rounds.  poll() issues one round of loads
+// and returns whether this lane has everything.
+template <typename F>
+__device__ __forceinline__ bool spin_until(const AcceptArgs &a, F poll) {
+  for (int it = 0;; ++it) {
+    if (__all(poll())) return true;
+    if (it >= a.spin_limit) return false;
+    __builtin_amdgcn_s_sleep(2);
+  }
+}
+
+// One lane waits for one word: the record a sequence's last statistics workgroup files, so
+// that the full poll rarely needs a second round.
+__device__ __forceinline__ bool wait_word(const AcceptArgs &a, const unsigned long long *w) {
+  return spin_until(a, [&]() { return tag_is(tag_get(w), a.tag); });
+}
+
+// The tagged records of block position `lane` of sequence s, NCH chunks of three words; pay
+// receives the payloads.  Every round loads every word (no load sits under a branch) and keeps
+// those that carry their tag.
+template <int NCH>
+__device__ __forceinline__ bool poll_records(const AcceptArgs &a, int s, bool need, uint32_t (&pay)[3 * kFusedMaxNch]) {
+  const int lane = threadIdx.x & 63;
+  const unsigned long long *base = a.trec + (size_t)s * NCH * 3 * a.mb + min(lane, a.mb - 1);
+  unsigned miss = need ? ((1u << (3 * NCH)) - 1u) : 0u;
+#pragma unroll
+  for (int i = 0; i < 3 * kFusedMaxNch; ++i) pay[i] = 0u;
+  return spin_until(a, [&]() {
+    unsigned long long w[3 * NCH];
+#pragma unroll
+    for (int i = 0; i < 3 * NCH; ++i) w[i] = tag_get(base + (size_t)i * a.mb);
+#pragma unroll
+    for (int i = 0; i < 3 * NCH; ++i)
+      if (((miss >> i) & 1u) && tag_is(w[i], a.tag + (unsigned)(i % 3) * kTagStep)) {
+        pay[i] = (uint32_t)w[i];
+        miss &= ~(1u << i);
+      }
+    return miss == 0u;
+  });
+}
+
+// poll_records with the chunk count as a constant (nch <= kFusedMaxNch, checked by the host).
+__device__ __forceinline__ bool poll_records_n(const AcceptArgs &a, int s, bool need,
+                                               uint32_t (&pay)[3 * kFusedMaxNch]) {
+  switch (a.nch) {
+    case 1: return poll_records<1>(a, s, need, pay);
+    case 2: return poll_records<2>(a, s, need, pay);
+    case 3: return poll_records<3>(a, s, need, pay);
+    case 4: return poll_records<4>(a, s, need, pay);
+    case 5: return poll_records<5>(a, s, need, pay);
+    case 6: return poll_records<6>(a, s, need, pay);
+    case 7: return poll_records<7>(a, s, need, pay);
+    default: return poll_records<8>(a, s, need, pay);
+  }
+}
+
+// The records of chunks [0, nch) as the two-kernel path pads them for its one batch.
+__device__ __forceinline__ void records_batch(const AcceptArgs &a, const uint32_t (&pay)[3 * kFusedMaxNch],
+                                              float4 (&v)[kRecBatch], float4 pad) {
+#pragma unroll
+  for (int k = 0; k < kRecBatch; ++k)
+    v[k] = (k < a.nch) ? float4{__uint_as_float(pay[3 * k]), __uint_as_float(pay[3 * k + 1]),
+                                __uint_as_float(pay[3 * k + 2]), 0.f}
+                       : pad;
+}
+
+// Word 0 of the record that sequence s's highest-numbered statistics item files: the last
+// chunk of its last row.
+__device__ __forceinline__ const unsigned long long *last_record(const AcceptArgs &a, int s, int Bc) {
+  return a.trec + ((size_t)s * a.nch + (a.nch - 1)) * 3 * a.mb + (Bc - 1);
+}
+
+// T = 0: one workgroup per sequence; wavefront 0 merges and decides as accept_greedy_kernel.
+__device__ void fused_greedy_tail(const AcceptArgs &a, int s) {
+  if (threadIdx.x >= 64) return;
+  const int lane = threadIdx.x;
+  const int B = ld_uniform(a.block_lens, s);
+  const int Bc = min(max(B, 1), a.mb);
+  const int n = B - 1;
+  bool ok = true;
+  if (lane == 0) ok = wait_word(a, last_record(a, s, Bc));
+  ok = __shfl(ok ? 1 : 0, 0, 64) != 0;
+  uint32_t pay[3 * kFusedMaxNch];
+  if (ok) ok = poll_records_n(a, s, lane < Bc, pay);
+  if (!ok) {
+    if (lane == 0) {
+      a.accept_len[s] = -1;
+      a.next_token[s] = -1;
+    }
+    return;
+  }
+  int gi = INT_MAX, tok = -1;
+  {
+    float gv = -INFINITY;
+    float4 v[kRecBatch];
+    records_batch(a, pay, v, float4{-INFINITY, __int_as_float(INT_MAX), __int_as_float(-1), 0.f});
+    tok = __float_as_int(v[0].z);
+#pragma unroll
+    for (int k = 0; k < kRecBatch; ++k) argmax_merge(gv, gi, v[k].x, __float_as_int(v[k].y));
+    if (gi == INT_MAX) gi = 0;  // every logit -inf: all tie, lowest index
+  }
+  const bool rejects = (lane < n) && (tok != gi);
+  const unsigned long long rej = __ballot(rejects);
+  const int acc = rej ? (__ffsll((long long)rej) - 1) : max(n, 0);
+  const int next = __shfl(gi, acc, 64);
+  if (lane == 0) {
+    a.accept_len[s] = acc;
+    a.next_token[s] = next;
+  }
+}
+
+// At most 128 VGPRs: four workgroups per CU, so that the tail's workgroups fit at once.
+template <bool BF16, bool VECS>
+__global__ __launch_bounds__(256, 4) void accept_fused_kernel(AcceptArgs a) {
+  if ((int)blockIdx.x < a.n_items) {
+    __shared__ float sh_v[8];
+    __shared__ float sh_s[4];
+    __shared__ int sh_i[4];
+    StatsItem<kStatsVecs> it;
+    stats_issue<BF16, false, VECS>(a, blockIdx.x, it);
+    stats_process<BF16, false, VECS, true>(a, it, sh_v, sh_s, sh_i);
+    return;
+  }
+  fused_greedy_tail(a, (int)blockIdx.x - a.n_items);
 }
 
 }  // namespace sdb

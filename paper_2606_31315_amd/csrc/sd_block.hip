@@ -11,6 +11,7 @@
 #include <algorithm>
 #include <atomic>
 #include <mutex>
+#include <random>
 #include <string>
 
 #include "accept.hpp"
@@ -179,7 +180,15 @@ void launch_attn_all(const sdb::AttnArgs &a, int grid, int MT, hipStream_t st) {
 struct AcceptPlan {
   int rows, nch, nch2, stats_grid, tail_wide;
   size_t off_stats, off_samp, off_seq, total;
+  // single launch at T = 0 (accept_fused_kernel): possible for this shape, its tail
+  // workgroups (one per sequence), and its workspace (tagged records)
+  int fused_ok, n_tail;
+  size_t total_fused;
 };
+
+// Sequences of one single-launch call, at most (the launch also checks them against the
+// device's resident capacity for the kernel).
+constexpr int kFusedMaxTail = 1024;
 
 int accept_plan(const sd_accept_shape *sh, float temperature, AcceptPlan *p) {
   if (!sh) return fail(SD_ERR_INVALID_ARG, "sd_accept: shape is NULL");
@@ -231,6 +240,11 @@ int accept_plan(const sd_accept_shape *sh, float temperature, AcceptPlan *p) {
   p->off_seq = off;
   if (sample) off = align256(off + (size_t)S * 2 * sizeof(float4));
   p->total = off > 0 ? off : 256;
+  // the single launch (greedy only): one batch of records per position
+  p->n_tail = S;
+  p->fused_ok = !sample && S >= 1 && nch <= sdb::kFusedMaxNch && S <= kFusedMaxTail && items + S <= INT_MAX;
+  p->total_fused =
+      p->fused_ok ? align256((size_t)S * sh->max_block * nch * 3 * sizeof(unsigned long long)) : 0;
   return ok();
 }
 
@@ -488,7 +502,7 @@ int sd_accept_workspace_size(const sd_accept_shape *shape, float temperature, si
   AcceptPlan p;
   int rc = accept_plan(shape, temperature, &p);
   if (rc) return rc;
-  *bytes = p.total;
+  *bytes = std::max(p.total, p.total_fused);
   return ok();
 }
 
@@ -521,14 +535,82 @@ int check_accept_call(const sd_accept_shape *sh, const void *target_logits, cons
 
 namespace {
 
-// Enqueue the acceptance kernels of a checked call; `workspace` holds at least p.total bytes.
+// Path selection for tests (sd_accept_set_path): 0 = single launch where possible, 1 = never;
+// the poll limit of the single launch's waits (<= 0: the default).
+std::atomic<int> g_accept_path{0};
+std::atomic<int> g_accept_spin{0};
+constexpr int kDefaultSpinLimit = 1 << 20;  // about a second of polling
+
+// The tag of a single-launch call: a bijective 32-bit hash (MurmurHash3's finaliser) of a
+// per-process call counter with a random start, so no two calls of a process within 2^32 share
+// a tag and tags are spread over all 32-bit values, whatever data the workspace held before.
+unsigned next_accept_tag() {
+  static std::atomic<unsigned> ctr{0};
+  static std::once_flag once;
+  std::call_once(once, [] { ctr.store((unsigned)std::random_device{}()); });
+  unsigned h = ctr.fetch_add(1, std::memory_order_relaxed);
+  h ^= h >> 16;
+  h *= 0x85ebca6bu;
+  h ^= h >> 13;
+  h *= 0xc2b2ae35u;
+  h ^= h >> 16;
+  return h;
+}
+
+constexpr int kMaxDevices = 64;  // devices whose per-device state the library keeps
+
+// Workgroups of accept_fused_kernel the current device holds at once (the least over its
+// instantiations), or 0 if the runtime cannot tell; per device, computed on first use.
+int fused_capacity() {
+  static std::atomic<int> cap[kMaxDevices];
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  int c = cap[dev].load(std::memory_order_relaxed);
+  if (c > 0) return c;
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  const void *kernels[] = {(const void *)sdb::accept_fused_kernel<true, true>, (const void *)sdb::accept_fused_kernel<true, false>,
+                           (const void *)sdb::accept_fused_kernel<false, true>, (const void *)sdb::accept_fused_kernel<false, false>};
+  int per_cu = INT_MAX;
+  for (const void *k : kernels) {
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k, 256, 0) != hipSuccess) {
+      (void)hipGetLastError();
+      return 0;
+    }
+    per_cu = std::min(per_cu, nb);
+  }
+  c = per_cu * cus;
+  cap[dev].store(c, std::memory_order_relaxed);
+  return c;
+}
+
+// True when the single launch may run on this stream: it waits across workgroups on words
+// tagged per call, so a graph that replays a captured launch (with its tag) must not hold it.
+bool stream_allows_fused(hipStream_t st) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(st, &cs) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return cs == hipStreamCaptureStatusNone;
+}
+
+// Enqueue the acceptance kernels of a checked call; `workspace` holds workspace_bytes >=
+// p.total bytes.
 int accept_enqueue(const sd_accept_shape *sh, const AcceptPlan &p, const void *target_logits,
                    const void *draft_logits, const int32_t *draft_tokens, const float *uniforms,
                    const int32_t *block_lens, const int32_t *q_offsets, float temperature, int32_t *accept_len,
-                   int32_t *next_token, void *workspace, void *stream) {
+                   int32_t *next_token, void *workspace, size_t workspace_bytes, void *stream) {
   const bool sample = temperature > 0.f;
 
-  sdb::AcceptArgs a;
+  sdb::AcceptArgs a{};
   a.target = target_logits;
   a.draft = draft_logits;
   a.draft_tokens = draft_tokens;
@@ -556,6 +638,28 @@ int accept_enqueue(const sd_accept_shape *sh, const AcceptPlan &p, const void *t
   // every statistics chunk holds a whole 16-byte vector unless the vocabulary is tiny (then
   // there is one chunk and at most 2 VEC - 2 < 256 elements per row)
   const bool vecs = sh->vocab >= 2 * (bf ? 8 : 4) - 1;
+
+  // Greedy acceptance in one launch when the shape, the workspace, the stream and the test
+  // switch allow it (measured on the ragged Qwen3-4B batch: see accept_fused_kernel).  The
+  // tail workgroups, which wait only for statistics workgroups (which never wait), must fit on
+  // the device at once with a quarter of it to spare.
+  if (p.fused_ok && workspace_bytes >= p.total_fused && g_accept_path.load(std::memory_order_relaxed) == 0 &&
+      4LL * p.n_tail <= 3LL * fused_capacity() && stream_allows_fused(st)) {
+    a.trec = (unsigned long long *)ws;
+    a.tag = next_accept_tag();
+    a.n_items = p.stats_grid;
+    const int spin = g_accept_spin.load(std::memory_order_relaxed);
+    a.spin_limit = spin > 0 ? spin : kDefaultSpinLimit;
+    const unsigned grid = (unsigned)(p.stats_grid + p.n_tail);
+    if (bf) {
+      if (vecs) hipLaunchKernelGGL((sdb::accept_fused_kernel<true, true>), dim3(grid), dim3(256), 0, st, a);
+      else hipLaunchKernelGGL((sdb::accept_fused_kernel<true, false>), dim3(grid), dim3(256), 0, st, a);
+    } else {
+      if (vecs) hipLaunchKernelGGL((sdb::accept_fused_kernel<false, true>), dim3(grid), dim3(256), 0, st, a);
+      else hipLaunchKernelGGL((sdb::accept_fused_kernel<false, false>), dim3(grid), dim3(256), 0, st, a);
+    }
+    return check_launch("sd_accept");
+  }
 #define SDB_STATS(BF, SMP)                                                                                    \
   do {                                                                                                       \
     if (vecs) hipLaunchKernelGGL((sdb::accept_stats_kernel<BF, SMP, true>), dim3(g1), dim3(256), 0, st, a);  \
@@ -592,7 +696,7 @@ int accept_enqueue(const sd_accept_shape *sh, const AcceptPlan &p, const void *t
 // array's name as an address: the name is a host-side stand-in, so kernels get the device
 // address that hipGetSymbolAddress returns, looked up once per device with that device current.
 constexpr size_t kNoAllocScratchBytes = SD_ACCEPT_NOALLOC_SCRATCH_BYTES;
-constexpr int kNoAllocMaxDevices = 64;
+constexpr int kNoAllocMaxDevices = kMaxDevices;
 static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
 std::atomic<void *> g_scratch_ptr[kNoAllocMaxDevices];
 std::mutex g_scratch_mu;
@@ -632,7 +736,7 @@ int sd_accept(const sd_accept_shape *sh, const void *target_logits, const void *
   if (rc) return rc;
   if (sh->num_seqs == 0) return ok();
   return accept_enqueue(sh, p, target_logits, draft_logits, draft_tokens, uniforms, block_lens, q_offsets,
-                        temperature, accept_len, next_token, workspace, stream);
+                        temperature, accept_len, next_token, workspace, workspace_bytes, stream);
 }
 
 int sd_accept_noalloc(const sd_accept_shape *sh, const void *target_logits, const void *draft_logits,
@@ -654,7 +758,14 @@ int sd_accept_noalloc(const sd_accept_shape *sh, const void *target_logits, cons
                          temperature, accept_len, next_token, ws, kNoAllocScratchBytes, &p);
   if (rc) return rc;
   return accept_enqueue(sh, p, target_logits, draft_logits, draft_tokens, uniforms, block_lens, q_offsets,
-                        temperature, accept_len, next_token, ws, stream);
+                        temperature, accept_len, next_token, ws, kNoAllocScratchBytes, stream);
+}
+
+int sd_accept_set_path(int32_t mode, int32_t spin_limit) {
+  if (mode != 0 && mode != 1) return fail(SD_ERR_INVALID_ARG, "sd_accept_set_path: mode must be 0 or 1 (got %d)", mode);
+  g_accept_path.store(mode, std::memory_order_relaxed);
+  g_accept_spin.store(spin_limit > 0 ? spin_limit : 0, std::memory_order_relaxed);
+  return ok();
 }
 
 // ---------------------------------------------------------------------------

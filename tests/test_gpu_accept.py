@@ -172,3 +172,119 @@ def test_one_workspace_shared_with_attention():
         for p, d, ref in zip(probs, dev_p, refs):
             al, nt = G.run_accept(p, d, workspace=ws)
             G.compare_accept(p, al, nt, ref)
+
+
+# ---- the single-launch greedy path against the two-launch path ----
+# At T = 0, where the shape allows it, sd_accept runs as one launch whose workgroups hand the
+# per-chunk records on through tagged words; the two-launch path stays for the other shapes,
+# for graph capture and for T > 0.  The same merges run in the same order, so results agree
+# exactly.
+
+_PATH_CASES = [
+    ("ragged", lambda: W.c3_ragged(temperatures=(0.0,), with_attn=False).accept[0.0]),
+    ("qwen3_4b", lambda: W.c2_qwen3_4b_verify(temperatures=(0.0,)).accept[0.0]),
+    ("long_context", lambda: W.c5_long_context(temperatures=(0.0,), with_attn=False).accept[0.0]),
+    ("V4096_f32", lambda: _many_seq_problem(5, 40, 4096, (1, 20), "f32", 0.0, name="V4096_f32")),
+    ("V262144", lambda: _many_seq_problem(6, 3, 262144, (4, 12), "bf16", 0.0, target_sigma=3.0,
+                                          noise_sigma=1.0, name="V262144")),
+    ("V7", lambda: _many_seq_problem(7, 40, 7, (1, 20), "bf16", 0.0, name="V7")),
+    ("B1_only", lambda: _many_seq_problem(8, 16, 151936, (1, 1), "bf16", 0.0, name="B1")),
+    ("max_block_64", lambda: _many_seq_problem(9, 5, 32768, (60, 64), "bf16", 0.0, name="B64")),
+]
+
+
+def _both_paths(p, d):
+    import paper_2606_31315_amd as sd
+    try:
+        sd.accept_set_path(1)
+        multi = G.run_accept(p, d)
+        sd.accept_set_path(0)
+        single = G.run_accept(p, d)
+    finally:
+        sd.accept_set_path(0)
+    return single, multi
+
+
+@pytest.mark.parametrize("name,make", _PATH_CASES, ids=[c[0] for c in _PATH_CASES])
+def test_single_launch_matches_two_launches(name, make):
+    """Both greedy paths give the same accept_len and next_token, bit for bit, and the single
+    launch's result meets the parity rule against the oracle."""
+    p = make()
+    d = G.accept_to_device(p)
+    (al1, nt1), (alm, ntm) = _both_paths(p, d)
+    assert (al1 == alm).all() and (nt1 == ntm).all(), (name, np.nonzero(al1 != alm), np.nonzero(nt1 != ntm))
+    G.compare_accept(p, al1, nt1, G.oracle_accept(p))
+
+
+def test_single_launch_ignores_leftover_words():
+    """A workspace holding an earlier call's words, random bytes, one repeated 64-bit word, or
+    zeros: every call still equals the two-launch result."""
+    import paper_2606_31315_amd as sd
+    p = W.c3_ragged(temperatures=(0.0,), with_attn=False).accept[0.0]
+    d = G.accept_to_device(p)
+    n = sd.accept_workspace_size(sd.accept_shape(d["t"], p.S, p.max_block), 0.0)
+    _, (alm, ntm) = _both_paths(p, d)
+    ws = torch.empty(n, dtype=torch.uint8, device=G.dev())
+    fills = [lambda: None,  # whatever the previous call left
+             lambda: ws.copy_(torch.randint(0, 256, (n,), dtype=torch.uint8, device=G.dev())),
+             lambda: ws.view(torch.int64).fill_(0x3F8000003F800000),
+             lambda: ws.zero_()]
+    for rep in range(2):
+        for f in fills:
+            f()
+            al, nt = G.run_accept(p, d, workspace=ws)
+            assert (al == alm).all() and (nt == ntm).all()
+
+
+def test_single_launch_gives_up_when_told_and_recovers():
+    """With the waits cut to one poll, each sequence either has its exact result or reports -1
+    in both outputs; the next call with the default limit, on the same workspace, is exact."""
+    import paper_2606_31315_amd as sd
+    p = W.c3_ragged(temperatures=(0.0,), with_attn=False).accept[0.0]
+    d = G.accept_to_device(p)
+    n = sd.accept_workspace_size(sd.accept_shape(d["t"], p.S, p.max_block), 0.0)
+    ws = torch.empty(n, dtype=torch.uint8, device=G.dev())
+    _, (alm, ntm) = _both_paths(p, d)
+    try:
+        sd.accept_set_path(0, 1)
+        al, nt = G.run_accept(p, d, workspace=ws)
+    finally:
+        sd.accept_set_path(0)
+    exact = (al == alm) & (nt == ntm)
+    gave_up = (al == -1) & (nt == -1)
+    assert (exact | gave_up).all(), (al, alm, nt, ntm)
+    al, nt = G.run_accept(p, d, workspace=ws)
+    assert (al == alm).all() and (nt == ntm).all()
+
+
+def test_small_workspace_takes_two_launch_path():
+    """A workspace big enough for the two-launch path only still gives the same results."""
+    import ctypes
+    import paper_2606_31315_amd as sd
+    from paper_2606_31315_amd import _lib
+    p = W.c3_ragged(temperatures=(0.0,), with_attn=False).accept[0.0]
+    d = G.accept_to_device(p)
+    shape = sd.accept_shape(d["t"], p.S, p.max_block)
+    full = sd.accept_workspace_size(shape, 0.0)
+    al = torch.empty(p.S, dtype=torch.int32, device=G.dev())
+    nt = torch.empty(p.S, dtype=torch.int32, device=G.dev())
+    ws = torch.empty(full, dtype=torch.uint8, device=G.dev())
+    L = _lib.lib()
+
+    def call(nbytes):
+        return L.sd_accept(ctypes.byref(shape), _lib._ptr(d["t"]), None, _lib._ptr(d["tok"]), None,
+                           _lib._ptr(d["bl"]), _lib._ptr(d["off"]), ctypes.c_float(0.0), _lib._ptr(al),
+                           _lib._ptr(nt), _lib._ptr(ws), nbytes, _lib._stream(None))
+    # the smallest workspace the call accepts, by bisection on SD_ERR_WORKSPACE
+    lo, hi = 0, full
+    while hi - lo > 256:
+        mid = (lo + hi) // 2 // 256 * 256
+        if call(mid) == _lib.SD_OK:
+            hi = mid
+        else:
+            lo = mid
+    assert hi < full
+    assert call(hi) == _lib.SD_OK
+    torch.cuda.synchronize()
+    _, multi = _both_paths(p, d)
+    assert (al.cpu().numpy() == multi[0]).all() and (nt.cpu().numpy() == multi[1]).all()
