@@ -579,7 +579,8 @@ __global__ __launch_bounds__(256) void block_attn_kernel(AttnArgs a) {
 // Merge of the split partials: workgroup (s, g, row block) combines
 //   O = sum_sp 2^(m_sp - M) O_sp / sum_sp 2^(m_sp - M) l_sp,  M = max_sp m_sp
 // for RB rows of the (sequence, kv head) group, D/4 threads per row, one float4 each.
-template <bool BF16, int D>
+// SB: splits whose loads are issued together (the host sizes it to the plan's split count).
+template <bool BF16, int D, int SB>
 __global__ __launch_bounds__(256) void block_attn_merge_kernel(AttnArgs a) {
   constexpr int EB = BF16 ? 2 : 4;
   constexpr int TPR = D / 4;       // threads per row
@@ -599,7 +600,6 @@ __global__ __launch_bounds__(256) void block_attn_merge_kernel(AttnArgs a) {
   const size_t wbase = (size_t)ps.x * a.Mpad + m;  // row m of split 0
   // online merge over batches of SB splits whose loads are issued together (clamped, no
   // per-load branch): one memory round trip per batch instead of one per split
-  constexpr int SB = 4;
   float mx = -INFINITY, lsum = 0.f;
   f32x4 acc{0.f, 0.f, 0.f, 0.f};
   for (int s0 = 0; s0 < nsplit; s0 += SB) {
