@@ -219,9 +219,13 @@ __device__ __forceinline__ bool attn_item(const AttnArgs &a, int b, AttnItem &it
 // Partial slot of split 0 of pair (s, g) and the pair's split count (0: no block).
 __device__ __forceinline__ int2 attn_pair_slots(const AttnArgs &a, int s, int g, int &B) {
   if (!a.dense) {
-    B = a.block_lens[s];
+    // both lengths in one round of scalar loads: one use of both before the branch on B, so the
+    // context length's load is not sunk behind it
+    B = ld_uniform(a.block_lens, s);
+    int ctx = ld_uniform(a.ctx_lens, s);
+    asm volatile("" : "+s"(B), "+s"(ctx));
     if (B <= 0) return int2{0, 0};
-    return int2{(s * a.Hkv + g) * a.max_splits, (a.ctx_lens[s] + B + a.split_len - 1) / a.split_len};
+    return int2{(s * a.Hkv + g) * a.max_splits, (ctx + B + a.split_len - 1) / a.split_len};
   }
   const int lane = threadIdx.x & 63;
   int before = 0;
@@ -589,6 +593,7 @@ __global__ __launch_bounds__(256) void block_attn_merge_kernel(AttnArgs a) {
   const int rb = blockIdx.x % nrb;
   const int sg = blockIdx.x / nrb;
   const int s = sg / a.Hkv, g = sg % a.Hkv;
+  const int qoff = ld_uniform(a.q_offsets, s);  // issued with the lengths, not after the merge
   int B;
   const int2 ps = attn_pair_slots(a, s, g, B);
   const int nsplit = ps.y;
@@ -623,7 +628,6 @@ __global__ __launch_bounds__(256) void block_attn_merge_kernel(AttnArgs a) {
     }
   }
   const f32x4 o = acc * (1.f / lsum);
-  const int qoff = a.q_offsets[s];
   char *orow = reinterpret_cast<char *>(a.out) + ((size_t)(qoff + m / a.G) * a.Hq + g * a.G + m % a.G) * D * EB;
   if constexpr (BF16)
     *reinterpret_cast<uint2 *>(orow + d * EB) = uint2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
