@@ -696,7 +696,7 @@ def main():
                                                      "block_attn_bf16_kernel + block_attn_merge_kernel",
                                                      traffic["sd_block_attn"]),
                          "sd_accept": call_entry(acc_us, acc_bytes,
-                                                 "accept_stats_kernel + accept_mass_kernel + accept_locate_kernel",
+                                                 "accept_stats_kernel + accept_draw_kernel",
                                                  traffic["sd_accept"])}},
     }
     # rows a sequential acceptance would have read: target rows 0..accept_len and the drafts

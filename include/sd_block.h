@@ -164,7 +164,7 @@ typedef struct sd_accept_shape {
 } sd_accept_shape;
 
 /* Workspace bytes sd_accept needs for this shape at this temperature (host-only): enough for
- * the single-launch path described under sd_accept where the shape allows it. */
+ * the tagged-word paths described under sd_accept where the shape allows them. */
 int sd_accept_workspace_size(const sd_accept_shape *shape, float temperature, size_t *bytes);
 
 /*
@@ -194,14 +194,19 @@ int sd_accept_workspace_size(const sd_accept_shape *shape, float temperature, si
  * accumulated in fp32, the acceptance ratio and the final draw's cumulative sums in fp64;
  * decisions within about 1e-6 of a boundary may differ from an fp64 evaluation.
  *
- * Paths.  At T = 0, where the shape allows it (at most 8 statistics chunks of 32768 bf16 /
- * 16384 fp32 logits per row, at most 1024 sequences), the workspace holds
- * sd_accept_workspace_size bytes and the stream is not capturing a graph, acceptance runs as
- * one launch whose workgroups hand the per-chunk records on through tagged words in the
- * workspace; otherwise, and at T > 0 always, as two launches (three at T > 0).  Both give
- * identical results.  The single launch needs one waiting workgroup per sequence resident; if
- * a wait gives up (after about a second, e.g. when other work holds the device), that sequence
- * reports -1 in accept_len and next_token.
+ * Paths.  Where the workspace holds sd_accept_workspace_size bytes, the stream is not
+ * capturing a graph and the shape allows it, workgroups hand partial results on through
+ * tagged words in the workspace instead of kernel boundaries:
+ *   T = 0: one launch (at most 8 statistics chunks of 32768 bf16 / 16384 fp32 logits per row,
+ *          at most 1024 sequences) instead of two;
+ *   T > 0: two launches instead of three (rows of at most 256 sampling chunks of 256 16-byte
+ *          vectors, i.e. 524288 bf16 / 262144 fp32 logits, and the num_seqs x chunks
+ *          workgroups of the second launch resident at once with a quarter of the device to
+ *          spare).
+ * Every path gives identical results.  The single launches need their waiting workgroups
+ * resident; a wait that gives up (after about a second, e.g. when other work holds the device)
+ * writes -1: at T = 0 its sequence reports -1 in accept_len and next_token, at T > 0 in one or
+ * both (an output that is not -1 is exact).
  * Errors: SD_ERR_INVALID_ARG, SD_ERR_WORKSPACE (smaller than the multi-launch path needs),
  * SD_ERR_HIP.  S == 0 returns SD_OK.
  */
@@ -235,7 +240,7 @@ int sd_accept_noalloc(const sd_accept_shape *shape, const void *target_logits, c
 
 /*
  * Test hook for the acceptance paths of the calls enqueued after it, process-wide:
- *   mode 0 (default): the single launch where sd_accept's "Paths" allow it; 1: never.
+ *   mode 0 (default): the tagged-word launches where sd_accept's "Paths" allow them; 1: never.
  *   spin_limit > 0: polls before a wait of the single launch gives up; <= 0: the default.
  * Errors: SD_ERR_INVALID_ARG for another mode.
  */

@@ -9,10 +9,11 @@
 //
 // Kernels (gfx950).  An agent-scope fence per workgroup costs an L2 write-back on gfx950
 // and one workgroup streams a row far below HBM speed, so every phase that needs a whole
-// row spreads it over many workgroups and hands results on across a kernel boundary.
-// (Measured on the ragged Qwen3-4B batch at T = 1: drawing the token in the mass kernel's
-// last workgroup per sequence, found by a counter behind a release fence, made the call
-// 35.9 us against 29.7 us with the separate locate kernel.)
+// row spreads it over many workgroups and hands results on across a kernel boundary, or
+// through tagged words that need no fence (the single launches below).  (Measured on the
+// ragged Qwen3-4B batch at T = 1: drawing the token in the mass kernel's last workgroup per
+// sequence, found by a counter behind a release fence, made the call 35.9 us against 29.7 us
+// with the separate locate kernel.)
 //   accept_stats_kernel     persistent grid over (row, vocab chunk) items of every target
 //                           row, and every draft row when T > 0.  One streaming pass of
 //                           16-byte loads: T = 0 keeps (max value, lowest index); T > 0 keeps
@@ -29,6 +30,12 @@
 //   accept_locate_kernel    T > 0, one workgroup per sequence: scans the chunk sums for the
 //                           chunk holding u* times the total mass, then scans that chunk in
 //                           vocabulary order.
+//   accept_fused_kernel     T = 0 in one launch: the statistics items, then one workgroup per
+//                           sequence that waits for its records (tagged words) and decides.
+//   accept_draw_kernel      T > 0, the mass and locate steps in one launch: the chunk sums are
+//                           handed between the workgroups of a sequence as tagged words.
+// The single launches run where the shape, the workspace and the stream allow them; the
+// launches above stay for the other cases and give the same results bit for bit.
 #pragma once
 
 #include <limits.h>
@@ -67,6 +74,10 @@ struct AcceptArgs {
   unsigned tag;              // this call's tag (a bijective hash of a per-process call counter)
   int n_items;               // statistics workgroups; workgroups past them run the tail
   int spin_limit;            // polls before a waiting workgroup gives up
+  // Single-launch draw (accept_draw_kernel, T > 0): the residual and p mass sums of every
+  // sampling chunk (floats) as tagged words, word k (0 residual, 1 p) carrying tag + k * kTagStep,
+  // at index (s * 2 + k) * nch2 + chunk.
+  unsigned long long *csum;
 };
 
 // ---- tagged words: one relaxed 64-bit atomic store or load at agent scope each ----
@@ -597,6 +608,25 @@ __device__ __forceinline__ void elem_masses(float t, float q, const SampleParams
 // then sums the residual (or p at the bonus row) and p over its chunk of the selected row.
 // NV: vectors per thread per round; the plan sizes chunks so that one round of NV = 1 covers
 // a chunk, which keeps the dependent chain at one round of row loads after the decision.
+// Wavefront 0 of a workgroup of sequence s decides and leaves the selection in sh_si:
+// (accept_len bits, residual?, target max, 1/target sum), (draft max, 1/draft sum, u*, -).
+// With publish set it also writes accept_len and the selection for the locate kernel.
+__device__ __forceinline__ void mass_decide(const AcceptArgs &a, int s, int B, float4 *sh_si, bool publish) {
+  if (threadIdx.x >= 64) return;
+  const SampleSel sel = sampling_decision(a, s, B);
+  if (threadIdx.x == 0) {
+    const float4 s0{__int_as_float(sel.acc), sel.residual ? 1.f : 0.f, sel.tm, 1.f / sel.ts};
+    const float4 s1{sel.residual ? sel.qm : 0.f, sel.residual ? 1.f / sel.qs : 0.f, sel.ustar, 0.f};
+    sh_si[0] = s0;
+    sh_si[1] = s1;
+    if (publish) {
+      a.accept_len[s] = sel.acc;
+      a.seqinfo[2 * s] = s0;
+      a.seqinfo[2 * s + 1] = s1;
+    }
+  }
+}
+
 template <bool BF16, int NV>
 __global__ __launch_bounds__(256) void accept_mass_kernel(AcceptArgs a) {
   constexpr int VEC = BF16 ? 8 : 4;
@@ -607,20 +637,7 @@ __global__ __launch_bounds__(256) void accept_mass_kernel(AcceptArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int B = ld_uniform(a.block_lens, s);
   const int off = ld_uniform(a.q_offsets, s);
-  if (wave == 0) {
-    const SampleSel sel = sampling_decision(a, s, B);
-    if (lane == 0) {
-      const float4 s0{__int_as_float(sel.acc), sel.residual ? 1.f : 0.f, sel.tm, 1.f / sel.ts};
-      const float4 s1{sel.residual ? sel.qm : 0.f, sel.residual ? 1.f / sel.qs : 0.f, sel.ustar, 0.f};
-      sh_si[0] = s0;
-      sh_si[1] = s1;
-      if (c == 0) {
-        a.accept_len[s] = sel.acc;
-        a.seqinfo[2 * s] = s0;
-        a.seqinfo[2 * s + 1] = s1;
-      }
-    }
-  }
+  mass_decide(a, s, B, sh_si, c == 0);
   __syncthreads();
   const float4 si0 = sh_si[0], si1 = sh_si[1];
   const int j = __float_as_int(si0.x);
@@ -692,8 +709,9 @@ __global__ __launch_bounds__(256) void accept_mass_kernel(AcceptArgs a) {
   const float wr = wave_sum_f(sr), wp = wave_sum_f(spm);
   if (lane == 0) { sh_r[wave] = wr; sh_p[wave] = wp; }
   __syncthreads();
-  if (tid == 0)
-    a.samp[(size_t)s * a.nch2 + c] = double2{sh_r[0] + sh_r[1] + sh_r[2] + sh_r[3], sh_p[0] + sh_p[1] + sh_p[2] + sh_p[3]};
+  if (tid == 0)  // rounded to float, as accept_draw_kernel files them
+    a.samp[(size_t)s * a.nch2 + c] = double2{(double)(float)(sh_r[0] + sh_r[1] + sh_r[2] + sh_r[3]),
+                                             (double)(float)(sh_p[0] + sh_p[1] + sh_p[2] + sh_p[3])};
 }
 
 // Final draw for sequence s (T > 0), one workgroup per sequence.  Wavefront 0 scans the
@@ -946,10 +964,11 @@ __global__ __launch_bounds__(kLocThreads) void accept_locate_kernel(AcceptArgs a
 // reports -1; a fresh tag per call makes a call ignore whatever an earlier call (or any other
 // use of the workspace) left behind.  Results equal the two-kernel path's bit for bit.
 // Measured on the ragged Qwen3-4B batch: 15.0 us per call against 17.2 us for two launches.
-// At T > 0 the same scheme needs three waits in a row (records, then every sampling chunk's
-// sums); each poll round is a trip to memory (about 1.5 us) and the workgroups of a sequence
-// see the words up to a round apart, so that single launch measured 26.8 us against 24.1 us
-// for the three-kernel path, which stays the T > 0 path.
+// At T > 0 a launch holding the statistics too needs two waits in a row (records, then every
+// sampling chunk's sums); each poll round is a trip to memory (about 1.5 us) and the
+// workgroups of a sequence see the records up to a round apart, so that single launch
+// measured 26.8 us against 24.1 us for three launches.  The statistics stay a launch of their
+// own at T > 0, and accept_draw_kernel below joins the mass and locate steps.
 // ===========================================================================================
 constexpr int kFusedMaxNch = 8;  // statistics chunks per row (one batch of records)
 static_assert(kFusedMaxNch == kRecBatch, "a position's records merge as one batch");
@@ -1079,6 +1098,287 @@ __global__ __launch_bounds__(256, 4) void accept_fused_kernel(AcceptArgs a) {
     return;
   }
   fused_greedy_tail(a, (int)blockIdx.x - a.n_items);
+}
+
+// ===========================================================================================
+// Sampling draw in one launch (T > 0, sampling chunks of at most 256 vectors).  Grid =
+// (sequence, sampling chunk), as accept_mass_kernel: every workgroup decides and sums its chunk
+// of the selected row as that kernel does, keeping its elements' masses in registers, and files
+// the chunk's two sums as tagged words.  While wavefront 0 waits for every chunk sum of the
+// sequence, the workgroup scans its own chunk as accept_locate_kernel would (run masses and
+// their prefixes over the chunk).  Every workgroup of a sequence then runs the locate kernel's
+// chunk search on the same words, so all agree on the chunk that holds u* times the total, and
+// only that chunk's workgroup goes on: the thread whose interval holds the target walks its run
+// and writes the outputs.  The sums are the mass kernel's, rounded to float as that kernel files
+// them, and the scans are the locate kernel's, so results agree bit for bit with the two
+// launches.  Every workgroup waits for all workgroups of its sequence, so the host launches it
+// only when the whole grid fits on the device at once with a quarter to spare.  A wait that
+// gives up after spin_limit polls writes -1 to both outputs of its sequence; the chosen chunk's
+// workgroup, once its wait has succeeded, writes the exact values, so an output that is not -1
+// is exact.  Measured on the ragged Qwen3-4B batch at T = 1: 22.7 us per call against 24.3 us
+// for the statistics, mass and locate launches (A/B, same box): the wait for the last chunk sum
+// (one round trip, about 1.5 us) replaces a kernel boundary and the locate kernel's two rounds
+// of loads.
+// ===========================================================================================
+
+// Poll the chunk sums of sequence s: lane l receives chunk 64k + l in cm[k] for k < P (zero
+// past the last chunk).  Rounds load only the residual sums, one word per chunk, until each
+// carries its tag: every workgroup of a sequence polls the same lines.  The p sums matter only
+// when no chunk has residual mass (the chunk search then draws from p); only then are they
+// polled too.  No load sits under a per-lane branch.  (Measured on the ragged Qwen3-4B batch:
+// polling all four halves of two double sums per chunk, 25.4 us per call; one float word,
+// 24.3 us; keeping two rounds in flight, a new one every half round trip, 23.9 us against
+// 22.7 us with one round at a time, since every extra load lands on the lines the sequence's
+// other workgroups poll.)
+template <int P>
+__device__ __forceinline__ bool poll_chunk_sums(const AcceptArgs &a, int s, double2 (&cm)[kLocSums]) {
+  static_assert(P >= 1 && P <= kLocSums, "chunk sums held in registers");
+  const int lane = threadIdx.x & 63;
+  const unsigned long long *base = a.csum + (size_t)s * 2 * a.nch2;
+  float r[P], pm[P];
+  unsigned miss = 0u;
+#pragma unroll
+  for (int k = 0; k < P; ++k) {
+    r[k] = pm[k] = 0.f;
+    if (64 * k + lane < a.nch2) miss |= 1u << k;
+  }
+  auto poll = [&](int kind, float (&dst)[P]) {
+    const unsigned tag = a.tag + (unsigned)kind * kTagStep;
+    unsigned m = miss;
+    auto issue = [&](unsigned long long (&w)[P]) {
+#pragma unroll
+      for (int k = 0; k < P; ++k) w[k] = tag_get(base + (size_t)kind * a.nch2 + min(64 * k + lane, a.nch2 - 1));
+    };
+    auto take = [&](const unsigned long long (&w)[P]) {
+#pragma unroll
+      for (int k = 0; k < P; ++k)
+        if (((m >> k) & 1u) && tag_is(w[k], tag)) {
+          dst[k] = tag_f(w[k]);
+          m &= ~(1u << k);
+        }
+      return m == 0u;
+    };
+    return spin_until(a, [&]() {
+      unsigned long long w[P];
+      issue(w);
+      return take(w);
+    });
+  };
+  bool ok = poll(0, r);
+  bool any_r = false;
+#pragma unroll
+  for (int k = 0; k < P; ++k) any_r |= __ballot(r[k] > 0.f) != 0;
+  if (ok && !any_r) ok = poll(1, pm);
+#pragma unroll
+  for (int k = 0; k < kLocSums; ++k) cm[k] = double2{0.0, 0.0};
+#pragma unroll
+  for (int k = 0; k < P; ++k) cm[k] = double2{(double)r[k], (double)pm[k]};
+  return ok;
+}
+
+__device__ __forceinline__ bool poll_chunk_sums_n(const AcceptArgs &a, int s, double2 (&cm)[kLocSums]) {
+  static_assert(kLocSums == 4, "one case per pass count");
+  switch ((a.nch2 + 63) / 64) {
+    case 1: return poll_chunk_sums<1>(a, s, cm);
+    case 2: return poll_chunk_sums<2>(a, s, cm);
+    case 3: return poll_chunk_sums<3>(a, s, cm);
+    default: return poll_chunk_sums<4>(a, s, cm);
+  }
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(256, 4) void accept_draw_kernel(AcceptArgs a) {
+  constexpr int VEC = BF16 ? 8 : 4;
+  constexpr int NW = 4;
+  static_assert(kLocThreads == 64 * NW, "the chunk scan runs on the whole workgroup");
+  __shared__ float4 sh_si[2];
+  __shared__ double sh_r[NW], sh_p[NW], sh_w[NW];
+  __shared__ float sh_em[2][2][2 * VEC];  // [head, tail][residual, p] masses of the scalar elements
+  __shared__ double sh_cex, sh_tgt;
+  __shared__ int sh_kc, sh_usep, sh_ok, sh_hit, sh_last[NW];
+  const int s = blockIdx.x / a.nch2;
+  const int c = blockIdx.x % a.nch2;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int B = ld_uniform(a.block_lens, s);
+  const int off = ld_uniform(a.q_offsets, s);
+  mass_decide(a, s, B, sh_si, false);
+  __syncthreads();
+  const float4 si0 = sh_si[0], si1 = sh_si[1];
+  const int j = __float_as_int(si0.x);
+  const bool residual = si0.y != 0.f;
+  const SampleParams sp{si0.z, si0.w, si1.x, si1.y, a.c};
+  const long long ta0 = (long long)(off + j) * a.V;
+  const long long da0 = (long long)(off - s + j) * a.V;  // read only at a rejection
+  const RowChunk ch = row_chunk<VEC>(ta0, a.V, c, a.nch2);
+  const bool dvec = ((ta0 - da0) % VEC) == 0;
+  const int nvc = (int)(ch.ve - ch.vb);  // <= 256: one vector per thread
+  const bool has = tid < nvc;
+
+  // ---- the chunk's masses: accept_mass_kernel's sums, element by element ----
+  float mr[VEC], mp[VEC];
+  float sr = 0.f, spm = 0.f;
+  {
+    u32x4 tb{0u, 0u, 0u, 0u}, qb{0u, 0u, 0u, 0u};
+    if (nvc > 0) {  // clamped: no per-load branch
+      const unsigned r = (unsigned)min(tid, nvc - 1);
+      tb = *reinterpret_cast<const u32x4 *>(reinterpret_cast<const char *>(a.target) + (ch.vb + r) * 16);
+      if (residual && dvec)
+        qb = *reinterpret_cast<const u32x4 *>(reinterpret_cast<const char *>(a.draft) +
+                                              (ch.vb + r + (da0 - ta0) / VEC) * 16);
+    }
+    float t[VEC], q[VEC];
+    unpack<BF16>(tb, t);
+    unpack<BF16>(qb, q);
+    if (residual && !dvec && has) {
+      const long long e = (ch.vb + tid) * VEC - ta0 + da0;
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) q[i] = load_elem<BF16>(a.draft, e + i);
+    }
+    float vr = 0.f, vp = 0.f;
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) {
+      elem_masses(t[i], q[i], sp, residual, mr[i], mp[i]);
+      vr += mr[i];
+      vp += mp[i];
+    }
+    if (has) {
+      sr += vr;
+      spm += vp;
+    }
+  }
+  // scalar head (chunk 0) and tail (last chunk): fewer than 2 * VEC elements each, one per thread
+  for (int e = ch.hb + tid; e < ch.he; e += 256) {
+    float er, ep;
+    elem_masses(load_elem<BF16>(a.target, ta0 + e), residual ? load_elem<BF16>(a.draft, da0 + e) : 0.f, sp,
+                residual, er, ep);
+    sr += er;
+    spm += ep;
+    if (e - ch.hb < 2 * VEC) { sh_em[0][0][e - ch.hb] = er; sh_em[0][1][e - ch.hb] = ep; }
+  }
+  for (int e = ch.tb + tid; e < ch.te; e += 256) {
+    float er, ep;
+    elem_masses(load_elem<BF16>(a.target, ta0 + e), residual ? load_elem<BF16>(a.draft, da0 + e) : 0.f, sp,
+                residual, er, ep);
+    sr += er;
+    spm += ep;
+    if (e - ch.tb < 2 * VEC) { sh_em[1][0][e - ch.tb] = er; sh_em[1][1][e - ch.tb] = ep; }
+  }
+  const float wr = wave_sum_f(sr), wp = wave_sum_f(spm);
+  if (lane == 0) { sh_r[wave] = wr; sh_p[wave] = wp; }
+  __syncthreads();
+  if (tid == 0) {  // the chunk's sums, rounded to float as accept_mass_kernel files them
+    const float cr = (float)(sh_r[0] + sh_r[1] + sh_r[2] + sh_r[3]), cp = (float)(sh_p[0] + sh_p[1] + sh_p[2] + sh_p[3]);
+    unsigned long long *w = a.csum + (size_t)s * 2 * a.nch2 + c;
+    tag_put(w, a.tag, __float_as_uint(cr));
+    tag_put(w + a.nch2, a.tag + kTagStep, __float_as_uint(cp));
+  }
+
+  // ---- the chunk's scan, ahead of the chunk search: accept_locate_kernel's run masses
+  // (residual masses at a rejection) and their prefixes over the chunk.  Only where no chunk
+  // of the sequence has residual mass (rounding only) is it redone with p. ----
+  const int eb = (int)((ch.vb + tid) * VEC - ta0);
+  float mm[VEC];
+  double pre_lo, pre_hi, own;
+  int elast;
+  auto chunk_scan = [&](bool use_q) {
+    own = 0.0;
+    elast = -1;
+    if (tid == 0)
+      for (int e = ch.hb; e < ch.he; ++e) {
+        const float m = use_q ? sh_em[0][0][e - ch.hb] : sh_em[0][1][e - ch.hb];
+        own += (double)m;
+        if (m > 0.f) elast = e;
+      }
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) {
+      const float m = has ? (use_q ? mr[i] : mp[i]) : 0.f;
+      mm[i] = m;
+      own += (double)m;
+      if (m > 0.f) elast = eb + i;
+    }
+    if (tid == kLocThreads - 1)
+      for (int e = ch.tb; e < ch.te; ++e) {
+        const float m = use_q ? sh_em[1][0][e - ch.tb] : sh_em[1][1][e - ch.tb];
+        own += (double)m;
+        if (m > 0.f) elast = e;
+      }
+    double ex;
+    const double in = wave_scan_d(own, &ex);
+    const int wl = wave_max_i(elast);
+    if (lane == 63) sh_w[wave] = in;
+    if (lane == 0) sh_last[wave] = wl;
+    __syncthreads();
+    double before = 0.0;
+    for (int w2 = 0; w2 < wave; ++w2) before += sh_w[w2];
+    pre_lo = before + ex;
+    pre_hi = before + in;
+  };
+  chunk_scan(residual);
+
+  // ---- every chunk sum of the sequence, then the chunk search ----
+  if (wave == 0) {
+    double2 cm[kLocSums];
+    const bool ok = poll_chunk_sums_n(a, s, cm);
+    if (ok) {
+      const ChunkPick cp = chunk_search([&](int k) { return pick_sums(cm, k); }, (a.nch2 + 63) / 64,
+                                        (double)si1.z);
+      if (lane == 0) {
+        sh_kc = cp.kc;
+        sh_cex = cp.cex;
+        sh_tgt = cp.tgt;
+        sh_usep = cp.use_p;
+      }
+    }
+    if (lane == 0) {
+      sh_ok = ok;
+      sh_hit = 0;
+    }
+  }
+  __syncthreads();
+  if (!sh_ok) {
+    if (tid == 0) {
+      a.accept_len[s] = -1;
+      a.next_token[s] = -1;
+    }
+    return;
+  }
+  if (sh_kc != c) return;
+
+  // ---- the chosen chunk: the thread whose interval holds the target walks its run ----
+  const bool use_q = residual && !sh_usep;
+  if (use_q != residual) {  // workgroup-uniform
+    __syncthreads();        // every read of sh_w and sh_last above is done
+    chunk_scan(use_q);
+  }
+  const double cex = sh_cex, tgt = sh_tgt;
+  const double lo = cex + pre_lo, hi = cex + pre_hi;
+  if (own > 0.0 && lo <= tgt && tgt < hi) {  // at most one thread: walk its run
+    double cum = lo;
+    int found = -1;
+    auto step = [&](int e, float m) {
+      if (found < 0 && m > 0.f) {
+        if (cum + (double)m > tgt) found = e;
+        cum += (double)m;
+      }
+    };
+    if (tid == 0)
+      for (int e = ch.hb; e < ch.he; ++e) step(e, use_q ? sh_em[0][0][e - ch.hb] : sh_em[0][1][e - ch.hb]);
+#pragma unroll
+    for (int i = 0; i < VEC; ++i)
+      if (has) step(eb + i, mm[i]);
+    if (tid == kLocThreads - 1)
+      for (int e = ch.tb; e < ch.te; ++e) step(e, use_q ? sh_em[1][0][e - ch.tb] : sh_em[1][1][e - ch.tb]);
+    a.next_token[s] = found >= 0 ? found : elast;  // rounding: the run's last token with mass
+    a.accept_len[s] = j;
+    sh_hit = 1;
+  }
+  __syncthreads();
+  if (tid == 0 && !sh_hit) {  // rounding: the chunk's last token with mass (0 if none)
+    int t = -1;
+    for (int w2 = 0; w2 < NW; ++w2) t = max(t, sh_last[w2]);
+    a.next_token[s] = max(t, 0);
+    a.accept_len[s] = j;
+  }
 }
 
 }  // namespace sdb

@@ -193,6 +193,10 @@ struct AcceptPlan {
   // workgroups (one per sequence), and its workspace (tagged records)
   int fused_ok, n_tail;
   size_t total_fused;
+  // single-launch draw at T > 0 (accept_draw_kernel): possible for this shape, and its
+  // workspace (the two-launch layout, then the tagged chunk sums)
+  int draw_ok;
+  size_t off_draw, total_draw;
 };
 
 // Sequences of one single-launch call, at most (the launch also checks them against the
@@ -254,6 +258,11 @@ int accept_plan(const sd_accept_shape *sh, float temperature, AcceptPlan *p) {
   p->fused_ok = !sample && S >= 1 && nch <= sdb::kFusedMaxNch && S <= kFusedMaxTail && items + S <= INT_MAX;
   p->total_fused =
       p->fused_ok ? align256((size_t)S * sh->max_block * nch * 3 * sizeof(unsigned long long)) : 0;
+  // the single-launch draw (sampling): chunks of one vector per thread, whose sums a
+  // wavefront holds in registers
+  p->draw_ok = sample && S >= 1 && !tail_wide && nch2 <= 64LL * sdb::kLocSums && (long long)S * nch2 <= INT_MAX;
+  p->off_draw = p->total;
+  p->total_draw = p->draw_ok ? p->total + align256((size_t)S * 2 * nch2 * sizeof(unsigned long long)) : 0;
   return ok();
 }
 
@@ -511,7 +520,7 @@ int sd_accept_workspace_size(const sd_accept_shape *shape, float temperature, si
   AcceptPlan p;
   int rc = accept_plan(shape, temperature, &p);
   if (rc) return rc;
-  *bytes = std::max(p.total, p.total_fused);
+  *bytes = std::max(p.total, std::max(p.total_fused, p.total_draw));
   return ok();
 }
 
@@ -568,35 +577,39 @@ unsigned next_accept_tag() {
 
 constexpr int kMaxDevices = 64;  // devices whose per-device state the library keeps
 
-// Workgroups of accept_fused_kernel the current device holds at once (the least over its
-// instantiations), or 0 if the runtime cannot tell; per device, computed on first use.
-int fused_capacity() {
-  static std::atomic<int> cap[kMaxDevices];
+// Workgroups of a single-launch acceptance kernel the current device holds at once (the least
+// over the instantiations of accept_fused_kernel, kind 0, or accept_draw_kernel, kind 1), or 0
+// if the runtime cannot tell; per device, computed on first use.
+int resident_capacity(int kind) {
+  static std::atomic<int> cap[2][kMaxDevices];
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
     (void)hipGetLastError();
     return 0;
   }
-  int c = cap[dev].load(std::memory_order_relaxed);
+  int c = cap[kind][dev].load(std::memory_order_relaxed);
   if (c > 0) return c;
   int cus = 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) {
     (void)hipGetLastError();
     return 0;
   }
-  const void *kernels[] = {(const void *)sdb::accept_fused_kernel<true, true>, (const void *)sdb::accept_fused_kernel<true, false>,
-                           (const void *)sdb::accept_fused_kernel<false, true>, (const void *)sdb::accept_fused_kernel<false, false>};
+  const void *fused[] = {(const void *)sdb::accept_fused_kernel<true, true>, (const void *)sdb::accept_fused_kernel<true, false>,
+                         (const void *)sdb::accept_fused_kernel<false, true>, (const void *)sdb::accept_fused_kernel<false, false>};
+  const void *draw[] = {(const void *)sdb::accept_draw_kernel<true>, (const void *)sdb::accept_draw_kernel<false>};
+  const void *const *ks = kind == 0 ? fused : draw;
+  const int nk = kind == 0 ? 4 : 2;
   int per_cu = INT_MAX;
-  for (const void *k : kernels) {
+  for (int i = 0; i < nk; ++i) {
     int nb = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k, 256, 0) != hipSuccess) {
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, ks[i], 256, 0) != hipSuccess) {
       (void)hipGetLastError();
       return 0;
     }
     per_cu = std::min(per_cu, nb);
   }
   c = per_cu * cus;
-  cap[dev].store(c, std::memory_order_relaxed);
+  cap[kind][dev].store(c, std::memory_order_relaxed);
   return c;
 }
 
@@ -653,7 +666,7 @@ int accept_enqueue(const sd_accept_shape *sh, const AcceptPlan &p, const void *t
   // tail workgroups, which wait only for statistics workgroups (which never wait), must fit on
   // the device at once with a quarter of it to spare.
   if (p.fused_ok && workspace_bytes >= p.total_fused && g_accept_path.load(std::memory_order_relaxed) == 0 &&
-      4LL * p.n_tail <= 3LL * fused_capacity() && stream_allows_fused(st)) {
+      4LL * p.n_tail <= 3LL * resident_capacity(0) && stream_allows_fused(st)) {
     a.trec = (unsigned long long *)ws;
     a.tag = next_accept_tag();
     a.n_items = p.stats_grid;
@@ -679,7 +692,23 @@ int accept_enqueue(const sd_accept_shape *sh, const AcceptPlan &p, const void *t
     hipLaunchKernelGGL((sdb::accept_mass_kernel<BF, NV>), dim3(S * p.nch2), dim3(256), 0, st, a);             \
     hipLaunchKernelGGL((sdb::accept_locate_kernel<BF, NV>), dim3(S), dim3(sdb::kLocThreads), 0, st, a);       \
   } while (0)
-  if (sample) {
+  // Sampling draw in one launch (mass and locate together) when the shape, the workspace, the
+  // stream and the test switch allow it and the whole grid fits on the device at once with a
+  // quarter to spare (every workgroup of accept_draw_kernel waits for its sequence's others).
+  if (sample && p.draw_ok && workspace_bytes >= p.total_draw && g_accept_path.load(std::memory_order_relaxed) == 0 &&
+      4LL * S * p.nch2 <= 3LL * resident_capacity(1) && stream_allows_fused(st)) {
+    a.csum = (unsigned long long *)(ws + p.off_draw);
+    a.tag = next_accept_tag();
+    const int spin = g_accept_spin.load(std::memory_order_relaxed);
+    a.spin_limit = spin > 0 ? spin : kDefaultSpinLimit;
+    if (bf) {
+      SDB_STATS(true, true);
+      hipLaunchKernelGGL((sdb::accept_draw_kernel<true>), dim3(S * p.nch2), dim3(256), 0, st, a);
+    } else {
+      SDB_STATS(false, true);
+      hipLaunchKernelGGL((sdb::accept_draw_kernel<false>), dim3(S * p.nch2), dim3(256), 0, st, a);
+    }
+  } else if (sample) {
     if (bf) {
       SDB_STATS(true, true);
       if (p.tail_wide) SDB_TAIL(true, sdb::kTailVecsWide);

@@ -193,6 +193,30 @@ _PATH_CASES = [
 ]
 
 
+# At T > 0, where the shape allows it, the mass and locate steps run as one launch whose
+# workgroups hand the per-chunk mass sums on through tagged words; the three-launch path stays
+# for wide chunks, grids larger than the device holds at once, graph capture and small
+# workspaces.  The same sums run in the same order, so results agree exactly.
+_DRAW_CASES = [
+    ("ragged", lambda: W.c3_ragged(temperatures=(1.0,), with_attn=False).accept[1.0]),
+    ("qwen3_4b", lambda: W.c2_qwen3_4b_verify(temperatures=(1.0,)).accept[1.0]),
+    # 32 sequences x 75 chunks: more workgroups than the single launch takes (three launches)
+    ("long_context", lambda: W.c5_long_context(temperatures=(1.0,), with_attn=False).accept[1.0]),
+    ("V4096_f32", lambda: _many_seq_problem(15, 40, 4096, (1, 20), "f32", 1.0, name="V4096_f32_T1")),
+    # fp32 rows of 37984 vectors: 149 chunks, three passes of the chunk search
+    ("V151936_f32", lambda: _many_seq_problem(16, 5, 151936, (2, 12), "f32", 1.0, target_sigma=3.0,
+                                              noise_sigma=1.0, name="V151936_f32_T1")),
+    # draft rows not vector-aligned with their target rows (V % 8 != 0)
+    ("V50001", lambda: _many_seq_problem(17, 9, 50001, (1, 16), "bf16", 1.0, target_sigma=3.0,
+                                         noise_sigma=1.0, name="V50001_T1")),
+    ("V7", lambda: _many_seq_problem(18, 40, 7, (1, 20), "bf16", 1.0, name="V7_T1")),
+    ("V1003", lambda: _many_seq_problem(19, 40, 1003, (1, 20), "bf16", 1.0, name="V1003_T1")),
+    ("B1_B2", lambda: _many_seq_problem(20, 16, 151936, (1, 2), "bf16", 1.0, target_sigma=3.0,
+                                       noise_sigma=1.0, name="B1_B2_T1")),
+    ("max_block_64", lambda: _many_seq_problem(21, 5, 32768, (60, 64), "bf16", 1.0, name="B64_T1")),
+]
+
+
 def _both_paths(p, d):
     import paper_2606_31315_amd as sd
     try:
@@ -216,13 +240,25 @@ def test_single_launch_matches_two_launches(name, make):
     G.compare_accept(p, al1, nt1, G.oracle_accept(p))
 
 
-def test_single_launch_ignores_leftover_words():
-    """A workspace holding an earlier call's words, random bytes, one repeated 64-bit word, or
-    zeros: every call still equals the two-launch result."""
-    import paper_2606_31315_amd as sd
-    p = W.c3_ragged(temperatures=(0.0,), with_attn=False).accept[0.0]
+@pytest.mark.parametrize("name,make", _DRAW_CASES, ids=[c[0] for c in _DRAW_CASES])
+def test_single_launch_draw_matches_three_launches(name, make):
+    """Both sampling paths give the same accept_len and next_token, bit for bit, and the single
+    launch's result meets the parity rule against the oracle."""
+    p = make()
     d = G.accept_to_device(p)
-    n = sd.accept_workspace_size(sd.accept_shape(d["t"], p.S, p.max_block), 0.0)
+    (al1, nt1), (alm, ntm) = _both_paths(p, d)
+    assert (al1 == alm).all() and (nt1 == ntm).all(), (name, np.nonzero(al1 != alm), np.nonzero(nt1 != ntm))
+    G.compare_accept(p, al1, nt1, G.oracle_accept(p))
+
+
+@pytest.mark.parametrize("T", [0.0, 1.0])
+def test_single_launch_ignores_leftover_words(T):
+    """A workspace holding an earlier call's words, random bytes, one repeated 64-bit word, or
+    zeros: every call still equals the multi-launch result."""
+    import paper_2606_31315_amd as sd
+    p = W.c3_ragged(temperatures=(T,), with_attn=False).accept[T]
+    d = G.accept_to_device(p)
+    n = sd.accept_workspace_size(sd.accept_shape(d["t"], p.S, p.max_block), T)
     _, (alm, ntm) = _both_paths(p, d)
     ws = torch.empty(n, dtype=torch.uint8, device=G.dev())
     fills = [lambda: None,  # whatever the previous call left
@@ -236,13 +272,15 @@ def test_single_launch_ignores_leftover_words():
             assert (al == alm).all() and (nt == ntm).all()
 
 
-def test_single_launch_gives_up_when_told_and_recovers():
-    """With the waits cut to one poll, each sequence either has its exact result or reports -1
-    in both outputs; the next call with the default limit, on the same workspace, is exact."""
+@pytest.mark.parametrize("T", [0.0, 1.0])
+def test_single_launch_gives_up_when_told_and_recovers(T):
+    """With the waits cut to one poll, every output is either exact or -1 (greedy: both outputs
+    of a sequence together); the next call with the default limit, on the same workspace, is
+    exact."""
     import paper_2606_31315_amd as sd
-    p = W.c3_ragged(temperatures=(0.0,), with_attn=False).accept[0.0]
+    p = W.c3_ragged(temperatures=(T,), with_attn=False).accept[T]
     d = G.accept_to_device(p)
-    n = sd.accept_workspace_size(sd.accept_shape(d["t"], p.S, p.max_block), 0.0)
+    n = sd.accept_workspace_size(sd.accept_shape(d["t"], p.S, p.max_block), T)
     ws = torch.empty(n, dtype=torch.uint8, device=G.dev())
     _, (alm, ntm) = _both_paths(p, d)
     try:
@@ -250,31 +288,35 @@ def test_single_launch_gives_up_when_told_and_recovers():
         al, nt = G.run_accept(p, d, workspace=ws)
     finally:
         sd.accept_set_path(0)
-    exact = (al == alm) & (nt == ntm)
-    gave_up = (al == -1) & (nt == -1)
-    assert (exact | gave_up).all(), (al, alm, nt, ntm)
+    if T == 0:
+        exact = (al == alm) & (nt == ntm)
+        gave_up = (al == -1) & (nt == -1)
+        assert (exact | gave_up).all(), (al, alm, nt, ntm)
+    else:
+        assert ((al == alm) | (al == -1)).all() and ((nt == ntm) | (nt == -1)).all(), (al, alm, nt, ntm)
     al, nt = G.run_accept(p, d, workspace=ws)
     assert (al == alm).all() and (nt == ntm).all()
 
 
-def test_small_workspace_takes_two_launch_path():
-    """A workspace big enough for the two-launch path only still gives the same results."""
+@pytest.mark.parametrize("T", [0.0, 1.0])
+def test_small_workspace_takes_multi_launch_path(T):
+    """A workspace big enough for the multi-launch path only still gives the same results."""
     import ctypes
     import paper_2606_31315_amd as sd
     from paper_2606_31315_amd import _lib
-    p = W.c3_ragged(temperatures=(0.0,), with_attn=False).accept[0.0]
+    p = W.c3_ragged(temperatures=(T,), with_attn=False).accept[T]
     d = G.accept_to_device(p)
     shape = sd.accept_shape(d["t"], p.S, p.max_block)
-    full = sd.accept_workspace_size(shape, 0.0)
+    full = sd.accept_workspace_size(shape, T)
     al = torch.empty(p.S, dtype=torch.int32, device=G.dev())
     nt = torch.empty(p.S, dtype=torch.int32, device=G.dev())
     ws = torch.empty(full, dtype=torch.uint8, device=G.dev())
     L = _lib.lib()
 
     def call(nbytes):
-        return L.sd_accept(ctypes.byref(shape), _lib._ptr(d["t"]), None, _lib._ptr(d["tok"]), None,
-                           _lib._ptr(d["bl"]), _lib._ptr(d["off"]), ctypes.c_float(0.0), _lib._ptr(al),
-                           _lib._ptr(nt), _lib._ptr(ws), nbytes, _lib._stream(None))
+        return L.sd_accept(ctypes.byref(shape), _lib._ptr(d["t"]), _lib._ptr(d["d"]), _lib._ptr(d["tok"]),
+                           _lib._ptr(d["u"]), _lib._ptr(d["bl"]), _lib._ptr(d["off"]), ctypes.c_float(T),
+                           _lib._ptr(al), _lib._ptr(nt), _lib._ptr(ws), nbytes, _lib._stream(None))
     # the smallest workspace the call accepts, by bisection on SD_ERR_WORKSPACE
     lo, hi = 0, full
     while hi - lo > 256:
