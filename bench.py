@@ -638,12 +638,16 @@ def main():
     # timed region: exactly K whole steps, nothing else on the stream
     K = args.steps
     ms_per_step = timed(step, K)
-    # spread: the same steps again in 5 batches; per-call durations: K calls of each operation
+    # Legs after the timed region (never part of value) run at least 200 calls: each batch
+    # starts from an idle stream, so a short batch would mostly measure the host's enqueue
+    # latency of its first call (about 13 us), not the kernels.
+    KI = max(K, 200)
+    # spread: the same steps again in 5 batches; per-call durations: KI calls of each operation
     # back to back in 5 batches (an event between every call would add a few microseconds of
     # its own to each); each reported as the median batch mean with the batch range
-    step_b = batched_us(torch, step, K)
-    attn_b = batched_us(torch, attn_call, K)
-    acc_b = batched_us(torch, accept_call, K)
+    step_b = batched_us(torch, step, KI)
+    attn_b = batched_us(torch, attn_call, KI)
+    acc_b = batched_us(torch, accept_call, KI)
     attn_us, acc_us = float(np.median(attn_b)), float(np.median(acc_b))
 
     ntok = work.verified_draft_tokens()
@@ -717,7 +721,7 @@ def main():
 
     for i in range(args.warmup):
         step0(i)
-    ms0 = timed(step0, K)
+    ms0 = timed(step0, KI)
     acc0_bytes = acc0.logit_bytes()
     al0_h = al0.cpu().numpy()
     gbps0 = (attn_bytes + acc0_bytes) / (ms0 * 1e-3) / 1e9
@@ -726,8 +730,8 @@ def main():
                  "step_gbps": round(gbps0, 1), "step_hbm_frac": round(gbps0 / HBM_PEAK_GBPS, 4),
                  "frac_of_read_ceiling": round(gbps0 / rc_gbps, 4),
                  "what": "the same step with greedy acceptance (T = 0): every target row read once"}
-    res["paged_attn_us"] = {f"page_{ps}_shuffled": paged_run(torch, sd, a, bufs, ps, K) for ps in (16, 64, 256)}
-    res["paged_attn_us"]["page_64_in_order"] = paged_run(torch, sd, a, bufs, 64, K, shuffle=False)
+    res["paged_attn_us"] = {f"page_{ps}_shuffled": paged_run(torch, sd, a, bufs, ps, KI) for ps in (16, 64, 256)}
+    res["paged_attn_us"]["page_64_in_order"] = paged_run(torch, sd, a, bufs, 64, KI, shuffle=False)
     if args.policy_prompts > 0:
         res["policy"] = policy_run(torch, sd, args.policy_prompts)
     if args.other_configs:

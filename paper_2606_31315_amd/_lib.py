@@ -129,11 +129,21 @@ def _check(rc: int) -> None:
 
 
 def _ptr(t: Optional[torch.Tensor]):
-    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+    """A tensor's device address for a c_void_p argument (every entry point declares its
+    argument types, so ctypes converts the integer; None is NULL)."""
+    return t.data_ptr() if t is not None else None
+
+
+# The current stream's handle without building a torch.cuda.Stream object (about 3 us of host
+# time per call otherwise); the public accessor where this torch has no raw one.
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+_cur_device = getattr(torch._C, "_cuda_getDevice", None)
 
 
 def _stream(stream) -> ctypes.c_void_p:
     if stream is None:
+        if _raw_stream is not None and _cur_device is not None:
+            return ctypes.c_void_p(_raw_stream(_cur_device()))
         stream = torch.cuda.current_stream()
     return ctypes.c_void_p(stream.cuda_stream)
 
@@ -152,9 +162,16 @@ def _shape(t: Optional[torch.Tensor], name: str, *dims) -> None:
     kernels read or write outside it."""
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch.Tensor")
-    if t.dim() != len(dims) or any(d is not None and t.shape[i] != d for i, d in enumerate(dims)):
+    shp = t.shape
+    ok = len(shp) == len(dims)
+    if ok:
+        for n, d in zip(shp, dims):
+            if d is not None and n != d:
+                ok = False
+                break
+    if not ok:
         want = "[" + ", ".join("*" if d is None else str(d) for d in dims) + "]"
-        raise ValueError(f"{name} has shape {list(t.shape)}, expected {want}")
+        raise ValueError(f"{name} has shape {list(shp)}, expected {want}")
 
 
 def _lens_shapes(S: int, **named) -> None:
@@ -203,6 +220,22 @@ def attn_shape(q: torch.Tensor, k_cache: torch.Tensor, max_ctx: int, max_block: 
                        float(scale))
 
 
+# Shape structs of the per-step calls, by their field values: the library only reads them, so
+# one struct serves every call of that shape (building one costs about a microsecond of host
+# time).  Bounded: cleared when it grows past _SHAPE_CACHE_MAX entries.
+_SHAPE_CACHE_MAX = 256
+_shape_cache: dict = {}
+
+
+def _cached_shape(key, make):
+    sh = _shape_cache.get(key)
+    if sh is None:
+        if len(_shape_cache) >= _SHAPE_CACHE_MAX:
+            _shape_cache.clear()
+        sh = _shape_cache[key] = make()
+    return sh
+
+
 def attn_workspace_size(shape: SdAttnShape) -> int:
     n = ctypes.c_size_t(0)
     _check(lib().sd_block_attn_workspace_size(ctypes.byref(shape), ctypes.byref(n)))
@@ -232,10 +265,10 @@ def block_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, ct
     if out is None:
         out = torch.empty_like(q)
     _need(out, "out", q.dtype, dev)
-    shape = attn_shape(q, k_cache, max_ctx, max_block, scale)
-    nbytes = attn_workspace_size(shape)
-    if workspace is None:
-        workspace = _default_ws.get(nbytes, dev)
+    shape = _cached_shape(("attn", S, q.shape[1], Hkv, D, Lmax, q.shape[0], int(max_ctx), int(max_block), q.dtype,
+                           float(scale)), lambda: attn_shape(q, k_cache, max_ctx, max_block, scale))
+    if workspace is None:  # a caller's workspace is checked against the need by the library
+        workspace = _default_ws.get(attn_workspace_size(shape), dev)
     _check(lib().sd_block_attn(ctypes.byref(shape), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(ctx_lens),
                                _ptr(block_lens), _ptr(q_offsets), int(mask_mode), _ptr(out), _ptr(workspace),
                                workspace.numel() * workspace.element_size(), _stream(stream)))
@@ -392,10 +425,10 @@ def accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor], dr
         accept_len = torch.empty(S, dtype=torch.int32, device=dev)
     if next_token is None:
         next_token = torch.empty(S, dtype=torch.int32, device=dev)
-    shape = accept_shape(target_logits, S, max_block)
-    nbytes = accept_workspace_size(shape, temperature)
-    if workspace is None:
-        workspace = _default_ws.get(nbytes, dev)
+    shape = _cached_shape(("accept", S, target_logits.shape[1], target_logits.shape[0], int(max_block),
+                           target_logits.dtype), lambda: accept_shape(target_logits, S, max_block))
+    if workspace is None:  # a caller's workspace is checked against the need by the library
+        workspace = _default_ws.get(accept_workspace_size(shape, temperature), dev)
     _check(lib().sd_accept(ctypes.byref(shape), _ptr(target_logits),
                            _ptr(draft_logits if temperature > 0 else None), _ptr(draft_tokens),
                            _ptr(uniforms if temperature > 0 else None), _ptr(block_lens), _ptr(q_offsets),
