@@ -56,6 +56,9 @@ struct AttnArgs {
   // fused append only: the block's new keys and values [total_q, Hkv, D]
   const void *k_new;
   const void *v_new;
+  // balanced plan (bf16, plain caches; bal_share): bal_grid workgroups, shares of at least
+  // bal_min_tiles key tiles of bal_kt keys
+  int bal, bal_grid, bal_min_tiles, bal_kt;
 };
 
 // ---- work items ----------------------------------------------------------------
@@ -216,8 +219,154 @@ __device__ __forceinline__ bool attn_item(const AttnArgs &a, int b, AttnItem &it
   return true;
 }
 
+// ---- balanced plan ---------------------------------------------------------------
+// Pair (s, g) holds n = ceil((ctx_s + B_s) / kt) key tiles (none when B_s = 0), each weighing
+// w = bal_weight(m-tiles of its block) units; the pairs line up in (sequence, kv head) order,
+// W units in all.  Workgroup w takes the tiles whose first unit lies in [w * per, (w + 1) * per),
+// per = max(ceil(W / bal_grid), bal_min_tiles * the lightest weight), so every workgroup gets
+// about the same work whatever the lengths are; its share is cut where it crosses from one pair
+// to the next, one work item per piece.  The piece of workgroup w in pair q = s * Hkv + g files
+// its partial at slot w + q, so a pair's pieces hold consecutive slots from (first workgroup) + q.
+// (Even splits per pair leave ragged batches with fractional waves: 16 sequences, contexts
+// 1k-8k, about 350 splits of up to 2064 keys on 256 CUs.)
+#ifndef SDB_BAL_WEIGHTS
+#define SDB_BAL_WEIGHTS 1
+#endif
+// Relative time of one key tile by the block's m-tiles (16-row query tiles): the split kernel
+// streams a tile in about 1.25 us up to 3 m-tiles; beyond that the wavefronts' LDS reads and
+// arithmetic set the pace (8 sequences x 8 kv heads, contexts 4096, one wave, MI355X: 1.24 us
+// per tile at 1-3 m-tiles, 1.43 at 4, 1.57 at 5, 1.74 at 6, 2.0 at 7, 2.05 at 8).
+__device__ __forceinline__ int bal_weight(int nmt) {
+  if (!SDB_BAL_WEIGHTS) return 1;
+  constexpr int kw[9] = {20, 20, 20, 20, 23, 25, 28, 32, 33};
+  return nmt <= 8 ? kw[nmt] : 33 + 4 * (nmt - 8);
+}
+
+struct BalShare {
+  int per, u0, u1;  // units per share; this workgroup's unit range [u0, u1)
+};
+
+// Lanes hold sequence values; per-pair tiles and weight of that sequence (0 past a.S / empty).
+__device__ __forceinline__ int bal_seq_tiles(bool live, int ctx, int B, int kt) {
+  return (live && B > 0) ? (ctx + B + kt - 1) / kt : 0;
+}
+__device__ __forceinline__ int bal_seq_weight(const AttnArgs &a, int B) {
+  return bal_weight((a.G * max(B, 0) + 15) / 16);
+}
+
+__device__ __forceinline__ int bal_per(const AttnArgs &a, int W) {
+  return max((W + a.bal_grid - 1) / a.bal_grid, a.bal_min_tiles * bal_weight(1));
+}
+
+// First tile of a pair (start unit p0, weight w) whose first unit is at or after unit u.
+__device__ __forceinline__ int bal_tile_at(int u, int p0, int w) {
+  return u <= p0 ? 0 : (u - p0 + w - 1) / w;
+}
+
+// This workgroup's share: the total W, one round of loads per 64 sequences.
+__device__ __forceinline__ BalShare bal_share(const AttnArgs &a, int w, int kt) {
+  const int lane = threadIdx.x & 63;
+  int W = 0;
+  for (int c0 = 0; c0 < a.S; c0 += 64) {
+    const int k = min(c0 + lane, a.S - 1);  // clamped: no per-load branch
+    const int B = a.block_lens[k];
+    const int u = bal_seq_tiles(c0 + lane < a.S, a.ctx_lens[k], B, kt) * bal_seq_weight(a, B) * a.Hkv;
+    W += __builtin_amdgcn_readlane(wave_scan_i(u), 63);
+  }
+  BalShare sh;
+  sh.per = bal_per(a, W);
+  sh.u0 = min(w * sh.per, W);
+  sh.u1 = min(sh.u0 + sh.per, W);
+  return sh;
+}
+
+// The next piece of the share: u0 is a cursor, the first unit not yet handed out.  The first
+// tile whose first unit is at or after u0 starts the piece, if that unit lies before u1; the
+// piece runs to the last tile of the same pair whose first unit lies before u1, and the cursor
+// moves to the first unit of the tile after it.  Every piece moves the cursor forward, so the
+// loop over pieces ends.  False when the share is done.
+__device__ __forceinline__ bool bal_item(const AttnArgs &a, BalShare &sh, int kt, AttnItem &it) {
+  const int lane = threadIdx.x & 63;
+  // Two rounds at most: when u0 lies inside a pair's last tile past its first unit, the next
+  // tile is the first of the next pair with tiles, whose first unit is that pair's start.
+  for (int round = 0; round < 2; ++round) {
+    if (sh.u0 >= sh.u1) return false;
+    int before = 0;
+    bool next_pair = false;
+    for (int c0 = 0; c0 < a.S; c0 += 64) {
+      const int k = min(c0 + lane, a.S - 1);  // clamped: no per-load branch
+      const int ctx = a.ctx_lens[k], B = a.block_lens[k], off = a.q_offsets[k];
+      const int t = bal_seq_tiles(c0 + lane < a.S, ctx, B, kt);
+      const int wt = bal_seq_weight(a, B);
+      const int sequ = t * wt * a.Hkv;
+      const int incl = before + wave_scan_i(sequ);
+      const unsigned long long hit = __ballot(incl > sh.u0 && incl - sequ <= sh.u0);  // holds unit u0
+      if (hit) {
+        const int l = __ffsll((long long)hit) - 1;  // wave-uniform
+        const int ts = __builtin_amdgcn_readlane(t, l), w = __builtin_amdgcn_readlane(wt, l);
+        const int pu = ts * w;  // units of each of the sequence's pairs
+        const int pre = __builtin_amdgcn_readlane(incl - sequ, l);
+        const int g = (sh.u0 - pre) / pu;
+        const int p0 = pre + g * pu;  // first unit of pair (s, g)
+        const int j0 = bal_tile_at(sh.u0, p0, w);
+        if (j0 >= ts) {  // past the first unit of the pair's last tile: the next pair
+          sh.u0 = p0 + pu;
+          next_pair = true;
+          break;
+        }
+        if (p0 + j0 * w >= sh.u1) {  // the next tile belongs to the next share
+          sh.u0 = sh.u1;
+          return false;
+        }
+        const int j1 = min(bal_tile_at(sh.u1, p0, w), ts);  // > j0
+        it.s = c0 + l;
+        it.g = g;
+        it.ctx = __builtin_amdgcn_readlane(ctx, l);
+        it.B = __builtin_amdgcn_readlane(B, l);
+        it.qoff = __builtin_amdgcn_readlane(off, l);
+        it.k0 = j0 * kt;
+        it.k1 = min(j1 * kt, it.ctx + it.B);
+        const int wf = p0 / sh.per, wl = (p0 + (ts - 1) * w) / sh.per;
+        const int wme = (p0 + j0 * w) / sh.per;  // this workgroup
+        it.nsplit = wl - wf + 1;
+        it.split = wme - wf;
+        it.slot = wme + it.s * a.Hkv + g;
+        sh.u0 = p0 + j1 * w;
+        return true;
+      }
+      before = __builtin_amdgcn_readlane(incl, 63);
+    }
+    if (!next_pair) return false;  // no sequence holds u0: past the last tile
+  }
+  return false;
+}
+
 // Partial slot of split 0 of pair (s, g) and the pair's split count (0: no block).
 __device__ __forceinline__ int2 attn_pair_slots(const AttnArgs &a, int s, int g, int &B) {
+  if (a.bal) {
+    const int lane = threadIdx.x & 63;
+    int W = 0, pre = 0, ts = 0, Bs = 0;
+    for (int c0 = 0; c0 < a.S; c0 += 64) {
+      const int k = min(c0 + lane, a.S - 1);  // clamped: no per-load branch
+      const int Bk = a.block_lens[k];
+      const int t = bal_seq_tiles(c0 + lane < a.S, a.ctx_lens[k], Bk, a.bal_kt);
+      const int sequ = t * bal_seq_weight(a, Bk) * a.Hkv;
+      const int incl = wave_scan_i(sequ);
+      if (s >= c0 && s < c0 + 64) {  // wave-uniform
+        const int l = s - c0;
+        pre = W + __builtin_amdgcn_readlane(incl - sequ, l);
+        ts = __builtin_amdgcn_readlane(t, l);
+        Bs = __builtin_amdgcn_readlane(Bk, l);
+      }
+      W += __builtin_amdgcn_readlane(incl, 63);
+    }
+    B = Bs;
+    if (Bs <= 0) return int2{0, 0};
+    const int per = bal_per(a, W), w = bal_seq_weight(a, Bs);
+    const int p0 = pre + g * ts * w;
+    const int wf = p0 / per, wl = (p0 + (ts - 1) * w) / per;
+    return int2{wf + s * a.Hkv + g, wl - wf + 1};
+  }
   if (!a.dense) {
     // both lengths in one round of scalar loads: one use of both before the branch on B, so the
     // context length's load is not sunk behind it

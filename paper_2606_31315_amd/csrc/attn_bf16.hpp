@@ -211,7 +211,10 @@ __device__ __forceinline__ void pv_step(const f32x4 (&p)[NSB], unsigned stage, c
 
 // APPEND: the block's keys and values are read from a.k_new / a.v_new rather than the cache,
 // and the split that covers them also writes them into the cache (sd_block_attn_append).
-template <int D, int MT, int KT_, int NS_, bool PAGED, bool APPEND = false>
+// BAL (the balanced plan): the workgroup streams its share of every pair's key tiles, one work
+// item per pair its share touches (bal_item), the body below once per item; otherwise the body
+// runs once, for the workgroup's one work item (attn_item).
+template <int D, int MT, int KT_, int NS_, bool PAGED, bool APPEND = false, bool BAL = false>
 __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   using T = Bf16Tile<D, KT_, NS_>;
   constexpr int KT = T::KT, NS = T::NS, NDT = D / 16, NST = D / 32, NSB = KT / 16;
@@ -221,309 +224,321 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) char ring_raw[NS * T::STAGEB];
   char SDB_LDS *ring = (char SDB_LDS *)(SDB_LDS void *)ring_raw;
 
-  AttnItem it;
-  if (!attn_item(a, blockIdx.x, it)) return;
-  const int s = it.s, g = it.g, k0 = it.k0, k1 = it.k1, nsplit = it.nsplit;
-  const int ctx = it.ctx, B = it.B, qoff = it.qoff;
-  const int M = a.G * B;
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int l16 = lane & 15;
-  const int kgrp = lane >> 4;
-  const int nmt = (M + 15) >> 4;
-  // Wavefront w runs on SIMD w % 4.  With 5 or 6 m-tiles, m-tiles 4 and 5 would put two whole
-  // m-tiles of work on one SIMD while others idle, so wavefronts 4-7 instead take the two key
-  // halves of m-tiles 4 and 5 (each keeps its own online-softmax state over its 32 keys of
-  // every tile; the halves are merged once, after the last tile): at most 1.5 m-tiles of work
-  // per SIMD instead of 2.
-  const bool hsplit = MT == 1 && (nmt == 5 || nmt == 6);
-  const int hlf = (hsplit && wave >= 4) ? ((wave - 4) & 1) : -1;  // key half, or -1: whole tiles
-  auto mtile = [&](int j) { return (hlf >= 0) ? 4 + ((wave - 4) >> 1) : wave + T::NW * j; };
-
-  const char *kbase = reinterpret_cast<const char *>(a.k);
-  const char *vbase = reinterpret_cast<const char *>(a.v);
-  if constexpr (!PAGED) {
-    kbase += ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
-    vbase += ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
-  }
-
-  // ---- query operands: element e of step st is dim st*32 + kgrp*8 + e of row m ----
-  bf16x8 qop[MT][NST];
-  f32x4 oacc[MT][NDT];
-  float m_run[MT], l_run[MT];
-  int row_i[MT];
-  bool act[MT];
-#pragma unroll
-  for (int j = 0; j < MT; ++j) {
-    const int mt = mtile(j);
-    const int m = mt * 16 + l16;
-    act[j] = mt < nmt;
-    m_run[j] = -INFINITY;
-    l_run[j] = 0.f;
-#pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) oacc[j][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const bool valid = act[j] && m < M;
-    row_i[j] = valid ? m / a.G : 0;
-    const char *qrow = reinterpret_cast<const char *>(a.q) +
-                       ((size_t)(qoff + (valid ? m / a.G : 0)) * a.Hq + g * a.G + (valid ? m % a.G : 0)) * D * EB;
-#pragma unroll
-    for (int st = 0; st < NST; ++st) {
-      const u32x4 raw = valid ? *reinterpret_cast<const u32x4 *>(qrow + (st * 32 + kgrp * 8) * EB) : u32x4{0, 0, 0, 0};
-      qop[j][st] = __builtin_bit_cast(bf16x8, raw);
-    }
-  }
-
-  // ---- per-lane LDS offsets, fixed for the whole loop ----
-  // K operand of sub-tile sb, step st: row sb*16 + l16, chunk (st*4 + kgrp) swizzled by the
-  // row (the swizzle only depends on l16); sb*16 rows are an immediate offset.
-  unsigned koff[NST];
-#pragma unroll
-  for (int st = 0; st < NST; ++st) koff[st] = l16 * T::ROWB + (((st * 4 + kgrp) ^ T::swz_k(l16)) << 4);
-  // V^T operand for head-dim tile dt: source row kgrp*4 + l16/4 (plus kk*32 + h*16 keys as
-  // an immediate), head dims dt*16 + 4*(l16%4) .. +3 (swizzle depends only on the row mod 8).
-  const int vrow = kgrp * 4 + (l16 >> 2);
-  unsigned voff[NDT];
-#pragma unroll
-  for (int dt = 0; dt < NDT; ++dt)
-    voff[dt] = T::TILEB + vrow * T::ROWB + (((2 * dt + ((l16 & 3) >> 1)) ^ T::swz_v(vrow)) << 4) + ((l16 & 1) << 3);
-
-  TileLoads<D, KT, NS> ld;
-  ld.init(wave, lane);
-  // paged caches: this sequence's row of the block table
-  [[maybe_unused]] const int *table = PAGED ? a.block_table + (size_t)s * a.max_pages : nullptr;
-  [[maybe_unused]] int pgn = 0;  // paged caches: page id of this wavefront's share of the next tile
-  // APPEND: the block rows of this kv head in the new-row arrays, and this split's share of
-  // them ([ab0, k1) of the keys) copied into the cache through registers: loaded now, stored
-  // after the last tile.  (Stores count in vmcnt: issued earlier, they would hold up the next
-  // tile wait until they were acknowledged.)
-  [[maybe_unused]] const size_t nstride = (size_t)a.Hkv * D * EB;
-  [[maybe_unused]] const char *knew = nullptr, *vnew = nullptr;
-  [[maybe_unused]] int ab0 = k1;
-  constexpr int NAV = D / 32;  // 64 rows x 2 x D*2/16 vectors over 512 threads
-  [[maybe_unused]] AppendVec cpv[NAV];
-  if constexpr (APPEND) {
-    knew = reinterpret_cast<const char *>(a.k_new) + ((size_t)qoff * a.Hkv + g) * D * EB;
-    vnew = reinterpret_cast<const char *>(a.v_new) + ((size_t)qoff * a.Hkv + g) * D * EB;
-    ab0 = max(k0, ctx);
-    if (ab0 < k1) {  // uniform: this split covers block rows ab0 - ctx .. k1 - 1 - ctx
-      constexpr int RV = D * EB / 16;  // 16-byte vectors per row
-      const int half = (k1 - ab0) * RV;  // K vectors, then as many V vectors
-#pragma unroll
-      for (int c = 0; c < NAV; ++c) {
-        const int v = min(tid + 512 * c, 2 * half - 1);  // clamped: no per-load branch
-        const int kv = v >= half, w = v - kv * half, r = w / RV, ch = w % RV;
-        cpv[c] = *reinterpret_cast<const AppendVec *>((kv ? vnew : knew) + (size_t)(ab0 - ctx + r) * nstride + ch * 16);
-      }
-    }
-  }
-  auto issue = [&](char SDB_LDS *stage, int key0) {
-    if constexpr (PAGED) {
-      ld.issue_paged(stage, kbase, vbase, key0, k1 - 1, pgn, a.page_log2, a.Hkv, g, wave);
-    } else if constexpr (APPEND) {
-      if (key0 + KT > ctx) ld.issue_append(stage, kbase, vbase, knew, vnew, nstride, key0, k1 - 1, ctx, wave);
-      else ld.issue(stage, kbase, vbase, key0, k1 - 1, wave);
+  [[maybe_unused]] BalShare bsh;
+  if constexpr (BAL) bsh = bal_share(a, blockIdx.x, KT);
+  for (;;) {  // one pass per work item
+    AttnItem it;
+    if constexpr (BAL) {
+      if (!bal_item(a, bsh, KT, it)) return;
     } else {
-      ld.issue(stage, kbase, vbase, key0, k1 - 1, wave);
+      if (!attn_item(a, blockIdx.x, it)) return;
     }
-  };
+    const int s = it.s, g = it.g, k0 = it.k0, k1 = it.k1, nsplit = it.nsplit;
+    const int ctx = it.ctx, B = it.B, qoff = it.qoff;
+    const int M = a.G * B;
 
-  // ---- pipeline prologue: tiles 0 .. NS-2 in flight ----
-  const int ntiles = (k1 - k0 + KT - 1) / KT;
-  if constexpr (PAGED) {
-    // the page ids of the first NS tiles in one batch of scalar loads: one round trip rather
-    // than one per tile (measured: 38.2 -> 35.6 us per call with shuffled 16-key pages,
-    // together with one id per wavefront and tile)
-    int pro[NS];
-#pragma unroll
-    for (int t = 0; t < NS; ++t) pro[t] = ld.fetch_page_raw(table, a.max_pages, a.page_log2, k0 + t * KT, k1 - 1, wave);
-    // one use of all the raw ids before any is clamped, so their loads go out together
-    if constexpr (NS == 3) asm volatile("" : "+s"(pro[0]), "+s"(pro[1]), "+s"(pro[2]));
-#pragma unroll
-    for (int t = 0; t < NS; ++t) pro[t] = TileLoads<D, KT, NS>::clamp_page(pro[t], a.num_pages);
-#pragma unroll
-    for (int t = 0; t < NS - 1; ++t)
-      if (t < ntiles) ld.issue_paged(ring + t * T::STAGEB, kbase, vbase, k0 + t * KT, k1 - 1, pro[t], a.page_log2, a.Hkv, g, wave);
-    pgn = pro[NS - 1];
-  } else {
-#pragma unroll
-    for (int t = 0; t < NS - 1; ++t)
-      if (t < ntiles) issue(ring + t * T::STAGEB, k0 + t * KT);
-  }
-  // keys every row can see: all of [k0, k1) when bidirectional, keys <= ctx when causal
-  const int vis_all = a.causal ? min(k1, ctx + 1) : k1;
-  const float sl2 = a.scale_log2;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int l16 = lane & 15;
+    const int kgrp = lane >> 4;
+    const int nmt = (M + 15) >> 4;
+    // Wavefront w runs on SIMD w % 4.  With 5 or 6 m-tiles, m-tiles 4 and 5 would put two whole
+    // m-tiles of work on one SIMD while others idle, so wavefronts 4-7 instead take the two key
+    // halves of m-tiles 4 and 5 (each keeps its own online-softmax state over its 32 keys of
+    // every tile; the halves are merged once, after the last tile): at most 1.5 m-tiles of work
+    // per SIMD instead of 2.
+    const bool hsplit = MT == 1 && (nmt == 5 || nmt == 6);
+    const int hlf = (hsplit && wave >= 4) ? ((wave - 4) & 1) : -1;  // key half, or -1: whole tiles
+    auto mtile = [&](int j) { return (hlf >= 0) ? 4 + ((wave - 4) >> 1) : wave + T::NW * j; };
 
-  // One wavefront's work on one m-tile over NSBW 16-key sub-blocks of a tile, starting at key
-  // kb (LDS rows from stg): scores, mask, online softmax, P.V.
-  auto tile_work = [&](auto nsbw_c, int j, unsigned stg, int kb, bool full) {
-    constexpr int NSBW = decltype(nsbw_c)::value;
-    // S^T = K Q^T: sacc[sb][r] is key kb + sb*16 + kgrp*4 + r of row l16 (unscaled)
-    f32x4 sacc[NSBW];
-#pragma unroll
-    for (int sb = 0; sb < NSBW; ++sb) sacc[sb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int st = 0; st < NST; ++st) {
-      const char SDB_LDS *kp = (const char SDB_LDS *)(uintptr_t)(stg + koff[st]);
-#pragma unroll
-      for (int sb = 0; sb < NSBW; ++sb) {
-        const bf16x8 av = *(const bf16x8 SDB_LDS *)(kp + sb * 16 * T::ROWB);
-        sacc[sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qop[j][st], sacc[sb], 0, 0, 0);
-      }
+    const char *kbase = reinterpret_cast<const char *>(a.k);
+    const char *vbase = reinterpret_cast<const char *>(a.v);
+    if constexpr (!PAGED) {
+      kbase += ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
+      vbase += ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
     }
-    // online softmax in the log2 domain: max of the raw scores, then one FMA per score
-    if (!full) {
-      const int lim = a.causal ? min(k1, ctx + row_i[j] + 1) : k1;
-#pragma unroll
-      for (int sb = 0; sb < NSBW; ++sb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (kb + sb * 16 + kgrp * 4 + r >= lim) sacc[sb][r] = -INFINITY;
-    }
-    float tmax = -INFINITY;
-#pragma unroll
-    for (int sb = 0; sb < NSBW; ++sb)
-      tmax = fmaxf(tmax, fmaxf(fmaxf(sacc[sb][0], sacc[sb][1]), fmaxf(sacc[sb][2], sacc[sb][3])));
-    tmax = fmaxf(tmax, shfl_xor_f(tmax, 16));
-    tmax = fmaxf(tmax, shfl_xor_f(tmax, 32));
-    const float mnew = fmaxf(m_run[j], tmax * sl2);
-    const float muse = (mnew == -INFINITY) ? 0.f : mnew;
-    float psum = 0.f;
-#pragma unroll
-    for (int sb = 0; sb < NSBW; ++sb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        sacc[sb][r] = fast_exp2(fmaf(sacc[sb][r], sl2, -muse));
-        psum += sacc[sb][r];
-      }
-    if (__any(mnew != m_run[j])) {
-      const float alpha = fast_exp2(m_run[j] - muse);
-      l_run[j] *= alpha;
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) oacc[j][dt] *= alpha;
-    }
-    m_run[j] = mnew;
-    l_run[j] += psum;
 
-    // O^T += V^T P^T over these keys in 32-key steps
-    pv_step<0, NDT, NSBW>(sacc, stg, voff, oacc[j]);
-    if constexpr (NSBW > 2) pv_step<1, NDT, NSBW>(sacc, stg, voff, oacc[j]);
-    if constexpr (NSBW > 4) {
-      pv_step<2, NDT, NSBW>(sacc, stg, voff, oacc[j]);
-      pv_step<3, NDT, NSBW>(sacc, stg, voff, oacc[j]);
-    }
-  };
-
-  for (int t = 0; t < ntiles; ++t) {
-    const int kt = k0 + t * KT;
-    const int ahead = min(ntiles - 1 - t, NS - 2);  // tiles issued after tile t
-    if (NS > 4 && ahead >= 3) wait_vmcnt<3 * T::LPW>();
-    else if (NS > 3 && ahead >= 2) wait_vmcnt<2 * T::LPW>();
-    else if (NS > 2 && ahead >= 1) wait_vmcnt<T::LPW>();
-    else wait_vmcnt<0>();
-    __syncthreads();  // tile t landed for every wavefront; stage (t-1) % NS is free again
-    if (t + NS - 1 < ntiles) issue(ring + ((t + NS - 1) % NS) * T::STAGEB, kt + (NS - 1) * KT);
-    const unsigned stage = (unsigned)(uintptr_t)(ring + (t % NS) * T::STAGEB);
-    const bool full = kt + KT <= vis_all;  // uniform: no key of this tile is masked for any row
-#pragma unroll
+    // ---- query operands: element e of step st is dim st*32 + kgrp*8 + e of row m ----
+    bf16x8 qop[MT][NST];
+    f32x4 oacc[MT][NDT];
+    float m_run[MT], l_run[MT];
+    int row_i[MT];
+    bool act[MT];
+  #pragma unroll
     for (int j = 0; j < MT; ++j) {
-      if (!act[j]) continue;  // uniform per wavefront
-      if (hlf < 0) tile_work(std::integral_constant<int, NSB>{}, j, stage, kt, full);
-      else tile_work(std::integral_constant<int, NSB / 2>{}, j, stage + (unsigned)(hlf * (KT / 2) * T::ROWB),
-                     kt + hlf * (KT / 2), full);
+      const int mt = mtile(j);
+      const int m = mt * 16 + l16;
+      act[j] = mt < nmt;
+      m_run[j] = -INFINITY;
+      l_run[j] = 0.f;
+  #pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) oacc[j][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const bool valid = act[j] && m < M;
+      row_i[j] = valid ? m / a.G : 0;
+      const char *qrow = reinterpret_cast<const char *>(a.q) +
+                         ((size_t)(qoff + (valid ? m / a.G : 0)) * a.Hq + g * a.G + (valid ? m % a.G : 0)) * D * EB;
+  #pragma unroll
+      for (int st = 0; st < NST; ++st) {
+        const u32x4 raw = valid ? *reinterpret_cast<const u32x4 *>(qrow + (st * 32 + kgrp * 8) * EB) : u32x4{0, 0, 0, 0};
+        qop[j][st] = __builtin_bit_cast(bf16x8, raw);
+      }
     }
-    if constexpr (PAGED) {
-      if (t + NS < ntiles) pgn = ld.fetch_page(table, a.max_pages, a.num_pages, a.page_log2, k0 + (t + NS) * KT, k1 - 1, wave);
-    }
-  }
 
-  if constexpr (APPEND) {
-    if (ab0 < k1) {  // the block rows this split covers, into the cache
-      constexpr int RV = D * EB / 16;
-      const int half = (k1 - ab0) * RV;
-      char *kc = reinterpret_cast<char *>(const_cast<void *>(a.k)) + ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
-      char *vc = reinterpret_cast<char *>(const_cast<void *>(a.v)) + ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
-#pragma unroll
-      for (int c = 0; c < NAV; ++c) {
-        const int v = tid + 512 * c;
-        if (v < 2 * half) {
+    // ---- per-lane LDS offsets, fixed for the whole loop ----
+    // K operand of sub-tile sb, step st: row sb*16 + l16, chunk (st*4 + kgrp) swizzled by the
+    // row (the swizzle only depends on l16); sb*16 rows are an immediate offset.
+    unsigned koff[NST];
+  #pragma unroll
+    for (int st = 0; st < NST; ++st) koff[st] = l16 * T::ROWB + (((st * 4 + kgrp) ^ T::swz_k(l16)) << 4);
+    // V^T operand for head-dim tile dt: source row kgrp*4 + l16/4 (plus kk*32 + h*16 keys as
+    // an immediate), head dims dt*16 + 4*(l16%4) .. +3 (swizzle depends only on the row mod 8).
+    const int vrow = kgrp * 4 + (l16 >> 2);
+    unsigned voff[NDT];
+  #pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+      voff[dt] = T::TILEB + vrow * T::ROWB + (((2 * dt + ((l16 & 3) >> 1)) ^ T::swz_v(vrow)) << 4) + ((l16 & 1) << 3);
+
+    TileLoads<D, KT, NS> ld;
+    ld.init(wave, lane);
+    // paged caches: this sequence's row of the block table
+    [[maybe_unused]] const int *table = PAGED ? a.block_table + (size_t)s * a.max_pages : nullptr;
+    [[maybe_unused]] int pgn = 0;  // paged caches: page id of this wavefront's share of the next tile
+    // APPEND: the block rows of this kv head in the new-row arrays, and this split's share of
+    // them ([ab0, k1) of the keys) copied into the cache through registers: loaded now, stored
+    // after the last tile.  (Stores count in vmcnt: issued earlier, they would hold up the next
+    // tile wait until they were acknowledged.)
+    [[maybe_unused]] const size_t nstride = (size_t)a.Hkv * D * EB;
+    [[maybe_unused]] const char *knew = nullptr, *vnew = nullptr;
+    [[maybe_unused]] int ab0 = k1;
+    constexpr int NAV = D / 32;  // 64 rows x 2 x D*2/16 vectors over 512 threads
+    [[maybe_unused]] AppendVec cpv[NAV];
+    if constexpr (APPEND) {
+      knew = reinterpret_cast<const char *>(a.k_new) + ((size_t)qoff * a.Hkv + g) * D * EB;
+      vnew = reinterpret_cast<const char *>(a.v_new) + ((size_t)qoff * a.Hkv + g) * D * EB;
+      ab0 = max(k0, ctx);
+      if (ab0 < k1) {  // uniform: this split covers block rows ab0 - ctx .. k1 - 1 - ctx
+        constexpr int RV = D * EB / 16;  // 16-byte vectors per row
+        const int half = (k1 - ab0) * RV;  // K vectors, then as many V vectors
+  #pragma unroll
+        for (int c = 0; c < NAV; ++c) {
+          const int v = min(tid + 512 * c, 2 * half - 1);  // clamped: no per-load branch
           const int kv = v >= half, w = v - kv * half, r = w / RV, ch = w % RV;
-          *reinterpret_cast<AppendVec *>((kv ? vc : kc) + (size_t)(ab0 + r) * T::ROWB + ch * 16) = cpv[c];
+          cpv[c] = *reinterpret_cast<const AppendVec *>((kv ? vnew : knew) + (size_t)(ab0 - ctx + r) * nstride + ch * 16);
         }
       }
     }
-  }
+    auto issue = [&](char SDB_LDS *stage, int key0) {
+      if constexpr (PAGED) {
+        ld.issue_paged(stage, kbase, vbase, key0, k1 - 1, pgn, a.page_log2, a.Hkv, g, wave);
+      } else if constexpr (APPEND) {
+        if (key0 + KT > ctx) ld.issue_append(stage, kbase, vbase, knew, vnew, nstride, key0, k1 - 1, ctx, wave);
+        else ld.issue(stage, kbase, vbase, key0, k1 - 1, wave);
+      } else {
+        ld.issue(stage, kbase, vbase, key0, k1 - 1, wave);
+      }
+    };
 
-  // ---- key halves of m-tiles 4 and 5: the second half's state joins the first's ----
-  if (hsplit) {  // uniform
-    constexpr int XS = NDT * 4 + 2;  // floats per lane: O, then m and l
-    float SDB_LDS *xch = (float SDB_LDS *)(SDB_LDS void *)ring_raw;  // the ring is no longer read
-    __syncthreads();
-    if (hlf == 1 && act[0]) {
-      float SDB_LDS *dst = xch + ((wave - 4) >> 1) * 64 * XS + lane;
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) dst[(dt * 4 + r) * 64] = oacc[0][dt][r];
-      dst[(NDT * 4) * 64] = m_run[0];
-      dst[(NDT * 4 + 1) * 64] = l_run[0];
+    // ---- pipeline prologue: tiles 0 .. NS-2 in flight ----
+    const int ntiles = (k1 - k0 + KT - 1) / KT;
+    if constexpr (PAGED) {
+      // the page ids of the first NS tiles in one batch of scalar loads: one round trip rather
+      // than one per tile (measured: 38.2 -> 35.6 us per call with shuffled 16-key pages,
+      // together with one id per wavefront and tile)
+      int pro[NS];
+  #pragma unroll
+      for (int t = 0; t < NS; ++t) pro[t] = ld.fetch_page_raw(table, a.max_pages, a.page_log2, k0 + t * KT, k1 - 1, wave);
+      // one use of all the raw ids before any is clamped, so their loads go out together
+      if constexpr (NS == 3) asm volatile("" : "+s"(pro[0]), "+s"(pro[1]), "+s"(pro[2]));
+  #pragma unroll
+      for (int t = 0; t < NS; ++t) pro[t] = TileLoads<D, KT, NS>::clamp_page(pro[t], a.num_pages);
+  #pragma unroll
+      for (int t = 0; t < NS - 1; ++t)
+        if (t < ntiles) ld.issue_paged(ring + t * T::STAGEB, kbase, vbase, k0 + t * KT, k1 - 1, pro[t], a.page_log2, a.Hkv, g, wave);
+      pgn = pro[NS - 1];
+    } else {
+  #pragma unroll
+      for (int t = 0; t < NS - 1; ++t)
+        if (t < ntiles) issue(ring + t * T::STAGEB, k0 + t * KT);
     }
-    __syncthreads();
-    if (hlf == 0 && act[0]) {
-      const float SDB_LDS *src = xch + ((wave - 4) >> 1) * 64 * XS + lane;
-      const float mb = src[(NDT * 4) * 64], lb = src[(NDT * 4 + 1) * 64];
-      const float mn = fmaxf(m_run[0], mb);
-      const float mu = (mn == -INFINITY) ? 0.f : mn;
-      const float sa = (m_run[0] == -INFINITY) ? 0.f : fast_exp2(m_run[0] - mu);
-      const float sb = (mb == -INFINITY) ? 0.f : fast_exp2(mb - mu);
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) oacc[0][dt][r] = oacc[0][dt][r] * sa + src[(dt * 4 + r) * 64] * sb;
-      l_run[0] = l_run[0] * sa + lb * sb;
-      m_run[0] = mn;
-    }
-    if (hlf == 1) act[0] = false;  // merged into the first half's wavefront
-  }
+    // keys every row can see: all of [k0, k1) when bidirectional, keys <= ctx when causal
+    const int vis_all = a.causal ? min(k1, ctx + 1) : k1;
+    const float sl2 = a.scale_log2;
 
-  // ---- epilogue: row sums over the four key groups, then output or partials ----
-#pragma unroll
-  for (int j = 0; j < MT; ++j) {
-    l_run[j] += shfl_xor_f(l_run[j], 16);
-    l_run[j] += shfl_xor_f(l_run[j], 32);
-  }
-  if (nsplit == 1) {
-#pragma unroll
+    // One wavefront's work on one m-tile over NSBW 16-key sub-blocks of a tile, starting at key
+    // kb (LDS rows from stg): scores, mask, online softmax, P.V.
+    auto tile_work = [&](auto nsbw_c, int j, unsigned stg, int kb, bool full) {
+      constexpr int NSBW = decltype(nsbw_c)::value;
+      // S^T = K Q^T: sacc[sb][r] is key kb + sb*16 + kgrp*4 + r of row l16 (unscaled)
+      f32x4 sacc[NSBW];
+  #pragma unroll
+      for (int sb = 0; sb < NSBW; ++sb) sacc[sb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  #pragma unroll
+      for (int st = 0; st < NST; ++st) {
+        const char SDB_LDS *kp = (const char SDB_LDS *)(uintptr_t)(stg + koff[st]);
+  #pragma unroll
+        for (int sb = 0; sb < NSBW; ++sb) {
+          const bf16x8 av = *(const bf16x8 SDB_LDS *)(kp + sb * 16 * T::ROWB);
+          sacc[sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qop[j][st], sacc[sb], 0, 0, 0);
+        }
+      }
+      // online softmax in the log2 domain: max of the raw scores, then one FMA per score
+      if (!full) {
+        const int lim = a.causal ? min(k1, ctx + row_i[j] + 1) : k1;
+  #pragma unroll
+        for (int sb = 0; sb < NSBW; ++sb)
+  #pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (kb + sb * 16 + kgrp * 4 + r >= lim) sacc[sb][r] = -INFINITY;
+      }
+      float tmax = -INFINITY;
+  #pragma unroll
+      for (int sb = 0; sb < NSBW; ++sb)
+        tmax = fmaxf(tmax, fmaxf(fmaxf(sacc[sb][0], sacc[sb][1]), fmaxf(sacc[sb][2], sacc[sb][3])));
+      tmax = fmaxf(tmax, shfl_xor_f(tmax, 16));
+      tmax = fmaxf(tmax, shfl_xor_f(tmax, 32));
+      const float mnew = fmaxf(m_run[j], tmax * sl2);
+      const float muse = (mnew == -INFINITY) ? 0.f : mnew;
+      float psum = 0.f;
+  #pragma unroll
+      for (int sb = 0; sb < NSBW; ++sb)
+  #pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          sacc[sb][r] = fast_exp2(fmaf(sacc[sb][r], sl2, -muse));
+          psum += sacc[sb][r];
+        }
+      if (__any(mnew != m_run[j])) {
+        const float alpha = fast_exp2(m_run[j] - muse);
+        l_run[j] *= alpha;
+  #pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) oacc[j][dt] *= alpha;
+      }
+      m_run[j] = mnew;
+      l_run[j] += psum;
+
+      // O^T += V^T P^T over these keys in 32-key steps
+      pv_step<0, NDT, NSBW>(sacc, stg, voff, oacc[j]);
+      if constexpr (NSBW > 2) pv_step<1, NDT, NSBW>(sacc, stg, voff, oacc[j]);
+      if constexpr (NSBW > 4) {
+        pv_step<2, NDT, NSBW>(sacc, stg, voff, oacc[j]);
+        pv_step<3, NDT, NSBW>(sacc, stg, voff, oacc[j]);
+      }
+    };
+
+    for (int t = 0; t < ntiles; ++t) {
+      const int kt = k0 + t * KT;
+      const int ahead = min(ntiles - 1 - t, NS - 2);  // tiles issued after tile t
+      if (NS > 4 && ahead >= 3) wait_vmcnt<3 * T::LPW>();
+      else if (NS > 3 && ahead >= 2) wait_vmcnt<2 * T::LPW>();
+      else if (NS > 2 && ahead >= 1) wait_vmcnt<T::LPW>();
+      else wait_vmcnt<0>();
+      __syncthreads();  // tile t landed for every wavefront; stage (t-1) % NS is free again
+      if (t + NS - 1 < ntiles) issue(ring + ((t + NS - 1) % NS) * T::STAGEB, kt + (NS - 1) * KT);
+      const unsigned stage = (unsigned)(uintptr_t)(ring + (t % NS) * T::STAGEB);
+      const bool full = kt + KT <= vis_all;  // uniform: no key of this tile is masked for any row
+  #pragma unroll
+      for (int j = 0; j < MT; ++j) {
+        if (!act[j]) continue;  // uniform per wavefront
+        if (hlf < 0) tile_work(std::integral_constant<int, NSB>{}, j, stage, kt, full);
+        else tile_work(std::integral_constant<int, NSB / 2>{}, j, stage + (unsigned)(hlf * (KT / 2) * T::ROWB),
+                       kt + hlf * (KT / 2), full);
+      }
+      if constexpr (PAGED) {
+        if (t + NS < ntiles) pgn = ld.fetch_page(table, a.max_pages, a.num_pages, a.page_log2, k0 + (t + NS) * KT, k1 - 1, wave);
+      }
+    }
+
+    if constexpr (APPEND) {
+      if (ab0 < k1) {  // the block rows this split covers, into the cache
+        constexpr int RV = D * EB / 16;
+        const int half = (k1 - ab0) * RV;
+        char *kc = reinterpret_cast<char *>(const_cast<void *>(a.k)) + ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
+        char *vc = reinterpret_cast<char *>(const_cast<void *>(a.v)) + ((size_t)(s * a.Hkv + g) * a.Lmax) * D * EB;
+  #pragma unroll
+        for (int c = 0; c < NAV; ++c) {
+          const int v = tid + 512 * c;
+          if (v < 2 * half) {
+            const int kv = v >= half, w = v - kv * half, r = w / RV, ch = w % RV;
+            *reinterpret_cast<AppendVec *>((kv ? vc : kc) + (size_t)(ab0 + r) * T::ROWB + ch * 16) = cpv[c];
+          }
+        }
+      }
+    }
+
+    // ---- key halves of m-tiles 4 and 5: the second half's state joins the first's ----
+    if (hsplit) {  // uniform
+      constexpr int XS = NDT * 4 + 2;  // floats per lane: O, then m and l
+      float SDB_LDS *xch = (float SDB_LDS *)(SDB_LDS void *)ring_raw;  // the ring is no longer read
+      __syncthreads();
+      if (hlf == 1 && act[0]) {
+        float SDB_LDS *dst = xch + ((wave - 4) >> 1) * 64 * XS + lane;
+  #pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+  #pragma unroll
+          for (int r = 0; r < 4; ++r) dst[(dt * 4 + r) * 64] = oacc[0][dt][r];
+        dst[(NDT * 4) * 64] = m_run[0];
+        dst[(NDT * 4 + 1) * 64] = l_run[0];
+      }
+      __syncthreads();
+      if (hlf == 0 && act[0]) {
+        const float SDB_LDS *src = xch + ((wave - 4) >> 1) * 64 * XS + lane;
+        const float mb = src[(NDT * 4) * 64], lb = src[(NDT * 4 + 1) * 64];
+        const float mn = fmaxf(m_run[0], mb);
+        const float mu = (mn == -INFINITY) ? 0.f : mn;
+        const float sa = (m_run[0] == -INFINITY) ? 0.f : fast_exp2(m_run[0] - mu);
+        const float sb = (mb == -INFINITY) ? 0.f : fast_exp2(mb - mu);
+  #pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+  #pragma unroll
+          for (int r = 0; r < 4; ++r) oacc[0][dt][r] = oacc[0][dt][r] * sa + src[(dt * 4 + r) * 64] * sb;
+        l_run[0] = l_run[0] * sa + lb * sb;
+        m_run[0] = mn;
+      }
+      if (hlf == 1) act[0] = false;  // merged into the first half's wavefront
+    }
+
+    // ---- epilogue: row sums over the four key groups, then output or partials ----
+  #pragma unroll
+    for (int j = 0; j < MT; ++j) {
+      l_run[j] += shfl_xor_f(l_run[j], 16);
+      l_run[j] += shfl_xor_f(l_run[j], 32);
+    }
+    if (nsplit == 1) {
+  #pragma unroll
+      for (int j = 0; j < MT; ++j) {
+        const int m = mtile(j) * 16 + l16;
+        if (!act[j] || m >= M) continue;
+        const float inv = 1.f / l_run[j];
+        char *orow = reinterpret_cast<char *>(a.out) + ((size_t)(qoff + m / a.G) * a.Hq + g * a.G + m % a.G) * D * EB;
+  #pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+          const f32x4 o = oacc[j][dt] * inv;
+          *reinterpret_cast<uint2 *>(orow + (dt * 16 + kgrp * 4) * EB) = uint2{cvt_pk_bf16(o[0], o[1]), cvt_pk_bf16(o[2], o[3])};
+        }
+      }
+      if constexpr (!BAL) return;
+      __syncthreads();  // every wavefront is done with the ring before the next item's loads
+      continue;
+    }
+    const size_t wrow = (size_t)it.slot * a.Mpad;
+  #pragma unroll
     for (int j = 0; j < MT; ++j) {
       const int m = mtile(j) * 16 + l16;
       if (!act[j] || m >= M) continue;
-      const float inv = 1.f / l_run[j];
-      char *orow = reinterpret_cast<char *>(a.out) + ((size_t)(qoff + m / a.G) * a.Hq + g * a.G + m % a.G) * D * EB;
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) {
-        const f32x4 o = oacc[j][dt] * inv;
-        *reinterpret_cast<uint2 *>(orow + (dt * 16 + kgrp * 4) * EB) = uint2{cvt_pk_bf16(o[0], o[1]), cvt_pk_bf16(o[2], o[3])};
+      float *prow = a.part_o + (wrow + m) * D;
+      // non-temporal: the partials are read once, by the merge kernel, so they go to memory now
+      // instead of waiting dirty in L2 for the write-back at the kernel's end (ragged Qwen3-4B
+      // batch, 7 interleaved rounds: 35.0 -> 34.0 us per call)
+  #pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+        __builtin_nontemporal_store(oacc[j][dt], reinterpret_cast<f32x4 *>(prow + dt * 16 + kgrp * 4));
+      if (kgrp == 0) {
+        typedef float f2v __attribute__((ext_vector_type(2)));
+        __builtin_nontemporal_store(f2v{m_run[j], l_run[j]}, reinterpret_cast<f2v *>(a.part_ml + wrow + m));
       }
     }
-    return;
-  }
-  const size_t wrow = (size_t)it.slot * a.Mpad;
-#pragma unroll
-  for (int j = 0; j < MT; ++j) {
-    const int m = mtile(j) * 16 + l16;
-    if (!act[j] || m >= M) continue;
-    float *prow = a.part_o + (wrow + m) * D;
-    // non-temporal: the partials are read once, by the merge kernel, so they go to memory now
-    // instead of waiting dirty in L2 for the write-back at the kernel's end (ragged Qwen3-4B
-    // batch, 7 interleaved rounds: 35.0 -> 34.0 us per call)
-#pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
-      __builtin_nontemporal_store(oacc[j][dt], reinterpret_cast<f32x4 *>(prow + dt * 16 + kgrp * 4));
-    if (kgrp == 0) {
-      typedef float f2v __attribute__((ext_vector_type(2)));
-      __builtin_nontemporal_store(f2v{m_run[j], l_run[j]}, reinterpret_cast<f2v *>(a.part_ml + wrow + m));
-    }
+    if constexpr (!BAL) return;
+    __syncthreads();  // every wavefront is done with the ring before the next item's loads
   }
 }
 

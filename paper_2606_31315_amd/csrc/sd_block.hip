@@ -67,8 +67,14 @@ constexpr int kBf16KT = SDB_BF16_KT, kBf16NS = SDB_BF16_NS;
 // ---------------------------------------------------------------------------
 struct AttnPlan {
   int G, KT, split_len, max_splits, Mpad, n_work, per_xcd, grid, dense, MT;
+  int bal;  // balanced shares for sd_block_attn (bf16, plain caches; see bal_share)
   size_t off_ml, off_o, total;
 };
+
+// Balanced plan: one workgroup per CU of the MI355X (the bf16 split kernel holds a CU), each
+// share at least 16 key tiles (1024 keys), like the shortest split of the other multi-wave plans.
+constexpr int kBalGrid = 256;
+constexpr int kBalMinTiles = 16;
 
 int attn_plan(const sd_attn_shape *sh, AttnPlan *p) {
   if (!sh) return fail(SD_ERR_INVALID_ARG, "sd_block_attn: shape is NULL");
@@ -140,14 +146,25 @@ int attn_plan(const sd_attn_shape *sh, AttnPlan *p) {
   p->dense = nw > target_wgs;
   p->per_xcd = (int)((nw + sdb::kNumXcd - 1) / sdb::kNumXcd);
   p->grid = p->dense ? (int)nw : p->per_xcd * sdb::kNumXcd;
+  // Where even splits would need more than one wave (bf16), every workgroup gets an equal share
+  // of all the pairs' (weighted) key tiles instead (bal_share), in the plain, paged and
+  // fused-append calls alike.  Partial slots: one per workgroup and pair a share touches, at
+  // most kBalGrid + pairs.
+  p->bal = sh->dtype == SD_BF16 && p->dense && p->max_splits > 1;
+  {  // the device sums tile weights (at most 33 + 4 per m-tile past 8) in 32-bit integers
+    const long long nmt_max = (G * (long long)sh->max_block + 15) / 16;
+    const long long wmax = 33 + 4 * std::max(0LL, nmt_max - 8);
+    if (pairs * ((max_L + kBf16KT - 1) / kBf16KT) * wmax > (1LL << 30)) p->bal = 0;
+  }
+  const long long slots = p->bal ? std::max(nw, (long long)kBalGrid + pairs) : nw;
   const int nmt = p->Mpad / 16;
   if (sh->dtype == SD_BF16) p->MT = nmt <= 8 ? 1 : 2;  // 8 wavefronts, 1 or 2 m-tiles each
   else p->MT = nmt <= 4 ? 1 : nmt <= 8 ? 2 : 4;      // 4 wavefronts
   size_t off = 0;
   p->off_ml = off;
-  if (p->max_splits > 1) off = align256(off + (size_t)nw * p->Mpad * sizeof(float2));
+  if (p->max_splits > 1) off = align256(off + (size_t)slots * p->Mpad * sizeof(float2));
   p->off_o = off;
-  if (p->max_splits > 1) off = align256(off + (size_t)nw * p->Mpad * D * sizeof(float));
+  if (p->max_splits > 1) off = align256(off + (size_t)slots * p->Mpad * D * sizeof(float));
   p->total = off > 0 ? off : 256;
   return ok();
 }
@@ -155,6 +172,21 @@ int attn_plan(const sd_attn_shape *sh, AttnPlan *p) {
 template <bool BF16, int D, int MT>
 void launch_attn(const sdb::AttnArgs &a, int grid, hipStream_t st) {
   hipLaunchKernelGGL((sdb::block_attn_kernel<BF16, D, MT>), dim3(grid), dim3(256), 0, st, a);
+}
+
+// The balanced plan (bf16): kBalGrid workgroups, then the merge.
+template <int D, bool PAGED = false, bool APPEND = false>
+void launch_attn_bal(sdb::AttnArgs a, int MT, hipStream_t st) {
+  a.bal = 1;
+  if (MT == 1)
+    hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 1, kBf16KT, kBf16NS, PAGED, APPEND, true>), dim3(a.bal_grid),
+                       dim3(512), 0, st, a);
+  else
+    hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 2, kBf16KT, kBf16NS, PAGED, APPEND, true>), dim3(a.bal_grid),
+                       dim3(512), 0, st, a);
+  constexpr int RB = 256 / (D / 4);
+  const int nrb = (a.Mpad + RB - 1) / RB;
+  hipLaunchKernelGGL((sdb::block_attn_merge_kernel<true, D, 8>), dim3(a.S * a.Hkv * nrb), dim3(256), 0, st, a);
 }
 
 template <bool BF16, int D, bool PAGED = false, bool APPEND = false>
@@ -378,6 +410,10 @@ int attn_args(const sd_attn_shape *sh, const AttnPlan &p, const void *q, const v
   a->block_table = nullptr;
   a->page_log2 = a->max_pages = a->num_pages = 0;
   a->k_new = a->v_new = nullptr;
+  a->bal = 0;  // sd_block_attn turns it on where its plan says so
+  a->bal_grid = kBalGrid;
+  a->bal_min_tiles = kBalMinTiles;
+  a->bal_kt = kBf16KT;
   return ok();
 }
 
@@ -401,6 +437,11 @@ int sd_block_attn(const sd_attn_shape *sh, const void *q, const void *k_cache, c
   const int grid = p.grid;
   hipStream_t st = (hipStream_t)stream;
   const bool bf = sh->dtype == SD_BF16;
+  if (p.bal) {
+    if (sh->head_dim == 128) launch_attn_bal<128>(a, p.MT, st);
+    else launch_attn_bal<64>(a, p.MT, st);
+    return check_launch("sd_block_attn");
+  }
   if (sh->head_dim == 128) {
     if (bf) launch_attn_all<true, 128>(a, grid, p.MT, st);
     else launch_attn_all<false, 128>(a, grid, p.MT, st);
@@ -432,8 +473,14 @@ int sd_block_attn_append(const sd_attn_shape *sh, const void *q, const void *k_n
   a.k_new = k_new;
   a.v_new = v_new;
   hipStream_t st = (hipStream_t)stream;
-  if (sh->head_dim == 128) launch_attn_all<true, 128, false, true>(a, p.grid, p.MT, st);
-  else launch_attn_all<true, 64, false, true>(a, p.grid, p.MT, st);
+  if (p.bal) {
+    if (sh->head_dim == 128) launch_attn_bal<128, false, true>(a, p.MT, st);
+    else launch_attn_bal<64, false, true>(a, p.MT, st);
+  } else if (sh->head_dim == 128) {
+    launch_attn_all<true, 128, false, true>(a, p.grid, p.MT, st);
+  } else {
+    launch_attn_all<true, 64, false, true>(a, p.grid, p.MT, st);
+  }
   return check_launch("sd_block_attn_append");
 }
 
@@ -477,8 +524,14 @@ int sd_block_attn_paged(const sd_attn_shape *sh, int32_t page_size, int32_t num_
   a.num_pages = num_pages;
   const int grid = p.grid;
   hipStream_t st = (hipStream_t)stream;
-  if (sh->head_dim == 128) launch_attn_all<true, 128, true>(a, grid, p.MT, st);
-  else launch_attn_all<true, 64, true>(a, grid, p.MT, st);
+  if (p.bal) {
+    if (sh->head_dim == 128) launch_attn_bal<128, true>(a, p.MT, st);
+    else launch_attn_bal<64, true>(a, p.MT, st);
+  } else if (sh->head_dim == 128) {
+    launch_attn_all<true, 128, true>(a, grid, p.MT, st);
+  } else {
+    launch_attn_all<true, 64, true>(a, grid, p.MT, st);
+  }
   return check_launch("sd_block_attn_paged");
 }
 

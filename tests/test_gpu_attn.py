@@ -213,3 +213,66 @@ def test_dense_plan_long_splits(S, ctx_hi, mode):
     """Plans at the split cap: up to 64 sequences the partial splits are ranked by length on
     the device, beyond that they follow sequence order; every output row compared."""
     G.check_attn(_long_split_sequences(7400 + S, S, ctx_hi, mode, f"long_splits_S{S}"))
+
+
+# ---- balanced shares: bf16 plans of more than one wave give every workgroup the same weighted
+# number of key tiles, cut where a share crosses from one (sequence, kv head) pair to the next ----
+
+def _attn_with_bounds(p, max_ctx, max_block):
+    """sd_block_attn with host bounds at or above the actual lengths (they set the plan); every
+    output row against the oracle."""
+    import paper_2606_31315_amd as sd
+    d = G.attn_to_device(p)
+    G.log(f"sd_block_attn {p.name} S={p.S} Hq={p.Hq} Hkv={p.Hkv} D={p.D} host bounds ctx<={max_ctx} B<={max_block}")
+    o = sd.block_attn(d["q"], d["k"], d["v"], d["ctx"], d["bl"], d["off"], p.mask_mode, max_ctx=max_ctx,
+                      max_block=max_block)
+    torch.cuda.synchronize()
+    got = o.float().cpu().numpy().astype(np.float64)
+    ref = G.oracle.block_attn(p.q, p.k_cache, p.v_cache, p.ctx_lens, p.block_lens, p.q_offsets, p.mask_mode, p.scale)
+    err = np.abs(got - ref).max()
+    G.log(f"  max-abs error {err:.3e}")
+    assert np.isfinite(got).all() and err <= G.ATTN_TOL["bf16"], err
+
+
+@pytest.mark.parametrize("mode", [CAUSAL, BIDIR])
+def test_balanced_short_lengths_under_long_bound(mode):
+    """Host bound 4096 keys, actual contexts 0-300 (some blocks empty): the shares shrink to
+    their 16-tile minimum, so most workgroups of the grid have nothing to do; D = 64. Cache rows
+    past each sequence's length hold NaN, so a tile read past a piece's end would show."""
+    rs = W._streams(7501)
+    S = 40
+    ctx = rs["ctx"].integers(0, 300, endpoint=True, size=S).astype(np.int32)
+    B = rs["B"].integers(0, 12, endpoint=True, size=S).astype(np.int32)
+    B[[0, 17]] = 0
+    B[5] = 12
+    p = W.make_attn(rs, S=S, Hq=8, Hkv=4, D=64, ctx_lens=ctx, block_lens=B, dtype="bf16", mask_mode=mode,
+                    Lmax=4096 + 12, name="bal_short_under_long_bound")
+    _attn_with_bounds(p, 4096, 12)
+
+
+@pytest.mark.parametrize("mode", [CAUSAL, BIDIR])
+def test_balanced_one_long_pair_over_many_shares(mode):
+    """One 30000-key sequence among short ones (50-600 keys): its pair is cut into some thirty
+    pieces on consecutive workgroups, merged in several batches; short pairs share workgroups."""
+    rs = W._streams(7502)
+    S = 20
+    ctx = rs["ctx"].integers(50, 600, endpoint=True, size=S).astype(np.int32)
+    B = rs["B"].integers(1, 16, endpoint=True, size=S).astype(np.int32)
+    ctx[6], B[6] = 30000, 16
+    p = W.make_attn(rs, S=S, Hq=4, Hkv=1, D=64, ctx_lens=ctx, block_lens=B, dtype="bf16", mask_mode=mode,
+                    name="bal_one_long_pair")
+    _attn_with_bounds(p, p.max_ctx, p.max_block)
+
+
+@pytest.mark.parametrize("mode", [CAUSAL, BIDIR])
+def test_balanced_two_mtiles_per_wavefront(mode):
+    """Eight query heads per kv head and blocks up to 24 rows (up to 12 m-tiles: two per
+    wavefront) under the balanced plan, 48 sequences with contexts 2500-5000."""
+    rs = W._streams(7503)
+    S = 48
+    ctx = rs["ctx"].integers(2500, 5000, endpoint=True, size=S).astype(np.int32)
+    B = rs["B"].integers(1, 24, endpoint=True, size=S).astype(np.int32)
+    B[3] = 24
+    p = W.make_attn(rs, S=S, Hq=16, Hkv=2, D=64, ctx_lens=ctx, block_lens=B, dtype="bf16", mask_mode=mode,
+                    name="bal_two_mtiles")
+    _attn_with_bounds(p, p.max_ctx, p.max_block)
