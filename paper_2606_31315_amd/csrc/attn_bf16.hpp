@@ -209,6 +209,19 @@ __device__ __forceinline__ void pv_step(const f32x4 (&p)[NSB], unsigned stage, c
   }
 }
 
+// The value of lane l combined with lane l ^ 16 (x16) or l ^ 32 (x32), by the gfx950 lane-swap
+// instructions: v_permlane16_swap / v_permlane32_swap with both operands x return, in every lane,
+// its own value and its partner's (one in each result), in VALU cycles instead of the LDS round
+// trip of a ds_bpermute shuffle.
+__device__ __forceinline__ float2 pair_x16(float x) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return float2{__uint_as_float(p[0]), __uint_as_float(p[1])};
+}
+__device__ __forceinline__ float2 pair_x32(float x) {
+  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return float2{__uint_as_float(p[0]), __uint_as_float(p[1])};
+}
+
 // APPEND: the block's keys and values are read from a.k_new / a.v_new rather than the cache,
 // and the split that covers them also writes them into the cache (sd_block_attn_append).
 // BAL (the balanced plan): the workgroup streams its share of every pair's key tiles, one work
@@ -395,8 +408,11 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   #pragma unroll
       for (int sb = 0; sb < NSBW; ++sb)
         tmax = fmaxf(tmax, fmaxf(fmaxf(sacc[sb][0], sacc[sb][1]), fmaxf(sacc[sb][2], sacc[sb][3])));
-      tmax = fmaxf(tmax, shfl_xor_f(tmax, 16));
-      tmax = fmaxf(tmax, shfl_xor_f(tmax, 32));
+      {  // the row's maximum over the four key groups (lanes l, l ^ 16, l ^ 32, l ^ 48)
+        const float2 p16 = pair_x16(tmax);
+        const float2 p32 = pair_x32(fmaxf(p16.x, p16.y));
+        tmax = fmaxf(p32.x, p32.y);
+      }
       const float mnew = fmaxf(m_run[j], tmax * sl2);
       const float muse = (mnew == -INFINITY) ? 0.f : mnew;
       float psum = 0.f;
@@ -490,8 +506,8 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   #pragma unroll
         for (int dt = 0; dt < NDT; ++dt)
   #pragma unroll
-          for (int r = 0; r < 4; ++r) oacc[0][dt][r] = oacc[0][dt][r] * sa + src[(dt * 4 + r) * 64] * sb;
-        l_run[0] = l_run[0] * sa + lb * sb;
+          for (int r = 0; r < 4; ++r) oacc[0][dt][r] = fmaf(oacc[0][dt][r], sa, src[(dt * 4 + r) * 64] * sb);
+        l_run[0] = fmaf(l_run[0], sa, lb * sb);  // explicit: rounding independent of contraction choices
         m_run[0] = mn;
       }
       if (hlf == 1) act[0] = false;  // merged into the first half's wavefront
@@ -500,8 +516,9 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
     // ---- epilogue: row sums over the four key groups, then output or partials ----
   #pragma unroll
     for (int j = 0; j < MT; ++j) {
-      l_run[j] += shfl_xor_f(l_run[j], 16);
-      l_run[j] += shfl_xor_f(l_run[j], 32);
+      const float2 p16 = pair_x16(l_run[j]);
+      const float2 p32 = pair_x32(p16.x + p16.y);
+      l_run[j] = p32.x + p32.y;
     }
     if (nsplit == 1) {
   #pragma unroll
