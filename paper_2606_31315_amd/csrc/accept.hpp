@@ -418,12 +418,11 @@ __device__ __forceinline__ void stats_process(const AcceptArgs &a, StatsItem<kSt
     sum = wave_sum_f(sum);
     xd = wave_max_f(xd);
   } else {
-#pragma unroll
-    for (int msk = 1; msk < 64; msk <<= 1) {
-      const float ov = __shfl_xor(bv, msk, 64);
-      const int oi = __shfl_xor(bi, msk, 64);
-      argmax_merge(bv, bi, ov, oi);
-    }
+    // the wavefront's largest value (NaN never wins), then the lowest index holding it: the
+    // argmax_merge order, by DPP lane moves instead of a butterfly of LDS shuffles
+    const float wmax = wave_max_f(bv);
+    bi = wave_min_i(bv == wmax ? bi : INT_MAX);
+    bv = wmax;
   }
 
   if (lane == 0) { sh_v[wave] = bv; sh_s[wave] = sum; sh_i[wave] = bi; if (SAMPLE) sh_v[4 + wave] = xd; }
@@ -495,7 +494,7 @@ __global__ __launch_bounds__(64) void accept_greedy_kernel(AcceptArgs a) {
   const bool rejects = (lane < n) && (tok != gi);
   const unsigned long long rej = __ballot(rejects);
   const int acc = rej ? (__ffsll((long long)rej) - 1) : max(n, 0);
-  const int next = __shfl(gi, acc, 64);
+  const int next = __builtin_amdgcn_readlane(gi, acc);  // wave-uniform lane
   if (lane == 0) {
     a.accept_len[s] = acc;
     a.next_token[s] = next;
@@ -569,11 +568,11 @@ __device__ __forceinline__ SampleSel sample_select(const AcceptArgs &a, int B, f
   SampleSel r;
   r.acc = rej ? (__ffsll((long long)rej) - 1) : max(n, 0);
   r.residual = r.acc < n;
-  r.tm = __shfl(tm, r.acc, 64);
-  r.ts = __shfl(ts, r.acc, 64);
-  r.qm = __shfl(qm, r.acc, 64);
-  r.qs = __shfl(qs, r.acc, 64);
-  r.ustar = __shfl(u, B - 1, 64);
+  r.tm = lane_f(tm, r.acc);  // wave-uniform lanes: scalar reads
+  r.ts = lane_f(ts, r.acc);
+  r.qm = lane_f(qm, r.acc);
+  r.qs = lane_f(qs, r.acc);
+  r.ustar = lane_f(u, B - 1);
   return r;
 }
 
@@ -1055,7 +1054,7 @@ __device__ void fused_greedy_tail(const AcceptArgs &a, int s) {
   const int n = B - 1;
   bool ok = true;
   if (lane == 0) ok = wait_word(a, last_record(a, s, Bc));
-  ok = __shfl(ok ? 1 : 0, 0, 64) != 0;
+  ok = __builtin_amdgcn_readlane(ok ? 1 : 0, 0) != 0;
   uint32_t pay[3 * kFusedMaxNch];
   if (ok) ok = poll_records_n(a, s, lane < Bc, pay);
   if (!ok) {
@@ -1078,7 +1077,7 @@ __device__ void fused_greedy_tail(const AcceptArgs &a, int s) {
   const bool rejects = (lane < n) && (tok != gi);
   const unsigned long long rej = __ballot(rejects);
   const int acc = rej ? (__ffsll((long long)rej) - 1) : max(n, 0);
-  const int next = __shfl(gi, acc, 64);
+  const int next = __builtin_amdgcn_readlane(gi, acc);  // wave-uniform lane
   if (lane == 0) {
     a.accept_len[s] = acc;
     a.next_token[s] = next;

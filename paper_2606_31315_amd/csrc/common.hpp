@@ -146,6 +146,21 @@ __device__ __forceinline__ float wave_max_f(float x) {
   return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
 }
 
+// Smallest value over the 64 lanes, in every lane.
+__device__ __forceinline__ int wave_min_i(int x) {
+  x = min(x, __builtin_amdgcn_update_dpp(INT_MAX, x, 0x128, 0xf, 0xf, false));
+  x = min(x, __builtin_amdgcn_update_dpp(INT_MAX, x, 0x124, 0xf, 0xf, false));
+  x = min(x, __builtin_amdgcn_update_dpp(INT_MAX, x, 0x122, 0xf, 0xf, false));
+  x = min(x, __builtin_amdgcn_update_dpp(INT_MAX, x, 0x121, 0xf, 0xf, false));
+  return min(min(__builtin_amdgcn_readlane(x, 0), __builtin_amdgcn_readlane(x, 16)),
+             min(__builtin_amdgcn_readlane(x, 32), __builtin_amdgcn_readlane(x, 48)));
+}
+
+// Value of lane l (wavefront-uniform l) in every lane: a scalar read, no LDS round trip.
+__device__ __forceinline__ float lane_f(float x, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
+}
+
 // Largest value over the 64 lanes, in every lane.
 __device__ __forceinline__ int wave_max_i(int x) {
   x = max(x, __builtin_amdgcn_update_dpp(INT_MIN, x, 0x128, 0xf, 0xf, false));
