@@ -209,6 +209,33 @@ __device__ __forceinline__ void pv_step(const f32x4 (&p)[NSB], unsigned stage, c
   }
 }
 
+// pv_step in two parts, so that the V^T operands can be read while the softmax runs: pv_issue
+// starts the transposed LDS reads of the 32-key step KK; pv_mma waits for them (and every earlier
+// LDS read) and multiplies.
+template <int KK, int NDT>
+__device__ __forceinline__ void pv_issue(unsigned stage, const unsigned (&voff)[NDT], s16x4 (&vv)[NDT][2]) {
+  constexpr int ROWB = NDT * 32;  // bytes per key row (D * 2)
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) {
+    vv[dt][0] = ds_read_tr16<(KK * 32 + 0) * ROWB>(stage + voff[dt]);
+    vv[dt][1] = ds_read_tr16<(KK * 32 + 16) * ROWB>(stage + voff[dt]);
+  }
+}
+template <int KK, int NDT, int NSB>
+__device__ __forceinline__ void pv_mma(const f32x4 (&p)[NSB], s16x4 (&vv)[NDT][2], f32x4 (&oacc)[NDT]) {
+  const u32x4 praw{cvt_pk_bf16(p[2 * KK][0], p[2 * KK][1]), cvt_pk_bf16(p[2 * KK][2], p[2 * KK][3]),
+                   cvt_pk_bf16(p[2 * KK + 1][0], p[2 * KK + 1][1]), cvt_pk_bf16(p[2 * KK + 1][2], p[2 * KK + 1][3])};
+  const bf16x8 pb = __builtin_bit_cast(bf16x8, praw);
+  wait_lds_tr<NDT>(vv);
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) {
+    typedef short s16x8 __attribute__((ext_vector_type(8)));
+    const s16x8 v8 = {vv[dt][0][0], vv[dt][0][1], vv[dt][0][2], vv[dt][0][3],
+                      vv[dt][1][0], vv[dt][1][1], vv[dt][1][2], vv[dt][1][3]};
+    oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, v8), pb, oacc[dt], 0, 0, 0);
+  }
+}
+
 // The value of lane l combined with lane l ^ 16 (x16) or l ^ 32 (x32), by the gfx950 lane-swap
 // instructions: v_permlane16_swap / v_permlane32_swap with both operands x return, in every lane,
 // its own value and its partner's (one in each result), in VALU cycles instead of the LDS round
@@ -227,12 +254,16 @@ __device__ __forceinline__ float2 pair_x32(float x) {
 // BAL (the balanced plan): the workgroup streams its share of every pair's key tiles, one work
 // item per pair its share touches (bal_item), the body below once per item; otherwise the body
 // runs once, for the workgroup's one work item (attn_item).
-template <int D, int MT, int KT_, int NS_, bool PAGED, bool APPEND = false, bool BAL = false>
+// VE (one m-tile per wavefront, blocks of 7-8 m-tiles): each tile's V^T operands are read from
+// LDS right after the QK^T products, so their latency runs under the softmax (8 sequences x 8
+// kv heads, contexts 4096, 8 m-tiles: 42.1 -> 41.2 us per call; at 3-6 m-tiles no faster).
+template <int D, int MT, int KT_, int NS_, bool PAGED, bool APPEND = false, bool BAL = false, bool VE = false>
 __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
   using T = Bf16Tile<D, KT_, NS_>;
   constexpr int KT = T::KT, NS = T::NS, NDT = D / 16, NST = D / 32, NSB = KT / 16;
   static_assert(NS >= 2 && NS <= 5, "ring depth");
   static_assert(KT == 64 || KT == 128, "key tile of 64 or 128 keys");
+  static_assert(!VE || MT == 1, "early V^T reads: registers for one m-tile per wavefront only");
   constexpr int EB = 2;
   __shared__ __attribute__((aligned(1024))) char ring_raw[NS * T::STAGEB];
   char SDB_LDS *ring = (char SDB_LDS *)(SDB_LDS void *)ring_raw;
@@ -395,6 +426,14 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
           sacc[sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qop[j][st], sacc[sb], 0, 0, 0);
         }
       }
+      // VE: the V^T operands of this tile's 32-key steps, read now (after the K reads the products
+      // above consumed), so that their LDS latency runs under the softmax below
+      constexpr bool vearly = VE && NSBW <= 4;
+      [[maybe_unused]] s16x4 vq[vearly ? NSBW / 2 : 1][NDT][2];
+      if constexpr (vearly) {
+        pv_issue<0, NDT>(stg, voff, vq[0]);
+        if constexpr (NSBW > 2) pv_issue<1, NDT>(stg, voff, vq[NSBW > 2 ? 1 : 0]);
+      }
       // online softmax in the log2 domain: max of the raw scores, then one FMA per score
       if (!full) {
         const int lim = a.causal ? min(k1, ctx + row_i[j] + 1) : k1;
@@ -433,11 +472,16 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
       l_run[j] += psum;
 
       // O^T += V^T P^T over these keys in 32-key steps
-      pv_step<0, NDT, NSBW>(sacc, stg, voff, oacc[j]);
-      if constexpr (NSBW > 2) pv_step<1, NDT, NSBW>(sacc, stg, voff, oacc[j]);
-      if constexpr (NSBW > 4) {
-        pv_step<2, NDT, NSBW>(sacc, stg, voff, oacc[j]);
-        pv_step<3, NDT, NSBW>(sacc, stg, voff, oacc[j]);
+      if constexpr (vearly) {
+        pv_mma<0, NDT, NSBW>(sacc, vq[0], oacc[j]);
+        if constexpr (NSBW > 2) pv_mma<1, NDT, NSBW>(sacc, vq[NSBW > 2 ? 1 : 0], oacc[j]);
+      } else {
+        pv_step<0, NDT, NSBW>(sacc, stg, voff, oacc[j]);
+        if constexpr (NSBW > 2) pv_step<1, NDT, NSBW>(sacc, stg, voff, oacc[j]);
+        if constexpr (NSBW > 4) {
+          pv_step<2, NDT, NSBW>(sacc, stg, voff, oacc[j]);
+          pv_step<3, NDT, NSBW>(sacc, stg, voff, oacc[j]);
+        }
       }
     };
 

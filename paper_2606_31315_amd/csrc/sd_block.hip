@@ -67,7 +67,8 @@ constexpr int kBf16KT = SDB_BF16_KT, kBf16NS = SDB_BF16_NS;
 // ---------------------------------------------------------------------------
 struct AttnPlan {
   int G, KT, split_len, max_splits, Mpad, n_work, per_xcd, grid, dense, MT;
-  int bal;  // balanced shares for sd_block_attn (bf16, plain caches; see bal_share)
+  int bal;  // balanced shares (bf16; see bal_share)
+  int ve;   // bf16 with one m-tile per wavefront and blocks of 7-8 m-tiles: early V^T reads (VE)
   size_t off_ml, off_o, total;
 };
 
@@ -160,6 +161,7 @@ int attn_plan(const sd_attn_shape *sh, AttnPlan *p) {
   const int nmt = p->Mpad / 16;
   if (sh->dtype == SD_BF16) p->MT = nmt <= 8 ? 1 : 2;  // 8 wavefronts, 1 or 2 m-tiles each
   else p->MT = nmt <= 4 ? 1 : nmt <= 8 ? 2 : 4;      // 4 wavefronts
+  p->ve = sh->dtype == SD_BF16 && nmt >= 7 && nmt <= 8;
   size_t off = 0;
   p->off_ml = off;
   if (p->max_splits > 1) off = align256(off + (size_t)slots * p->Mpad * sizeof(float2));
@@ -176,9 +178,12 @@ void launch_attn(const sdb::AttnArgs &a, int grid, hipStream_t st) {
 
 // The balanced plan (bf16): kBalGrid workgroups, then the merge.
 template <int D, bool PAGED = false, bool APPEND = false>
-void launch_attn_bal(sdb::AttnArgs a, int MT, hipStream_t st) {
+void launch_attn_bal(sdb::AttnArgs a, int MT, hipStream_t st, bool ve) {
   a.bal = 1;
-  if (MT == 1)
+  if (ve)
+    hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 1, kBf16KT, kBf16NS, PAGED, APPEND, true, true>),
+                       dim3(a.bal_grid), dim3(512), 0, st, a);
+  else if (MT == 1)
     hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 1, kBf16KT, kBf16NS, PAGED, APPEND, true>), dim3(a.bal_grid),
                        dim3(512), 0, st, a);
   else
@@ -190,9 +195,12 @@ void launch_attn_bal(sdb::AttnArgs a, int MT, hipStream_t st) {
 }
 
 template <bool BF16, int D, bool PAGED = false, bool APPEND = false>
-void launch_attn_all(const sdb::AttnArgs &a, int grid, int MT, hipStream_t st) {
+void launch_attn_all(const sdb::AttnArgs &a, int grid, int MT, hipStream_t st, bool ve = false) {
   if constexpr (BF16) {
-    if (MT == 1)
+    if (ve)
+      hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 1, kBf16KT, kBf16NS, PAGED, APPEND, false, true>), dim3(grid),
+                         dim3(512), 0, st, a);
+    else if (MT == 1)
       hipLaunchKernelGGL((sdb::block_attn_bf16_kernel<D, 1, kBf16KT, kBf16NS, PAGED, APPEND>), dim3(grid), dim3(512), 0,
                          st, a);
     else
@@ -438,15 +446,15 @@ int sd_block_attn(const sd_attn_shape *sh, const void *q, const void *k_cache, c
   hipStream_t st = (hipStream_t)stream;
   const bool bf = sh->dtype == SD_BF16;
   if (p.bal) {
-    if (sh->head_dim == 128) launch_attn_bal<128>(a, p.MT, st);
-    else launch_attn_bal<64>(a, p.MT, st);
+    if (sh->head_dim == 128) launch_attn_bal<128>(a, p.MT, st, p.ve);
+    else launch_attn_bal<64>(a, p.MT, st, p.ve);
     return check_launch("sd_block_attn");
   }
   if (sh->head_dim == 128) {
-    if (bf) launch_attn_all<true, 128>(a, grid, p.MT, st);
+    if (bf) launch_attn_all<true, 128>(a, grid, p.MT, st, p.ve);
     else launch_attn_all<false, 128>(a, grid, p.MT, st);
   } else {
-    if (bf) launch_attn_all<true, 64>(a, grid, p.MT, st);
+    if (bf) launch_attn_all<true, 64>(a, grid, p.MT, st, p.ve);
     else launch_attn_all<false, 64>(a, grid, p.MT, st);
   }
   return check_launch("sd_block_attn");
@@ -474,12 +482,12 @@ int sd_block_attn_append(const sd_attn_shape *sh, const void *q, const void *k_n
   a.v_new = v_new;
   hipStream_t st = (hipStream_t)stream;
   if (p.bal) {
-    if (sh->head_dim == 128) launch_attn_bal<128, false, true>(a, p.MT, st);
-    else launch_attn_bal<64, false, true>(a, p.MT, st);
+    if (sh->head_dim == 128) launch_attn_bal<128, false, true>(a, p.MT, st, p.ve);
+    else launch_attn_bal<64, false, true>(a, p.MT, st, p.ve);
   } else if (sh->head_dim == 128) {
-    launch_attn_all<true, 128, false, true>(a, p.grid, p.MT, st);
+    launch_attn_all<true, 128, false, true>(a, p.grid, p.MT, st, p.ve);
   } else {
-    launch_attn_all<true, 64, false, true>(a, p.grid, p.MT, st);
+    launch_attn_all<true, 64, false, true>(a, p.grid, p.MT, st, p.ve);
   }
   return check_launch("sd_block_attn_append");
 }
@@ -525,12 +533,12 @@ int sd_block_attn_paged(const sd_attn_shape *sh, int32_t page_size, int32_t num_
   const int grid = p.grid;
   hipStream_t st = (hipStream_t)stream;
   if (p.bal) {
-    if (sh->head_dim == 128) launch_attn_bal<128, true>(a, p.MT, st);
-    else launch_attn_bal<64, true>(a, p.MT, st);
+    if (sh->head_dim == 128) launch_attn_bal<128, true>(a, p.MT, st, p.ve);
+    else launch_attn_bal<64, true>(a, p.MT, st, p.ve);
   } else if (sh->head_dim == 128) {
-    launch_attn_all<true, 128, true>(a, grid, p.MT, st);
+    launch_attn_all<true, 128, true>(a, grid, p.MT, st, p.ve);
   } else {
-    launch_attn_all<true, 64, true>(a, grid, p.MT, st);
+    launch_attn_all<true, 64, true>(a, grid, p.MT, st, p.ve);
   }
   return check_launch("sd_block_attn_paged");
 }
