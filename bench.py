@@ -457,7 +457,7 @@ def batched_us(torch, fn, n, nb=5):
     return out
 
 
-def other_configs_run(torch, sd, reps=20):
+def other_configs_run(torch, sd, reps=200):
     """The drafter pass (16 sequences, ctx U{1024..8192}, B U{8..32}, bidirectional) and the
     long-context serving step (32 sequences, ctx U{8192..32768}, B U{4..32}, causal attention,
     then acceptance at T = 1 over V = 151936), with the seeded lengths of those workloads and
@@ -469,7 +469,10 @@ def other_configs_run(torch, sd, reps=20):
     out = {"qwen3_4b_verify_S1_ctx2048_B16": c2_run(torch, sd)}
 
     def timed(fn, n):
-        fn()
+        # 20 untimed calls first: a GPU that has idled runs its first few milliseconds of work
+        # several percent slower while its clocks come back up
+        for i in range(20):
+            fn(i)
         torch.cuda.synchronize()
         t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         t0.record()
