@@ -45,7 +45,7 @@ def _take_block_rows(p):
     return k_new, v_new, kc, vc
 
 
-def _check(p):
+def _check(p, with_oracle=True):
     dev = G.dev()
     k_new, v_new, kc, vc = _take_block_rows(p)
     d = G.attn_to_device(p)
@@ -59,11 +59,12 @@ def _check(p):
         assert np.array_equal(got.float().cpu().numpy(), want.float().numpy(), equal_nan=True)
     o = out.float().cpu().numpy().astype(np.float64)
     assert np.isfinite(o).all(), "a poisoned cache row reached the output"
-    ref = oracle.block_attn(p.q, p.k_cache, p.v_cache, p.ctx_lens, p.block_lens, p.q_offsets, p.mask_mode,
-                            p.scale)
-    err = np.abs(o - ref).max() if o.size else 0.0
-    G.log(f"  max-abs error {err:.3e}")
-    assert err <= G.ATTN_TOL["bf16"]
+    if with_oracle:
+        ref = oracle.block_attn(p.q, p.k_cache, p.v_cache, p.ctx_lens, p.block_lens, p.q_offsets, p.mask_mode,
+                                p.scale)
+        err = np.abs(o - ref).max() if o.size else 0.0
+        G.log(f"  max-abs error {err:.3e}")
+        assert err <= G.ATTN_TOL["bf16"]
     two_call = G.run_attn(p, d)
     assert torch.equal(out.view(torch.int16), two_call.view(torch.int16)), "differs from sd_block_attn"
 

@@ -6,9 +6,13 @@ vocabularies, one-row blocks, every temperature path), within the documented lim
 (1 <= max_block <= 64, group size x max_block <= 256 query rows)."""
 import numpy as np
 import pytest
+import torch
 
 import gpu_util as G
+import oracle
+import paper_2606_31315_amd as sd
 from paper_2606_31315_amd import workloads as W
+from test_gpu_append import _check as append_check
 
 pytestmark = pytest.mark.gpu
 
@@ -103,3 +107,80 @@ def test_accept_random_shape(i):
     p = W.make_accept(rs, name=f"sweep{i}", **sh)
     G.log(f"  case {i}: B {sh['block_lens'].tolist()}")
     G.check_accept(p)
+
+
+# ---- the paged and fused-append variants on random shapes (bf16, as those calls require) ----
+N_VARIANTS = 16
+
+
+def _bf16(sh: dict) -> dict:
+    return dict(sh, dtype="bf16")
+
+
+def _pad_caches(p, page_size):
+    """The problem's caches padded with NaN keys to a whole number of pages."""
+    Lp = ((p.Lmax + page_size - 1) // page_size) * page_size
+    k = torch.nn.functional.pad(p.k_cache, (0, 0, 0, Lp - p.Lmax), value=float("nan"))
+    v = torch.nn.functional.pad(p.v_cache, (0, 0, 0, Lp - p.Lmax), value=float("nan"))
+    return k, v
+
+
+def _paged_against_contiguous(p, rs, page_size, with_oracle):
+    """sd_block_attn_paged over a shuffled page pool: bit-identical to sd_block_attn on the same
+    keys, and (with_oracle) within the bf16 tolerance of the oracle row by row."""
+    k, v = _pad_caches(p, page_size)
+    kp, vp, table = W.paginate(rs, k, v, page_size)
+    dev = G.dev()
+    G.log(f"sd_block_attn_paged {p.name} S={p.S} page={page_size} pages={kp.shape[0]} mask={p.mask_mode}")
+    got = sd.block_attn_paged(p.q.to(dev), kp.to(dev), vp.to(dev), torch.from_numpy(table).to(dev),
+                              torch.from_numpy(p.ctx_lens).to(dev), torch.from_numpy(p.block_lens).to(dev),
+                              torch.from_numpy(p.q_offsets).to(dev), p.mask_mode, max_ctx=p.max_ctx,
+                              max_block=p.max_block)
+    torch.cuda.synchronize()
+    d = G.attn_to_device(p)
+    d["k"], d["v"] = k.to(dev), v.to(dev)
+    ref = G.run_attn(p, d)
+    assert torch.equal(got.view(torch.int16), ref.view(torch.int16)), "paged output differs from contiguous"
+    if with_oracle:
+        o = got.float().cpu().numpy().astype(np.float64)
+        want = oracle.block_attn(p.q, p.k_cache, p.v_cache, p.ctx_lens, p.block_lens, p.q_offsets, p.mask_mode,
+                                 p.scale)
+        err = np.abs(o - want).max() if o.size else 0.0
+        G.log(f"  max-abs error {err:.3e}")
+        assert err <= G.ATTN_TOL["bf16"]
+
+
+@pytest.mark.parametrize("i", range(N_VARIANTS))
+def test_paged_random_shape(i):
+    sh = _bf16(attn_shape(200 + i))
+    rs = W._streams(81000 + i)
+    p = W.make_attn(rs, name=f"paged_sweep{i}", **sh)
+    page_size = int(np.random.default_rng(71000 + i).choice([16, 32, 64, 128, 256, 1024]))
+    _paged_against_contiguous(p, rs, page_size, with_oracle=True)
+
+
+@pytest.mark.parametrize("i", range(4))
+def test_paged_random_multiwave(i):
+    sh = _bf16(waves_shape(100 + i))
+    rs = W._streams(86000 + i)
+    p = W.make_attn(rs, name=f"paged_waves{i}", **sh)
+    page_size = int(np.random.default_rng(76000 + i).choice([16, 64, 256]))
+    _paged_against_contiguous(p, rs, page_size, with_oracle=False)
+
+
+@pytest.mark.parametrize("i", range(N_VARIANTS))
+def test_append_random_shape(i):
+    """sd_block_attn_append: caches bit-exact, output within tolerance of the oracle and
+    bit-identical to sd_block_attn (the fused-append checks of the named cases)."""
+    sh = _bf16(attn_shape(300 + i))
+    rs = W._streams(82000 + i)
+    p = W.make_attn(rs, name=f"append_sweep{i}", **sh)
+    append_check(p)
+
+
+@pytest.mark.parametrize("i", range(4))
+def test_append_random_multiwave(i):
+    sh = _bf16(waves_shape(200 + i))
+    rs = W._streams(87000 + i)
+    p = W.make_attn(rs, name=f"append_waves{i}", **sh)
+    append_check(p, with_oracle=False)
