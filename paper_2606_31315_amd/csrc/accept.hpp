@@ -76,9 +76,18 @@ struct AcceptArgs {
   int spin_limit;            // polls before a waiting workgroup gives up
   // Single-launch draw (accept_draw_kernel, T > 0): the residual and p mass sums of every
   // sampling chunk (floats) as tagged words, word k (0 residual, 1 p) carrying tag + k * kTagStep,
-  // at index (s * 2 + k) * nch2 + chunk.
+  // in kSumReplicas copies, at index ((s * kSumReplicas + r) * 2 + k) * nch2 + chunk.
   unsigned long long *csum;
 };
+
+// Copies of the draw kernel's chunk sums: the workgroups of chunk c poll copy c mod
+// kSumReplicas, so each cache line of sums serves a few pollers instead of all of a sequence's
+// (ragged Qwen3-4B batch at T = 1, 75 chunks per row: sd_accept 22.76 us with one copy, 21.96
+// with 16; 22.07 with 8, 21.99 with 32).
+#ifndef SDB_SUM_REPLICAS
+#define SDB_SUM_REPLICAS 16
+#endif
+constexpr int kSumReplicas = SDB_SUM_REPLICAS;
 
 // ---- tagged words: one relaxed 64-bit atomic store or load at agent scope each ----
 // A relaxed atomic access is single-copy atomic and coherent across the XCDs' L2 caches, so
@@ -1130,10 +1139,10 @@ __global__ __launch_bounds__(256, 4) void accept_fused_kernel(AcceptArgs a) {
 // 22.7 us with one round at a time, since every extra load lands on the lines the sequence's
 // other workgroups poll.)
 template <int P>
-__device__ __forceinline__ bool poll_chunk_sums(const AcceptArgs &a, int s, double2 (&cm)[kLocSums]) {
+__device__ __forceinline__ bool poll_chunk_sums(const AcceptArgs &a, int s, int copy, double2 (&cm)[kLocSums]) {
   static_assert(P >= 1 && P <= kLocSums, "chunk sums held in registers");
   const int lane = threadIdx.x & 63;
-  const unsigned long long *base = a.csum + (size_t)s * 2 * a.nch2;
+  const unsigned long long *base = a.csum + (size_t)(s * kSumReplicas + copy) * 2 * a.nch2;
   float r[P], pm[P];
   unsigned miss = 0u;
 #pragma unroll
@@ -1175,13 +1184,13 @@ __device__ __forceinline__ bool poll_chunk_sums(const AcceptArgs &a, int s, doub
   return ok;
 }
 
-__device__ __forceinline__ bool poll_chunk_sums_n(const AcceptArgs &a, int s, double2 (&cm)[kLocSums]) {
+__device__ __forceinline__ bool poll_chunk_sums_n(const AcceptArgs &a, int s, int copy, double2 (&cm)[kLocSums]) {
   static_assert(kLocSums == 4, "one case per pass count");
   switch ((a.nch2 + 63) / 64) {
-    case 1: return poll_chunk_sums<1>(a, s, cm);
-    case 2: return poll_chunk_sums<2>(a, s, cm);
-    case 3: return poll_chunk_sums<3>(a, s, cm);
-    default: return poll_chunk_sums<4>(a, s, cm);
+    case 1: return poll_chunk_sums<1>(a, s, copy, cm);
+    case 2: return poll_chunk_sums<2>(a, s, copy, cm);
+    case 3: return poll_chunk_sums<3>(a, s, copy, cm);
+    default: return poll_chunk_sums<4>(a, s, copy, cm);
   }
 }
 
@@ -1265,11 +1274,12 @@ __global__ __launch_bounds__(256, 4) void accept_draw_kernel(AcceptArgs a) {
   const float wr = wave_sum_f(sr), wp = wave_sum_f(spm);
   if (lane == 0) { sh_r[wave] = wr; sh_p[wave] = wp; }
   __syncthreads();
-  if (tid == 0) {  // the chunk's sums, rounded to float as accept_mass_kernel files them
+  if (tid < 2 * kSumReplicas) {  // the chunk's sums, rounded to float as accept_mass_kernel files
+    // them; one word of one copy per lane
     const float cr = (float)(sh_r[0] + sh_r[1] + sh_r[2] + sh_r[3]), cp = (float)(sh_p[0] + sh_p[1] + sh_p[2] + sh_p[3]);
-    unsigned long long *w = a.csum + (size_t)s * 2 * a.nch2 + c;
-    tag_put(w, a.tag, __float_as_uint(cr));
-    tag_put(w + a.nch2, a.tag + kTagStep, __float_as_uint(cp));
+    const int k = tid & 1, r = tid >> 1;
+    tag_put(a.csum + ((size_t)(s * kSumReplicas + r) * 2 + k) * a.nch2 + c, a.tag + (unsigned)k * kTagStep,
+            __float_as_uint(k ? cp : cr));
   }
 
   // ---- the chunk's scan, ahead of the chunk search: accept_locate_kernel's run masses
@@ -1317,7 +1327,7 @@ __global__ __launch_bounds__(256, 4) void accept_draw_kernel(AcceptArgs a) {
   // ---- every chunk sum of the sequence, then the chunk search ----
   if (wave == 0) {
     double2 cm[kLocSums];
-    const bool ok = poll_chunk_sums_n(a, s, cm);
+    const bool ok = poll_chunk_sums_n(a, s, c % kSumReplicas, cm);
     if (ok) {
       const ChunkPick cp = chunk_search([&](int k) { return pick_sums(cm, k); }, (a.nch2 + 63) / 64,
                                         (double)si1.z);

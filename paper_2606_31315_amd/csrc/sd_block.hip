@@ -302,7 +302,8 @@ int accept_plan(const sd_accept_shape *sh, float temperature, AcceptPlan *p) {
   // wavefront holds in registers
   p->draw_ok = sample && S >= 1 && !tail_wide && nch2 <= 64LL * sdb::kLocSums && (long long)S * nch2 <= INT_MAX;
   p->off_draw = p->total;
-  p->total_draw = p->draw_ok ? p->total + align256((size_t)S * 2 * nch2 * sizeof(unsigned long long)) : 0;
+  p->total_draw =
+      p->draw_ok ? p->total + align256((size_t)S * sdb::kSumReplicas * 2 * nch2 * sizeof(unsigned long long)) : 0;
   return ok();
 }
 
