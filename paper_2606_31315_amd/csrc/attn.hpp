@@ -232,14 +232,18 @@ __device__ __forceinline__ bool attn_item(const AttnArgs &a, int b, AttnItem &it
 #ifndef SDB_BAL_WEIGHTS
 #define SDB_BAL_WEIGHTS 1
 #endif
-// Relative time of one key tile by the block's m-tiles (16-row query tiles): the split kernel
-// streams a tile in about 1.25 us up to 3 m-tiles; beyond that the wavefronts' LDS reads and
-// arithmetic set the pace (8 sequences x 8 kv heads, contexts 4096, one wave, MI355X: 1.24 us
-// per tile at 1-3 m-tiles, 1.43 at 4, 1.57 at 5, 1.74 at 6, 2.0 at 7, 2.05 at 8).
+// Relative time of one key tile by the block's m-tiles (16-row query tiles): up to 3 m-tiles
+// the split kernel streams a tile at the memory's pace; beyond that the wavefronts' LDS reads
+// and arithmetic add to it (8 sequences x 8 kv heads, contexts 4096, one wave, MI355X: 33.1 us
+// per call at 2 m-tiles, 33.7 at 3, 34.5 at 4, 35.5 at 5, 37.9 at 6, 40.0 at 7, 41.6 at 8).
+// Chosen by A/B on the multi-wave batches: against the steeper table measured before the
+// kernel's lane swaps (20, 23, 25, 28, 32, 33 for 1-3 ... 8 m-tiles), 16 sequences with contexts
+// 1k-8k 82.75 -> 81.14 us per call, 32 sequences with contexts 8k-32k 472.9 -> 452.1 us.
+constexpr int kBalWeightMax8 = 31;  // the weight at 8 m-tiles; 4 more per m-tile past 8
 __device__ __forceinline__ int bal_weight(int nmt) {
   if (!SDB_BAL_WEIGHTS) return 1;
-  constexpr int kw[9] = {20, 20, 20, 20, 23, 25, 28, 32, 33};
-  return nmt <= 8 ? kw[nmt] : 33 + 4 * (nmt - 8);
+  constexpr int kw[9] = {20, 20, 20, 20, 22, 24, 26, 29, kBalWeightMax8};
+  return nmt <= 8 ? kw[nmt] : kBalWeightMax8 + 4 * (nmt - 8);
 }
 
 struct BalShare {

@@ -152,9 +152,9 @@ int attn_plan(const sd_attn_shape *sh, AttnPlan *p) {
   // fused-append calls alike.  Partial slots: one per workgroup and pair a share touches, at
   // most kBalGrid + pairs.
   p->bal = sh->dtype == SD_BF16 && p->dense && p->max_splits > 1;
-  {  // the device sums tile weights (at most 33 + 4 per m-tile past 8) in 32-bit integers
+  {  // the device sums tile weights (at most kBalWeightMax8 + 4 per m-tile past 8) in 32-bit integers
     const long long nmt_max = (G * (long long)sh->max_block + 15) / 16;
-    const long long wmax = 33 + 4 * std::max(0LL, nmt_max - 8);
+    const long long wmax = sdb::kBalWeightMax8 + 4 * std::max(0LL, nmt_max - 8);
     if (pairs * ((max_L + kBf16KT - 1) / kBf16KT) * wmax > (1LL << 30)) p->bal = 0;
   }
   const long long slots = p->bal ? std::max(nw, (long long)kBalGrid + pairs) : nw;
