@@ -88,6 +88,7 @@ struct AcceptArgs {
 #define SDB_SUM_REPLICAS 16
 #endif
 constexpr int kSumReplicas = SDB_SUM_REPLICAS;
+static_assert(kSumReplicas >= 1 && 2 * kSumReplicas <= 256, "one word of one copy per thread of the filing workgroup");
 
 // ---- tagged words: one relaxed 64-bit atomic store or load at agent scope each ----
 // A relaxed atomic access is single-copy atomic and coherent across the XCDs' L2 caches, so
@@ -322,7 +323,7 @@ __device__ __forceinline__ void stats_process(const AcceptArgs &a, StatsItem<kSt
   auto reduce = [&]() {
     if constexpr (SAMPLE) {
       // One pass over the elements, each unpacked once: a running (m, sum of exp2((x - m) c))
-      // per thread, folded a group of SDB_STATS_GROUP vectors at a time -- the group's maximum by v_max3,
+      // per thread, folded SDB_STATS_GROUP vectors at a time -- the group's maximum by v_max3,
       // one rescale of the running sum when the maximum moved, then exp2 per element.  About
       // five VALU instructions per element (unpack, max3/2, fma, exp2, add) against ten for a
       // max pass and an exp pass that each unpack.

@@ -444,7 +444,7 @@ __global__ __launch_bounds__(512) void block_attn_bf16_kernel(AttnArgs a) {
         // Every K operand of the tile is read first, then each step's products follow a counted
         // wait for that step's reads only, so the LDS latency is exposed once per tile rather
         // than once per step (the compiler's own schedule waited for all reads in flight before
-        // each group of products).  Ragged Qwen3-4B batch: 33.53 -> 33.31 us per call; not for
+        // each group of products).  Ragged Qwen3-4B batch: 33.43 -> 33.21 us per call; not for
         // two m-tiles per wavefront, whose register budget would spill.
         bf16x8 kf[NST][NSBW];
   #pragma unroll
