@@ -184,3 +184,19 @@ def test_append_random_multiwave(i):
     rs = W._streams(87000 + i)
     p = W.make_attn(rs, name=f"append_waves{i}", **sh)
     append_check(p, with_oracle=False)
+
+
+N_EXTREME = 12
+
+
+@pytest.mark.parametrize("i", range(N_EXTREME))
+def test_accept_extreme_temperature(i):
+    """Very low and very high temperatures: near-one-hot and near-flat distributions (exp2
+    arguments far below zero, and sums over almost the whole vocabulary)."""
+    r = np.random.default_rng(99000 + i)
+    sh = accept_shape(300 + i)
+    sh["temperature"] = float(r.choice([0.02, 0.1, 4.0, 20.0]))
+    rs = W._streams(96000 + i)
+    p = W.make_accept(rs, name=f"extreme{i}", **sh)
+    G.log(f"  case {i}: T {sh['temperature']} V {sh['V']} B {sh['block_lens'].tolist()}")
+    G.check_accept(p)
