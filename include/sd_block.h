@@ -171,7 +171,8 @@ int sd_accept_workspace_size(const sd_accept_shape *shape, float temperature, si
  *   target_logits [total_q, V]       row q_offsets[s] + i: target logits after block position i
  *   draft_logits  [total_q - S, V]   row q_offsets[s] - s + j: drafter logits for block position
  *                                    j + 1, j < B_s - 1 (read only when temperature > 0; may be NULL
- *                                    at temperature 0)
+ *                                    at temperature 0, or when every block holds only its anchor,
+ *                                    total_q = S)
  *   draft_tokens  [total_q - S] int32  drafted token of block position j + 1, in [0, V) (a token
  *                                    outside that range is never accepted)
  *   uniforms      [total_q] fp32 in [0, 1): slot q_offsets[s] + j drives acceptance test j;

@@ -601,9 +601,11 @@ int check_accept_call(const sd_accept_shape *sh, const void *target_logits, cons
   if (!target_logits || !block_lens || !q_offsets || !accept_len || !next_token || !workspace)
     return fail(SD_ERR_INVALID_ARG, "sd_accept: NULL pointer argument");
   if (sh->total_q > sh->num_seqs && !draft_tokens) return fail(SD_ERR_INVALID_ARG, "draft_tokens is NULL");
-  if (sample && (!draft_logits || !uniforms))
-    return fail(SD_ERR_INVALID_ARG, "draft_logits and uniforms are required when temperature > 0");
-  if (!aligned16(target_logits) || (sample && !aligned16(draft_logits)))
+  // draft rows exist only where some block holds a drafted token (total_q > S)
+  const bool drafts = sh->total_q > sh->num_seqs;
+  if (sample && ((drafts && !draft_logits) || !uniforms))
+    return fail(SD_ERR_INVALID_ARG, "draft_logits (when total_q > num_seqs) and uniforms are required when temperature > 0");
+  if (!aligned16(target_logits) || (sample && drafts && !aligned16(draft_logits)))
     return fail(SD_ERR_INVALID_ARG, "logits must be 16-byte aligned");
   if (((uintptr_t)workspace & 255u) != 0) return fail(SD_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
   if (workspace_bytes < p->total)

@@ -98,6 +98,18 @@ def test_identical_draft_accepts_everything():
     assert (al == bl - 1).all()
 
 
+@pytest.mark.parametrize("T", [0.0, 1.0])
+def test_every_block_only_its_anchor(T):
+    """Blocks of one token everywhere: no drafted token and no draft row (total_q = S), so the
+    call takes an empty draft_logits and the draw at T > 0 is the bonus draw from each target row."""
+    rs = W._streams(4321)
+    p = W.make_accept(rs, block_lens=np.ones(12, np.int32), V=151936, dtype="bf16", temperature=T,
+                      target_sigma=3.0, noise_sigma=1.0, name="anchors_only")
+    assert p.total_q == p.S
+    al, nt, ref = G.check_accept(p)
+    assert (al == 0).all()
+
+
 def test_temperature_two():
     rs = W._streams(32)
     bl = np.array([10, 14, 4, 20], dtype=np.int32)
