@@ -148,7 +148,9 @@ def oracle_accept(p: AcceptProblem):
 
 def sample_tie_bound(ref, compared_mask) -> float:
     """Largest admissible count of final-draw near-ties among the compared sequences."""
-    ps = np.asarray(ref.sample_tie_p, dtype=np.float64)[compared_mask]
+    # each is a probability: where every interval is narrower than the band the oracle's sum of the
+    # masses can round a few ulps above one, which would make the variance term negative
+    ps = np.clip(np.asarray(ref.sample_tie_p, dtype=np.float64)[compared_mask], 0.0, 1.0)
     return float(ps.sum() + 4.0 * np.sqrt((ps * (1.0 - ps)).sum()) + 1.0)
 
 
