@@ -86,12 +86,16 @@ def test_commit_exact():
     assert ctx.cpu().tolist() == list(OS.commit([0, 5, 4000, 7], [0, 3, 23, 1]))
 
 
-def _run_steps(T, steps, seed, layers=2, dtype="bf16"):
+def _run_steps(T, steps, seed, layers=2, dtype="bf16", shape=None, mask=W.MASK_CAUSAL_IN_BLOCK):
+    """`steps` verify steps of `layers` layers, each checked against the oracle's step; `shape`
+    (Hq, Hkv, D, V, block_lens, ctx_lens) replaces the default four-sequence batch."""
     rs = W._streams(seed)
-    S, Hq, Hkv, D, V = 4, 32, 8, 128, 32000
-    B = np.array([12, 16, 5, 24], np.int32)
+    sh = shape or dict(Hq=32, Hkv=8, D=128, V=32000, block_lens=[12, 16, 5, 24], ctx_lens=[1500, 3000, 40, 2200])
+    Hq, Hkv, D, V = sh["Hq"], sh["Hkv"], sh["D"], sh["V"]
+    B = np.asarray(sh["block_lens"], np.int32)
+    S = len(B)
     off = W.offsets_from_lens(B)
-    ctx = np.array([1500, 3000, 40, 2200], np.int32)
+    ctx = np.asarray(sh["ctx_lens"], np.int32)
     Lmax = int(ctx.max() + steps * B.max())
     caches = [W.step_caches(rs, S=S, Hkv=Hkv, D=D, Lmax=Lmax, ctx_lens=ctx, dtype=dtype) for _ in range(layers)]
     dev = G.dev()
@@ -109,12 +113,12 @@ def _run_steps(T, steps, seed, layers=2, dtype="bf16"):
                            v_cache=dv, out=torch.empty_like(b["q"], device=dev)))
         da = G.accept_to_device(acc)
         G.log(f"sd_verify_step step {step} T={T} layers={layers} max_ctx={max_ctx}")
-        al, nt = sd.verify_step(dl, d_ctx, d_bl, d_off, W.MASK_CAUSAL_IN_BLOCK, da["t"], da["d"], da["tok"], da["u"],
+        al, nt = sd.verify_step(dl, d_ctx, d_bl, d_off, mask, da["t"], da["d"], da["tok"], da["u"],
                                 T, max_ctx=max_ctx, max_block=int(B.max()))
         torch.cuda.synchronize()
         ol = [dict(q=b["q"], k_new=b["k_new"], v_new=b["v_new"], k_cache=k, v_cache=v)
               for (k, v), b in zip(caches, blks)]
-        ref = OS.verify_step(ol, ctx, B, off, W.MASK_CAUSAL_IN_BLOCK, acc.target, acc.draft, acc.draft_tokens,
+        ref = OS.verify_step(ol, ctx, B, off, mask, acc.target, acc.draft, acc.draft_tokens,
                              acc.uniforms, T, band=G.BAND)
         for l in range(layers):
             err = np.abs(dl[l]["out"].float().cpu().numpy() - ref.outs[l]).max()
@@ -146,3 +150,27 @@ def test_verify_step_fp32_two_steps():
     """fp32 caches and logits: the step appends with sd_kv_append and then attends (the fused
     append is bf16 only); outputs at the fp32 tolerance, caches bit-exact."""
     _run_steps(1.0, steps=2, seed=4203, dtype="f32")
+
+
+def step_shape(i: int) -> dict:
+    """Shape of verify-step case i (seeded; no arithmetic of the method)."""
+    r = np.random.default_rng(91000 + i)
+    S = int(r.integers(1, 9))
+    Hkv = int(r.choice([1, 2, 8]))
+    G_ = int(r.choice([1, 2, 4]))
+    B = r.integers(1, min(32, 256 // G_) + 1, size=S)
+    B[r.random(S) < 0.2] = 1
+    return dict(Hq=G_ * Hkv, Hkv=Hkv, D=int(r.choice([64, 128])), V=int(r.integers(1000, 60001)),
+                block_lens=B.tolist(), ctx_lens=r.integers(0, 3001, size=S).tolist(),
+                T=float(r.choice([0.0, 1.0])), dtype="f32" if r.random() < 0.25 else "bf16",
+                layers=int(r.integers(1, 4)),
+                mask=W.MASK_BIDIR_IN_BLOCK if r.random() < 0.4 else W.MASK_CAUSAL_IN_BLOCK)
+
+
+@pytest.mark.parametrize("i", range(8))
+def test_verify_step_random_shape(i):
+    """Seeded random batches through two multi-layer verify steps: group sizes, head dims,
+    vocabularies, masks, dtypes and one-token blocks mixed."""
+    sh = step_shape(i)
+    G.log(f"  case {i}: {sh}")
+    _run_steps(sh["T"], steps=2, seed=4300 + i, layers=sh["layers"], dtype=sh["dtype"], shape=sh, mask=sh["mask"])
