@@ -224,6 +224,7 @@ struct StatsItem {
   u32x4 v[NV];   // this thread's vectors (clamped loads; padding applied when processed)
   float xh, xt;  // head and tail element (or element tid of a tiny row)
   float uj;      // uniform of the position (target rows, T > 0)
+  float xd;      // T > 0: the drafted token's logit where this chunk holds it, else NaN
   int rec, tok;  // record index (-1: not recorded), drafted token or -1
   int c;         // chunk index
   int e0;        // row-relative element of the chunk's first whole vector
@@ -291,11 +292,27 @@ __device__ __forceinline__ void stats_issue(const AcceptArgs &a, int item, Stats
   }
   it.rec = (j >= 0 && j < a.mb) ? ((is_draft ? a.S : 0) + sq) * a.mb + j : -1;
   it.tok = tok;
+  // T > 0: the drafted token's logit by a scalar load of its own, in the chunk whose elements
+  // hold it (head and tail included), so that no lane's registers are searched for it and no
+  // wait on the vectors in flight comes before the arithmetic
+  it.xd = NAN;
+  if (SAMPLE && tok >= 0) {
+    const int cs = (it.c == 0) ? 0 : it.e0;
+    const int ce = last ? a.V : it.e0 + it.nvc * VEC;
+    if (tok >= cs && tok < ce) {
+      const unsigned long long e = a0 + (unsigned)tok;
+      if constexpr (BF16) {
+        const uint32_t w = ld_uniform(reinterpret_cast<const uint32_t *>(base), (long long)(e >> 1));
+        it.xd = __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+      } else {
+        it.xd = ld_uniform(reinterpret_cast<const float *>(base), (long long)e);
+      }
+    }
+  }
 }
 
 // Reduce one landed item to its record: T > 0 (max, sum of exp2((x - max) c)) with one
-// rescale per item, and the drafted token's logit taken from the register that holds it;
-// T = 0 (max, lowest index).
+// rescale per item, and the drafted token's logit as loaded at issue; T = 0 (max, lowest index).
 template <bool BF16, bool SAMPLE, bool VECS, bool FUSED = false>
 __device__ __forceinline__ void stats_process(const AcceptArgs &a, StatsItem<kStatsVecs> &it, float *sh_v,
                                               float *sh_s, int *sh_i) {
@@ -404,32 +421,11 @@ __device__ __forceinline__ void stats_process(const AcceptArgs &a, StatsItem<kSt
     }
   };
 
-  float xd = NAN;  // T > 0: the drafted token's logit, in the one thread holding it
-  if (SAMPLE && it.tok >= 0) {
-    const int t = it.tok;
-    if (hv && eh == t) xd = xh;
-    if (tv && et == t) xd = xt;
-    if (VECS) {
-      const int r = t - it.e0;  // element offset into the chunk's vectors
-      if (r >= 0 && r < it.nvc * VEC && ((r / VEC) & 255) == tid) {
-        const int ut = (r / VEC) >> 8, et2 = r % VEC;
-#pragma unroll
-        for (int u = 0; u < kStatsVecs; ++u)
-          if (u == ut) {
-            float x[VEC];
-            unpack<BF16>(it.v[u], x);
-#pragma unroll
-            for (int e = 0; e < VEC; ++e)
-              if (e == et2) xd = x[e];
-          }
-      }
-    }
-  }
+  float xd = it.xd;  // T > 0: uniform over the workgroup
 
   reduce();
   if constexpr (SAMPLE) {
     sum = wave_sum_f(sum);
-    xd = wave_max_f(xd);
   } else {
     // the wavefront's largest value (NaN never wins), then the lowest index holding it: the
     // argmax_merge order, by DPP lane moves instead of a butterfly of LDS shuffles
@@ -438,13 +434,12 @@ __device__ __forceinline__ void stats_process(const AcceptArgs &a, StatsItem<kSt
     bv = wmax;
   }
 
-  if (lane == 0) { sh_v[wave] = bv; sh_s[wave] = sum; sh_i[wave] = bi; if (SAMPLE) sh_v[4 + wave] = xd; }
+  if (lane == 0) { sh_v[wave] = bv; sh_s[wave] = sum; sh_i[wave] = bi; }
   __syncthreads();
   if (tid == 0) {
     for (int w2 = 1; w2 < 4; ++w2) {
       if constexpr (SAMPLE) {
         lse_merge(bv, sum, sh_v[w2], sh_s[w2], a.c);
-        xd = fmaxf(xd, sh_v[4 + w2]);
       } else {
         argmax_merge(bv, bi, sh_v[w2], sh_i[w2]);
       }

@@ -66,6 +66,25 @@ def test_large_vocab_shapes(V, dtype, S, bl_range, T):
     G.check_accept(p)
 
 
+@pytest.mark.parametrize("T", [1.0, 0.0])
+@pytest.mark.parametrize("V,dtype", [(151936, "bf16"), (150001, "bf16"), (131075, "f32")])
+def test_drafted_tokens_at_chunk_edges(V, dtype, T):
+    """Drafted tokens on the elements where a row's statistics chunks meet: the first and last
+    elements, the unaligned head and tail (odd vocabularies shift every row's vector boundary),
+    and the first and last elements of each chunk of whole vectors; each position's acceptance
+    test reads that token's logit."""
+    import dataclasses
+    p = _many_seq_problem(V + 17, 9, V, (8, 24), dtype, T, target_sigma=3.0, noise_sigma=0.3,
+                          name=f"edges_V{V}")
+    vec = 8 if dtype == "bf16" else 4
+    chunk = 256 * 16 * vec  # elements in a chunk of whole vectors
+    edges = [0, 1, 2, vec - 1, vec, vec + 1, V - 1, V - 2, V - vec, V - vec - 1]
+    for k in range(1, V // chunk + 1):
+        edges += [k * chunk + d for d in (-vec, -2, -1, 0, 1, 2, vec) if 0 <= k * chunk + d < V]
+    tokens = np.array([edges[i % len(edges)] for i in range(len(p.draft_tokens))], np.int32)
+    G.check_accept(dataclasses.replace(p, draft_tokens=tokens))
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_greedy_ties_lowest_index(dtype):
     """Integer-valued logits at V=151936: the maximum is tied in many rows, and across vocabulary
