@@ -394,16 +394,21 @@ def _accept_checks(target_logits, draft_logits, draft_tokens, uniforms, block_le
     _shape(draft_tokens, "draft_tokens", None)
     if draft_tokens.shape[0] < total_q - S:
         raise ValueError(f"draft_tokens has {draft_tokens.shape[0]} entries, needs total_q - S = {total_q - S}")
-    if temperature > 0:
+    # no draft row exists where every block holds only its anchor (total_q = S): then
+    # draft_logits may be None
+    need_draft = temperature > 0 and (draft_logits is not None or total_q > S)
+    if need_draft:
         _shape(draft_logits, "draft_logits", total_q - S, V)
+    if temperature > 0:
         _shape(uniforms, "uniforms", total_q)
     for name, t in (("accept_len", accept_len), ("next_token", next_token)):
         if t is not None:
             _shape(t, name, S)
     dev = target_logits.device
     _need(target_logits, "target_logits", device=dev)
-    if temperature > 0:
+    if need_draft:
         _need(draft_logits, "draft_logits", target_logits.dtype, dev)
+    if temperature > 0:
         _need(uniforms, "uniforms", torch.float32, dev)
     for name, t in (("draft_tokens", draft_tokens), ("block_lens", block_lens), ("q_offsets", q_offsets)):
         _need(t, name, torch.int32, dev)
@@ -573,8 +578,12 @@ def verify_step(layers, ctx_lens: torch.Tensor, block_lens: torch.Tensor, q_offs
     _shape(draft_tokens, "draft_tokens", None)
     if draft_tokens.shape[0] < total_q - S:
         raise ValueError(f"draft_tokens has {draft_tokens.shape[0]} entries, needs total_q - S = {total_q - S}")
-    if temperature > 0:
+    # no draft row exists where every block holds only its anchor (total_q = S): then
+    # draft_logits may be None
+    need_draft = temperature > 0 and (draft_logits is not None or total_q > S)
+    if need_draft:
         _shape(draft_logits, "draft_logits", total_q - S, V)
+    if temperature > 0:
         _shape(uniforms, "uniforms", total_q)
     for name, t in (("accept_len", accept_len), ("next_token", next_token)):
         if t is not None:

@@ -124,6 +124,11 @@ def call_accept(T=1.0, **over):
 def test_accept_shapes():
     expect_device_error(call_accept)
     expect_device_error(call_accept, T=0.0, draft_logits=None, uniforms=None)
+    # T > 0: the draft tensor may be left out only where no block holds a drafted token
+    expect_device_error(call_accept, target_logits=meta(S, V), draft_logits=None, draft_tokens=i32(0),
+                        uniforms=meta(S, dtype=torch.float32))
+    with pytest.raises(TypeError, match="draft_logits"):
+        call_accept(draft_logits=None)
     expect_shape_error(call_accept, "draft_logits", draft_logits=meta(TQ, V))       # one row per draft
     expect_shape_error(call_accept, "draft_logits", draft_logits=meta(TQ - S, V + 1))
     expect_shape_error(call_accept, "uniforms", uniforms=meta(TQ - 1, dtype=torch.float32))

@@ -5,6 +5,7 @@ import scipy.stats
 import torch
 
 import gpu_util as G
+import paper_2606_31315_amd as sd
 from paper_2606_31315_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
@@ -127,6 +128,11 @@ def test_every_block_only_its_anchor(T):
     assert p.total_q == p.S
     al, nt, ref = G.check_accept(p)
     assert (al == 0).all()
+    # the same call with no draft tensor at all
+    d = G.accept_to_device(p)
+    al2, nt2 = sd.accept(d["t"], None, d["tok"], d["u"], d["bl"], d["off"], T, max_block=p.max_block)
+    torch.cuda.synchronize()
+    assert np.array_equal(al2.cpu().numpy(), al) and np.array_equal(nt2.cpu().numpy(), nt)
 
 
 def test_temperature_two():
